@@ -1,0 +1,221 @@
+"""fp64 CPU oracle for paged decode attention -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  It shares no code with the HIP library
+(no kernels, headers, helpers or constants) and never calls it.
+
+What it computes.  The paper's kernel family (iv) (Method, "Principle-Driven
+LLM Kernel Generator") is single-token decode attention over a paged KV cache:
+an online-softmax pass over the cached keys and values of each sequence, split
+across workgroups and finished by a merge of the per-split results.  Split
+plus online softmax plus merge reaches, in exact arithmetic, plain softmax
+attention of one query row over the sequence's cached tokens, so
+:func:`attend` is that plain definition written out:
+
+    for sequence b with L_b cached tokens and query head h, with kv head
+    g = h // G (G = Hq / Hkv, consecutive query heads share a kv head),
+        k_t = K[page(b, t), t mod P, g, :],  v_t likewise,
+        page(b, t) = block_table[b, t // P],
+        s_t = sigma * <q[b, h, :], k_t>          (sigma = the fp32 scale)
+        w_t = exp(s_t - max s) / sum_u exp(s_u - max s)
+        out[b, h, :] = sum_t w_t v_t,   lse = max s + log sum_u exp(s_u - max s)
+
+with every bf16 input widened exactly to fp64 and all arithmetic in fp64.
+A sequence with L_b = 0 yields a zero row (lse = -inf).
+
+:func:`split_merge` follows the algorithm instead: per-chunk running max,
+denominator and unnormalised accumulator, then the log-sum-exp merge of the
+chunks.  It is pinned against :func:`attend` for arbitrary chunkings.
+
+Readings where the paper is silent (it prints no attention formula, page
+size, layout or tolerance): standard scaled dot-product softmax with no other
+mask than the length, KV pool layout [num_pages, P, Hkv, D], lengths that
+include the token appended for the current step, and zero output for an
+empty sequence.
+"""
+from __future__ import annotations
+
+import math
+from typing import Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+__all__ = ["bf16_to_f64", "attend", "attend_pairs", "weights", "split_merge",
+           "brute_force_tiny"]
+
+
+def bf16_to_f64(bits) -> np.ndarray:
+    """Exact value of bf16 bit patterns as float64 (bits are the top half of
+    an IEEE float32)."""
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def _sigma(scale) -> float:
+    # the kernel receives the scale as fp32; use exactly that number
+    return float(np.float32(scale))
+
+
+def _gather(cache_bits, block_table_row, length, page_size, g) -> np.ndarray:
+    """[L, D] fp64 rows of kv head g for tokens 0..L-1 of one sequence."""
+    t = np.arange(length)
+    pages = np.asarray(block_table_row)[t // page_size].astype(np.int64)
+    slots = t % page_size
+    return bf16_to_f64(cache_bits[pages, slots, g, :])
+
+
+def _one_group(q_bits, k_bits, v_bits, bt_row, length, page_size, g, group, sigma):
+    """Outputs [G, D] and lse [G] for kv head g of one sequence."""
+    d = q_bits.shape[-1]
+    if length == 0:
+        return np.zeros((group, d)), np.full(group, -np.inf), np.zeros((group, 0))
+    kt = _gather(k_bits, bt_row, length, page_size, g)
+    vt = _gather(v_bits, bt_row, length, page_size, g)
+    qg = bf16_to_f64(q_bits[g * group:(g + 1) * group, :])
+    s = sigma * (qg @ kt.T)                      # [G, L]
+    m = s.max(axis=1, keepdims=True)
+    e = np.exp(s - m)
+    den = e.sum(axis=1, keepdims=True)
+    w = e / den
+    return w @ vt, (m + np.log(den))[:, 0], w
+
+
+def attend(q, k_cache, v_cache, block_table, context_lens, scale):
+    """Plain fp64 decode attention over the whole batch.
+
+    q: uint16 [B, Hq, D]; k_cache, v_cache: uint16 [N, P, Hkv, D];
+    block_table: int [B, maxp]; context_lens: int [B]; scale: float.
+    Returns (out float64 [B, Hq, D], lse float64 [B, Hq]).
+    """
+    bsz, hq, d = q.shape
+    _, page_size, hkv, _ = k_cache.shape
+    group = hq // hkv
+    sigma = _sigma(scale)
+    out = np.zeros((bsz, hq, d))
+    lse = np.full((bsz, hq), -np.inf)
+    for b in range(bsz):
+        length = int(context_lens[b])
+        for g in range(hkv):
+            o, l_, _ = _one_group(q[b], k_cache, v_cache, block_table[b], length,
+                                  page_size, g, group, sigma)
+            out[b, g * group:(g + 1) * group] = o
+            lse[b, g * group:(g + 1) * group] = l_
+    return out, lse
+
+
+def attend_pairs(q, k_cache, v_cache, block_table, context_lens, scale,
+                 pairs: Iterable[Tuple[int, int]]):
+    """Same definition for selected (sequence b, kv head g) pairs only.
+
+    Returns {(b, g): (out [G, D], lse [G])}; used to check full-size runs on
+    sampled outputs.
+    """
+    hq = q.shape[1]
+    _, page_size, hkv, _ = k_cache.shape
+    group = hq // hkv
+    sigma = _sigma(scale)
+    res = {}
+    for b, g in pairs:
+        o, l_, _ = _one_group(q[b], k_cache, v_cache, block_table[b],
+                              int(context_lens[b]), page_size, g, group, sigma)
+        res[(int(b), int(g))] = (o, l_)
+    return res
+
+
+def weights(q, k_cache, block_table, context_lens, scale, b, h) -> np.ndarray:
+    """Softmax weights w_t (fp64, length L_b) of query head h of sequence b."""
+    hq = q.shape[1]
+    _, page_size, hkv, _ = k_cache.shape
+    group = hq // hkv
+    g = h // group
+    length = int(context_lens[b])
+    _, _, w = _one_group(q[b], k_cache, k_cache, block_table[b], length,
+                         page_size, g, group, _sigma(scale))
+    return w[h - g * group]
+
+
+def split_merge(q, k_cache, v_cache, block_table, context_lens, scale,
+                bounds: Sequence[Sequence[int]]):
+    """Split-then-merge form of the same attention, in fp64.
+
+    ``bounds[b]`` is an increasing list of token offsets 0 = c_0 <= c_1 <= ...
+    <= c_n = L_b; chunk j covers tokens [c_j, c_{j+1}) and may be empty.
+    Per chunk (and query head): m_j = max s, l_j = sum exp(s - m_j),
+    a_j = sum exp(s - m_j) v.  Merge: M = max over non-empty chunks of m_j,
+    out = sum_j exp(m_j - M) a_j / sum_j exp(m_j - M) l_j; empty chunks carry
+    no weight.  Returns out float64 [B, Hq, D].
+    """
+    bsz, hq, d = q.shape
+    _, page_size, hkv, _ = k_cache.shape
+    group = hq // hkv
+    sigma = _sigma(scale)
+    out = np.zeros((bsz, hq, d))
+    for b in range(bsz):
+        length = int(context_lens[b])
+        cuts = list(bounds[b])
+        assert cuts[0] == 0 and cuts[-1] == length and all(
+            x <= y for x, y in zip(cuts, cuts[1:]))
+        if length == 0:
+            continue
+        for g in range(hkv):
+            kt = _gather(k_cache, block_table[b], length, page_size, g)
+            vt = _gather(v_cache, block_table[b], length, page_size, g)
+            qg = bf16_to_f64(q[b, g * group:(g + 1) * group, :])
+            parts = []
+            for lo, hi in zip(cuts, cuts[1:]):
+                if hi == lo:
+                    continue
+                s = sigma * (qg @ kt[lo:hi].T)          # [G, n]
+                m = s.max(axis=1, keepdims=True)
+                e = np.exp(s - m)
+                parts.append((m[:, 0], e.sum(axis=1), e @ vt[lo:hi]))
+            big_m = np.max(np.stack([p[0] for p in parts]), axis=0)       # [G]
+            num = np.zeros((group, d))
+            den = np.zeros(group)
+            for m_j, l_j, a_j in parts:
+                f = np.exp(m_j - big_m)
+                num += f[:, None] * a_j
+                den += f * l_j
+            out[b, g * group:(g + 1) * group] = num / den[:, None]
+    return out
+
+
+def brute_force_tiny(q, k_cache, v_cache, block_table, context_lens, scale):
+    """Pure-Python loops with exactly rounded sums (math.fsum); for tiny
+    inputs only.  Returns a nested list out[b][h][d] of floats."""
+    bsz, hq, d = q.shape
+    _, page_size, hkv, _ = k_cache.shape
+    group = hq // hkv
+    sigma = _sigma(scale)
+    qf = bf16_to_f64(q)
+    kf = bf16_to_f64(k_cache)
+    vf = bf16_to_f64(v_cache)
+    result: List[List[List[float]]] = []
+    for b in range(bsz):
+        rows = []
+        length = int(context_lens[b])
+        for h in range(hq):
+            g = h // group
+            if length == 0:
+                rows.append([0.0] * d)
+                continue
+            scores = []
+            for t in range(length):
+                page = int(block_table[b][t // page_size])
+                slot = t % page_size
+                scores.append(sigma * math.fsum(
+                    float(qf[b, h, i]) * float(kf[page, slot, g, i]) for i in range(d)))
+            top = max(scores)
+            ex = [math.exp(s - top) for s in scores]
+            den = math.fsum(ex)
+            row = []
+            for i in range(d):
+                acc = []
+                for t in range(length):
+                    page = int(block_table[b][t // page_size])
+                    slot = t % page_size
+                    acc.append(ex[t] * float(vf[page, slot, g, i]))
+                row.append(math.fsum(acc) / den)
+            rows.append(row)
+        result.append(rows)
+    return result

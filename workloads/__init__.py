@@ -1,0 +1,300 @@
+"""Seeded synthetic inputs for paged decode attention.
+
+This module only builds inputs: bf16 bit patterns for q and the paged K/V
+pools, the per-sequence page tables and context lengths.  It holds none of
+the attention arithmetic, so both the fp64 oracle and the GPU path can be fed
+from it without sharing any of the method's code.
+
+Storage conventions (the contract of the library's entry point):
+
+* ``q``            uint16 bf16 bits, ``[B, Hq, D]`` contiguous.
+* ``k_cache``      uint16 bf16 bits, ``[num_pages, P, Hkv, D]`` contiguous.
+* ``v_cache``      same shape and layout as ``k_cache``.
+* ``block_table``  int32 ``[B, max_pages]``; row ``b`` lists the physical pages
+  of sequence ``b`` in token order.  Columns at or beyond ``ceil(L_b / P)`` are
+  filled with -1 (never valid page ids).
+* ``context_lens`` int32 ``[B]``; ``L_b`` counts every cached token of the
+  sequence, including the one appended for the current decode step.
+
+The paper's serving runtime keeps KV in fixed-size blocks of a shared pool
+(Method, "Kernel Customization and Multi-Request Adaptation") and advances each
+sequence length by one after the append (same section, the ``kv_append``
+paragraph).  Page size, layout and distributions are not printed in the paper;
+the five named workloads below are synthetic stand-ins shaped like the model
+families it evaluates (Experiments, Setup).
+
+Generation recipe, fixed for reproducibility: one ``numpy.random.Generator``
+(PCG64) per workload; draw order lengths -> pool permutation -> q -> K -> V.
+Normal deviates come from the inverse CDF of a uniform 16-bit draw: the draw
+i indexes a 65536-entry table whose entry is the standard-normal quantile at
+(i + 0.5) / 65536, times the requested standard deviation, rounded to bf16
+with round-to-nearest-even.  This is a bf16 N(0, std^2) sample with tails cut
+at about 4.2 std, and it is ~20x faster than float normals, which matters for
+the multi-GB pools.
+"""
+from __future__ import annotations
+
+import dataclasses
+import functools
+import math
+import statistics
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+BF16_NAN = np.uint16(0x7FC0)
+_CHUNK = 1 << 24  # values per draw call; part of the recipe (do not change)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (round-to-nearest-even), return uint16 bits.
+
+    Inputs here are finite normals; NaN/inf handling is not needed.
+    """
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    return (rounded >> np.uint32(16)).astype(np.uint16)
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to float32."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+@functools.lru_cache(maxsize=8)
+def _quantile_table(std: float) -> np.ndarray:
+    nd = statistics.NormalDist(0.0, 1.0)
+    z = np.array([nd.inv_cdf((i + 0.5) / 65536.0) for i in range(65536)], dtype=np.float64)
+    return f32_to_bf16_bits((z * std).astype(np.float32))
+
+
+def _normal_bf16(rng: np.random.Generator, shape, std: float = 1.0) -> np.ndarray:
+    table = _quantile_table(float(std))
+    n = int(np.prod(shape, dtype=np.int64))
+    out = np.empty(n, dtype=np.uint16)
+    for s in range(0, n, _CHUNK):
+        e = min(n, s + _CHUNK)
+        idx = rng.integers(0, 65536, size=e - s, dtype=np.uint16)
+        np.take(table, idx, out=out[s:e])
+    return out.reshape(shape)
+
+
+@dataclasses.dataclass(frozen=True)
+class Config:
+    """One synthetic decode-attention workload."""
+
+    name: str
+    batch: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    page_size: int
+    seed: int
+    lengths: str            # "fixed:<L>", "uniform:<lo>:<hi>", "zipf:<s>:<lo>:<hi>"
+    pool: str               # "perm:<pool_pages>", "exact", "holes:<frac>"
+    q_std: float = 1.0
+    description: str = ""
+
+    @property
+    def group(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+
+CONFIGS: Dict[str, Config] = {
+    "tiny": Config(
+        "tiny", 1, 8, 2, 64, 16, 0, "fixed:256", "perm:64",
+        description="batch 1, 8:2 heads (G=4), D=64, L=256, P=16, 16 pages "
+                    "drawn from a shuffled pool of 64"),
+    "llama8b": Config(
+        "llama8b", 1, 32, 8, 128, 16, 1, "fixed:4096", "perm:4096",
+        description="Llama-3-8B-shaped layer, batch 1, 32:8 heads, D=128, "
+                    "L=4096, P=16, 256 pages scattered over a 4096-page pool"),
+    "batched": Config(
+        "batched", 64, 32, 8, 128, 16, 2, "uniform:128:8192", "exact",
+        description="batch 64, 32:8 heads, D=128, L~U[128,8192], P=16, one "
+                    "shuffled pool sized to the total tokens"),
+    "long70b": Config(
+        "long70b", 4, 64, 8, 128, 16, 3, "fixed:131072", "exact", q_std=0.5,
+        description="70B-shaped long-context layer, batch 4, 64:8 heads (G=8), "
+                    "D=128, L=131072, P=16, shuffled pool, q~N(0,0.5^2)"),
+    "ragged": Config(
+        "ragged", 256, 40, 8, 128, 32, 4, "zipf:1.2:16:32768", "holes:0.1",
+        description="batch 256, 40:8 heads (G=5), D=128, L~Zipf(1.2) clipped "
+                    "to [16,32768] and never a multiple of 32, P=32, shuffled "
+                    "pool with 10% unused holes"),
+}
+CONFIG_ORDER = ["tiny", "llama8b", "batched", "long70b", "ragged"]
+
+
+@dataclasses.dataclass
+class Workload:
+    """Inputs of one paged decode-attention call (host numpy arrays)."""
+
+    q: np.ndarray             # uint16 [B, Hq, D]
+    k_cache: np.ndarray       # uint16 [N, P, Hkv, D]
+    v_cache: np.ndarray       # uint16 [N, P, Hkv, D]
+    block_table: np.ndarray   # int32 [B, maxp]
+    context_lens: np.ndarray  # int32 [B]
+    scale: np.float32
+    name: str = "custom"
+
+    @property
+    def batch(self) -> int:
+        return self.q.shape[0]
+
+    @property
+    def num_q_heads(self) -> int:
+        return self.q.shape[1]
+
+    @property
+    def head_dim(self) -> int:
+        return self.q.shape[2]
+
+    @property
+    def num_kv_heads(self) -> int:
+        return self.k_cache.shape[2]
+
+    @property
+    def page_size(self) -> int:
+        return self.k_cache.shape[1]
+
+    @property
+    def num_pages(self) -> int:
+        return self.k_cache.shape[0]
+
+    @property
+    def max_pages(self) -> int:
+        return self.block_table.shape[1]
+
+    def algorithmic_bytes(self) -> int:
+        """Bytes the operation must move at minimum: each cached K and V
+        element of the live tokens once (shared by the GQA group), q in, out
+        out, the used page ids and the lengths."""
+        lens = self.context_lens.astype(np.int64)
+        d, hkv, hq, b = self.head_dim, self.num_kv_heads, self.num_q_heads, self.batch
+        pages = int(np.sum((lens + self.page_size - 1) // self.page_size))
+        return int(4 * d * hkv * int(lens.sum()) + 2 * 2 * b * hq * d + 4 * pages + 4 * b)
+
+
+def _draw_lengths(cfg: Config, rng: np.random.Generator) -> np.ndarray:
+    kind, *args = cfg.lengths.split(":")
+    if kind == "fixed":
+        return np.full(cfg.batch, int(args[0]), dtype=np.int64)
+    if kind == "uniform":
+        lo, hi = int(args[0]), int(args[1])
+        return rng.integers(lo, hi + 1, size=cfg.batch, dtype=np.int64)
+    if kind == "zipf":
+        s, lo, hi = float(args[0]), int(args[1]), int(args[2])
+        lens = np.clip(rng.zipf(s, size=cfg.batch).astype(np.int64), lo, hi)
+        # every sequence ends in a partly filled page
+        lens = np.where(lens % cfg.page_size == 0, lens - 1, lens)
+        return lens
+    raise ValueError(f"unknown length spec {cfg.lengths!r}")
+
+
+def build(
+    lengths: Sequence[int],
+    num_q_heads: int,
+    num_kv_heads: int,
+    head_dim: int,
+    page_size: int,
+    seed: int,
+    *,
+    pool: str = "exact",
+    q_std: float = 1.0,
+    scale: Optional[float] = None,
+    poison: bool = True,
+    max_pages: Optional[int] = None,
+    name: str = "custom",
+    rng: Optional[np.random.Generator] = None,
+) -> Workload:
+    """Build a workload for explicit lengths.
+
+    ``pool``: ``"exact"`` (pool = pages needed, shuffled), ``"perm:<N>"``
+    (pool of N pages, the used ones drawn by a random permutation) or
+    ``"holes:<f>"`` (pool = ceil(needed / (1-f)), pages handed out in
+    sequence order from a random permutation, the rest unused).
+    With ``poison`` every pool slot that no live token uses (unused pages
+    and the tail slots of each last page) holds bf16 NaN.
+    """
+    if rng is None:
+        rng = np.random.Generator(np.random.PCG64(seed))
+    lens = np.asarray(lengths, dtype=np.int64)
+    b = lens.shape[0]
+    if num_q_heads % num_kv_heads:
+        raise ValueError("num_q_heads must be a multiple of num_kv_heads")
+    npages = (lens + page_size - 1) // page_size
+    need = int(npages.sum())
+    kind, *args = pool.split(":")
+    if kind == "exact":
+        n_pool = max(need, 1)
+    elif kind == "perm":
+        n_pool = int(args[0])
+    elif kind == "holes":
+        n_pool = max(int(math.ceil(need / (1.0 - float(args[0])))), 1)
+    else:
+        raise ValueError(f"unknown pool spec {pool!r}")
+    if n_pool < need:
+        raise ValueError("pool smaller than the pages needed")
+    perm = rng.permutation(n_pool).astype(np.int64)
+    maxp = int(npages.max()) if b else 0
+    if max_pages is not None:
+        if max_pages < maxp:
+            raise ValueError("max_pages below the longest sequence")
+        maxp = max_pages
+    maxp = max(maxp, 1)
+    bt = np.full((b, maxp), -1, dtype=np.int32)
+    cursor = 0
+    for i in range(b):
+        bt[i, : npages[i]] = perm[cursor: cursor + npages[i]]
+        cursor += int(npages[i])
+    q = _normal_bf16(rng, (b, num_q_heads, head_dim), q_std)
+    k = _normal_bf16(rng, (n_pool, page_size, num_kv_heads, head_dim))
+    v = _normal_bf16(rng, (n_pool, page_size, num_kv_heads, head_dim))
+    if poison:
+        used = np.zeros(n_pool, dtype=bool)
+        for i in range(b):
+            used[bt[i, : npages[i]]] = True
+            tail = int(lens[i] % page_size)
+            if tail:
+                last = bt[i, npages[i] - 1]
+                k[last, tail:] = BF16_NAN
+                v[last, tail:] = BF16_NAN
+        k[~used] = BF16_NAN
+        v[~used] = BF16_NAN
+    if scale is None:
+        scale = 1.0 / math.sqrt(head_dim)
+    return Workload(q=q, k_cache=k, v_cache=v, block_table=bt,
+                    context_lens=lens.astype(np.int32), scale=np.float32(scale), name=name)
+
+
+def make(name: str, *, poison: bool = True, seed: Optional[int] = None) -> Workload:
+    """Build one of the five named workloads with its fixed seed."""
+    cfg = CONFIGS[name]
+    rng = np.random.Generator(np.random.PCG64(cfg.seed if seed is None else seed))
+    lens = _draw_lengths(cfg, rng)
+    return build(lens, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.page_size,
+                 cfg.seed, pool=cfg.pool, q_std=cfg.q_std, poison=poison, name=name, rng=rng)
+
+
+def lengths_of(name: str, seed: Optional[int] = None) -> np.ndarray:
+    """The context lengths a named workload draws (cheap: no KV generated)."""
+    cfg = CONFIGS[name]
+    rng = np.random.Generator(np.random.PCG64(cfg.seed if seed is None else seed))
+    return _draw_lengths(cfg, rng)
+
+
+def permute_pages(w: Workload, seed: int) -> Workload:
+    """Move every physical page to a new slot of the pool and remap the page
+    table accordingly.  The logical KV of every sequence is unchanged."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    n = w.num_pages
+    new_of_old = rng.permutation(n)
+    k = np.empty_like(w.k_cache)
+    v = np.empty_like(w.v_cache)
+    k[new_of_old] = w.k_cache
+    v[new_of_old] = w.v_cache
+    bt = w.block_table.copy()
+    live = bt >= 0
+    bt[live] = new_of_old[bt[live]].astype(np.int32)
+    return dataclasses.replace(w, k_cache=k, v_cache=v, block_table=bt)
