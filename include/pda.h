@@ -1,0 +1,166 @@
+/*
+ * pda.h -- paged decode attention for AMD MI355X (gfx950), C ABI.
+ *
+ * The operation is the decode-attention body of the paper's kernel family
+ * (iv) (Method, "Principle-Driven LLM Kernel Generator"): one query token per
+ * sequence attends over that sequence's cached keys and values, which live in
+ * fixed-size pages of a shared pool addressed through a per-sequence page
+ * table (the paged KV cache of Method, "Kernel Customization and
+ * Multi-Request Adaptation").  The work is split along the context across
+ * many waves, each running an online softmax over its share, and the
+ * per-split results are merged with a log-sum-exp combination (the paper's
+ * "cross-CTA merging"; the appendix describes its hand-written reference as
+ * merging without a separate reduction kernel).
+ *
+ * For sequence b with L_b cached tokens and query head h (kv head
+ * g = h / G, G = num_q_heads / num_kv_heads):
+ *     s_t        = scale * <q[b,h,:], K[page(b,t), t % P, g, :]>
+ *     out[b,h,:] = sum_t softmax(s)_t * V[page(b,t), t % P, g, :]
+ *     page(b,t)  = block_table[b, t / P],   t = 0 .. L_b - 1
+ * L_b counts every cached token including the one appended for the current
+ * step (the paper advances the length by one after its KV append).  A
+ * sequence with L_b = 0 gets a zero output row.
+ *
+ * Arithmetic: bf16 inputs, fp32 accumulation (scores, running max and sum,
+ * the probability-times-value products via bf16 matrix cores with the
+ * probabilities rounded to bf16), bf16 round-to-nearest-even output.
+ *
+ * Memory: every pointer argument of paged_decode_attention is a DEVICE
+ * pointer on the current HIP device.  The caller allocates and owns all of
+ * them; the library never frees or retains them.  The library owns one
+ * internal workspace per (device, stream), grown on demand (see
+ * pda_workspace_reserve) and released by pda_release_workspaces.
+ *
+ * Errors: every entry point returns PDA_OK (0) or a PDA_ERR_* code and sets a
+ * thread-local message readable with pda_last_error().  Argument checks run
+ * before any HIP call; on an argument error nothing is launched and `out` is
+ * untouched.  Device-resident contents are not validated: page ids outside
+ * [0, num_pages) are clamped into range and lengths are clamped to
+ * [0, max_pages_per_seq * page_size], so bad contents give unspecified
+ * values but never an out-of-bounds access.
+ */
+#ifndef PDA_H
+#define PDA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PDA_VERSION 1
+
+enum pda_status {
+  PDA_OK = 0,
+  PDA_ERR_NULL = 1,        /* a required pointer is NULL                          */
+  PDA_ERR_SHAPE = 2,       /* a size is out of range or inconsistent              */
+  PDA_ERR_UNSUPPORTED = 3, /* valid but not implemented (head_dim, group, page)   */
+  PDA_ERR_SCALE = 4,       /* scale is not a finite number                        */
+  PDA_ERR_ALIGN = 5,       /* q, k_cache, v_cache or out not 16-byte aligned      */
+  PDA_ERR_HIP = 6          /* a HIP runtime call failed (message has the detail)  */
+};
+
+/* Supported set of this version. */
+#define PDA_MAX_BATCH 8192
+#define PDA_MAX_GROUP 16      /* num_q_heads / num_kv_heads                */
+#define PDA_MAX_PAGE_SIZE 1024
+
+/*
+ * paged_decode_attention -- the decode-attention step described above.
+ *
+ *   q            bf16 [batch, num_q_heads, head_dim], contiguous, 16-B aligned.
+ *   k_cache      bf16 [num_pages, page_size, num_kv_heads, head_dim],
+ *                contiguous, 16-B aligned (token-major pages; the kv heads of
+ *                one token are adjacent).
+ *   v_cache      same shape and layout as k_cache.
+ *   block_table  int32 [batch, max_pages_per_seq], row-major.  Only the first
+ *                ceil(L_b / page_size) entries of row b are read.
+ *   context_lens int32 [batch], on the device (no host read, so the call can
+ *                be captured in a HIP graph).
+ *   out          bf16 [batch, num_q_heads, head_dim], contiguous, 16-B
+ *                aligned; fully written on success.  Must not alias inputs.
+ *   head_dim     64 or 128.   page_size: a power of two in [1, 1024].
+ *   num_q_heads  a multiple of num_kv_heads, with group <= 16.
+ *   batch        0 .. 8192 (0 is a no-op).
+ *   scale        finite fp32 multiplier of the scores (usually 1/sqrt(D)).
+ *   stream       hipStream_t to launch on; NULL means the null stream.
+ *
+ * Asynchronous: returns after enqueueing; no host synchronisation.  Calls on
+ * one stream are ordered; calls on different streams use separate
+ * workspaces.  If the stream is being captured, the workspace must already
+ * be large enough (pda_workspace_reserve), otherwise PDA_ERR_HIP.
+ */
+int paged_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                           const int32_t* block_table, const int32_t* context_lens,
+                           void* out,
+                           int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                           int32_t head_dim, int32_t page_size, int32_t num_pages,
+                           int32_t max_pages_per_seq,
+                           float scale, void* stream);
+
+/*
+ * pda_plan -- host-only dry run of the split planner: how the context of the
+ * batch is spread over waves (the paper's split across CTAs, sized here to
+ * fill the given number of compute units).  No HIP call.
+ *   num_cus      compute units of the target device (256 on MI355X).
+ *   grid_blocks  out: workgroups of the split kernel.
+ *   waves        out: waves (workers) in that grid.
+ *   workspace_bytes out: device workspace the call needs for this shape.
+ * Returns PDA_OK or an argument error as paged_decode_attention would.
+ */
+int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+             int32_t page_size, int32_t max_pages_per_seq, int32_t num_cus,
+             int32_t* grid_blocks, int32_t* waves, int64_t* workspace_bytes);
+
+/*
+ * pda_workspace_reserve -- grow the workspace of (current device, stream) so
+ * that a later call with this shape allocates nothing (e.g. before graph
+ * capture).  Synchronous; may call hipMalloc.
+ */
+int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                          int32_t head_dim, int32_t page_size, int32_t max_pages_per_seq,
+                          void* stream);
+
+/* Free every workspace the library holds (synchronises their streams). */
+int pda_release_workspaces(void);
+
+/* Thread-local message of the last failing call on this thread ("" if none). */
+const char* pda_last_error(void);
+
+/* PDA_VERSION of the built library. */
+int32_t pda_version(void);
+
+/*
+ * Planner options (tuning and testing).  The split planner spreads the
+ * batch's context over min(num_cus * blocks_per_cu * 4 waves,
+ * ceil(total 32-token steps / min_steps)) waves.
+ *   PDA_OPT_BLOCKS_PER_CU  workgroups of 4 waves per compute unit, 1..8
+ *                          (default 2, env PDA_BLOCKS_PER_CU).
+ *   PDA_OPT_MIN_STEPS      fewest 32-token steps a wave is given, >= 1
+ *                          (default 2, env PDA_MIN_STEPS); a large value
+ *                          forces fewer splits, 1 the most.
+ * Options are process-wide and apply to later calls.  pda_set_option
+ * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
+ * returns the current value or -1 for an unknown option.
+ */
+#define PDA_OPT_BLOCKS_PER_CU 1
+#define PDA_OPT_MIN_STEPS 2
+int pda_set_option(int32_t option, int32_t value);
+int32_t pda_get_option(int32_t option);
+
+/*
+ * Kernel timing for measurement harnesses.  While enabled, every
+ * paged_decode_attention call records HIP events on its stream around each
+ * kernel it launches.  pda_profile_read synchronises those events, returns
+ * the summed milliseconds of the split kernel and of the merge kernel and
+ * the number of calls recorded since the last read, and clears the record.
+ */
+int pda_profile_enable(int32_t on);
+int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDA_H */

@@ -1,0 +1,172 @@
+"""ctypes binding of libpda.so (argument marshalling only).
+
+Every step of paged decode attention runs in the HIP kernels of the library;
+this module only checks tensor metadata, extracts device pointers and sizes
+and forwards them, with torch's current HIP stream, to the C ABI declared in
+include/pda.h.  There is no fallback: if the library cannot be loaded, every
+call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional, Tuple
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_lib", "libpda.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "pda.h")
+
+PDA_OK = 0
+ERRORS = {1: "PDA_ERR_NULL", 2: "PDA_ERR_SHAPE", 3: "PDA_ERR_UNSUPPORTED", 4: "PDA_ERR_SCALE",
+          5: "PDA_ERR_ALIGN", 6: "PDA_ERR_HIP"}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class PdaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def _declare(lib: ctypes.CDLL) -> None:
+    i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+    lib.paged_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp]
+    lib.paged_decode_attention.restype = ctypes.c_int
+    lib.pda_plan.argtypes = [i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32),
+                             ctypes.POINTER(i64)]
+    lib.pda_plan.restype = ctypes.c_int
+    lib.pda_workspace_reserve.argtypes = [i32, i32, i32, i32, i32, i32, vp]
+    lib.pda_workspace_reserve.restype = ctypes.c_int
+    lib.pda_release_workspaces.argtypes = []
+    lib.pda_release_workspaces.restype = ctypes.c_int
+    lib.pda_last_error.argtypes = []
+    lib.pda_last_error.restype = ctypes.c_char_p
+    lib.pda_version.argtypes = []
+    lib.pda_version.restype = i32
+    lib.pda_set_option.argtypes = [i32, i32]
+    lib.pda_set_option.restype = ctypes.c_int
+    lib.pda_get_option.argtypes = [i32]
+    lib.pda_get_option.restype = i32
+    lib.pda_profile_enable.argtypes = [i32]
+    lib.pda_profile_enable.restype = ctypes.c_int
+    lib.pda_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(i64)]
+    lib.pda_profile_read.restype = ctypes.c_int
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the built library (raises if it is missing: build it first with
+    ``python -m paper_2606_07665_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise RuntimeError(f"HIP library not built: {path} is missing "
+                               "(run python -m paper_2606_07665_amd.build)")
+        lib = ctypes.CDLL(path)
+        _declare(lib)
+        _lib = lib
+    return _lib
+
+
+def declared_symbols(header: str = HEADER):
+    """Function names declared in include/pda.h."""
+    text = open(header).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b([a-z_][a-z0-9_]*)\s*\(", text, flags=re.M)))
+
+
+def _check(rc: int) -> None:
+    if rc != PDA_OK:
+        raise PdaError(rc, load().pda_last_error().decode())
+
+
+def last_error() -> str:
+    return load().pda_last_error().decode()
+
+
+def version() -> int:
+    return int(load().pda_version())
+
+
+def raw_call(q_ptr, k_ptr, v_ptr, bt_ptr, lens_ptr, out_ptr, batch, hq, hkv, d, page_size, num_pages,
+             max_pages, scale, stream_ptr=None) -> int:
+    """Direct C call with integer pointers; returns the status code."""
+    return load().paged_decode_attention(q_ptr, k_ptr, v_ptr, bt_ptr, lens_ptr, out_ptr, batch, hq, hkv, d,
+                                         page_size, num_pages, max_pages, ctypes.c_float(scale), stream_ptr)
+
+
+def _stream_ptr(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
+    """out[b, h] = softmax(scale * q[b, h] . K_b^T) V_b over the paged cache.
+
+    q, out: bf16 [B, Hq, D]; k_cache, v_cache: bf16 [N, P, Hkv, D];
+    block_table: int32 [B, maxp]; context_lens: int32 [B]; all contiguous on
+    one GPU.  Launches on ``stream`` (default: torch's current stream).
+    """
+    import torch
+    for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
+                        ("v_cache", v_cache, torch.bfloat16), ("out", out, torch.bfloat16),
+                        ("block_table", block_table, torch.int32), ("context_lens", context_lens, torch.int32)):
+        if t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if q.dim() != 3 or k_cache.dim() != 4 or v_cache.shape != k_cache.shape or out.shape != q.shape:
+        raise ValueError("shapes: q/out [B,Hq,D], k_cache/v_cache [N,P,Hkv,D]")
+    b, hq, d = q.shape
+    n, p, hkv, d2 = k_cache.shape
+    if d2 != d or block_table.dim() != 2 or block_table.shape[0] != b or context_lens.shape != (b,):
+        raise ValueError("inconsistent shapes between q, caches, block_table and context_lens")
+    _check(raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+                    context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1],
+                    float(scale), _stream_ptr(stream)))
+    return out
+
+
+def plan(batch, hq, hkv, d, page_size, max_pages, num_cus=256) -> Tuple[int, int, int]:
+    """(grid blocks, waves, workspace bytes) the split planner picks."""
+    g, w, ws = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int64()
+    _check(load().pda_plan(batch, hq, hkv, d, page_size, max_pages, num_cus,
+                           ctypes.byref(g), ctypes.byref(w), ctypes.byref(ws)))
+    return g.value, w.value, ws.value
+
+
+def workspace_reserve(batch, hq, hkv, d, page_size, max_pages, stream=None) -> None:
+    _check(load().pda_workspace_reserve(batch, hq, hkv, d, page_size, max_pages, _stream_ptr(stream)))
+
+
+def release_workspaces() -> None:
+    _check(load().pda_release_workspaces())
+
+
+OPT_BLOCKS_PER_CU = 1
+OPT_MIN_STEPS = 2
+
+
+def set_option(option: int, value: int) -> None:
+    _check(load().pda_set_option(option, value))
+
+
+def get_option(option: int) -> int:
+    return int(load().pda_get_option(option))
+
+
+def profile_enable(on: bool = True) -> None:
+    _check(load().pda_profile_enable(1 if on else 0))
+
+
+def profile_read() -> Tuple[float, float, int]:
+    """(split kernel ms, merge kernel ms, calls) summed since the last read."""
+    s, m, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+    _check(load().pda_profile_read(ctypes.byref(s), ctypes.byref(m), ctypes.byref(n)))
+    return s.value, m.value, n.value

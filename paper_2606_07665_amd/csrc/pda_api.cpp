@@ -1,0 +1,387 @@
+// C-ABI host side of the paged decode attention library: argument checks
+// (before any HIP call), the split planner, per-(device, stream) workspaces
+// and optional event timing.  The kernels live in pda_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "pda.h"
+#include "pda_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(PDA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+int env_int(const char* name, int dflt, int lo, int hi) {
+  const char* s = std::getenv(name);
+  if (!s || !*s) return dflt;
+  long v = std::strtol(s, nullptr, 10);
+  if (v < lo) v = lo;
+  if (v > hi) v = hi;
+  return static_cast<int>(v);
+}
+
+// Tunables of the planner: defaults, environment overrides, pda_set_option.
+constexpr int kMaxBlocksPerCu = 8;
+constexpr int kMaxMinSteps = 1 << 30;
+std::atomic<int> g_blocks_per_cu{-1};
+std::atomic<int> g_min_steps{-1};
+
+int blocks_per_cu() {
+  int v = g_blocks_per_cu.load();
+  if (v < 0) {
+    v = env_int("PDA_BLOCKS_PER_CU", 2, 1, kMaxBlocksPerCu);
+    g_blocks_per_cu.store(v);
+  }
+  return v;
+}
+int min_steps_per_wave() {
+  int v = g_min_steps.load();
+  if (v < 0) {
+    v = env_int("PDA_MIN_STEPS", 2, 1, kMaxMinSteps);
+    g_min_steps.store(v);
+  }
+  return v;
+}
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+int log2i(int x) {
+  int s = 0;
+  while ((1 << s) < x) ++s;
+  return s;
+}
+
+int check_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp) {
+  if (batch < 0) return fail(PDA_ERR_SHAPE, "batch must be >= 0 (got %d)", batch);
+  if (hq <= 0 || hkv <= 0) return fail(PDA_ERR_SHAPE, "head counts must be positive (q %d, kv %d)", hq, hkv);
+  if (hq % hkv) return fail(PDA_ERR_SHAPE, "num_q_heads %d is not a multiple of num_kv_heads %d", hq, hkv);
+  if (hq / hkv > PDA_MAX_GROUP)
+    return fail(PDA_ERR_UNSUPPORTED, "query group %d exceeds %d", hq / hkv, PDA_MAX_GROUP);
+  if (d != 64 && d != 128) return fail(PDA_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", d);
+  if (p <= 0 || maxp <= 0) return fail(PDA_ERR_SHAPE, "page_size and max_pages_per_seq must be positive");
+  if (!is_pow2(p) || p > PDA_MAX_PAGE_SIZE)
+    return fail(PDA_ERR_UNSUPPORTED, "page_size %d (supported: powers of two up to %d)", p, PDA_MAX_PAGE_SIZE);
+  if (batch > PDA_MAX_BATCH) return fail(PDA_ERR_UNSUPPORTED, "batch %d exceeds %d", batch, PDA_MAX_BATCH);
+  const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
+  if (max_ctx > (int64_t{1} << 30)) return fail(PDA_ERR_SHAPE, "max_pages_per_seq * page_size too large");
+  const int64_t steps = static_cast<int64_t>(batch) * ((max_ctx + pda::kStep - 1) / pda::kStep);
+  if (steps >= (int64_t{1} << 31))
+    return fail(PDA_ERR_UNSUPPORTED, "batch * max context exceeds 2^36 tokens");
+  return PDA_OK;
+}
+
+struct Plan {
+  int grid = 0;
+  int waves = 0;
+  int64_t slots = 0;
+  int64_t off_acc = 0, off_ml = 0, off_pref = 0, bytes = 0;
+};
+
+int64_t align256(int64_t x) { return (x + 255) & ~int64_t{255}; }
+
+Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus) {
+  Plan pl;
+  const int group = hq / hkv;
+  const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
+  const int64_t steps_max = static_cast<int64_t>(batch) * hkv * ((max_ctx + pda::kStep - 1) / pda::kStep);
+  const int64_t target = static_cast<int64_t>(num_cus) * blocks_per_cu() * pda::kWavesPerBlock;
+  int64_t waves = (steps_max + min_steps_per_wave() - 1) / min_steps_per_wave();
+  if (waves > target) waves = target;
+  if (waves < 1) waves = 1;
+  pl.grid = static_cast<int>((waves + pda::kWavesPerBlock - 1) / pda::kWavesPerBlock);
+  pl.waves = pl.grid * pda::kWavesPerBlock;
+  pl.slots = static_cast<int64_t>(pl.waves) + static_cast<int64_t>(batch) * hkv;
+  pl.off_acc = 0;
+  pl.off_ml = align256(pl.slots * group * d * 4);
+  pl.off_pref = pl.off_ml + align256(pl.slots * group * 2 * 4);
+  pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1) * 4);
+  return pl;
+}
+
+int device_cus(int dev, int* cus) {
+  static std::mutex mu;
+  static std::map<int, int> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(dev);
+  if (it != cache.end()) {
+    *cus = it->second;
+    return PDA_OK;
+  }
+  int n = 0;
+  hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute(multiprocessor count)");
+  cache[dev] = n;
+  *cus = n;
+  return PDA_OK;
+}
+
+// ---------------------------------------------------------------- workspaces
+struct Workspace {
+  void* ptr = nullptr;
+  int64_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  Workspace& ws = g_ws[{dev, st}];
+  if (ws.bytes >= need) {
+    *out = ws.ptr;
+    return PDA_OK;
+  }
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(st, &cap);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+  if (cap != hipStreamCaptureStatusNone)
+    return fail(PDA_ERR_HIP, "workspace must grow to %lld bytes while the stream is being captured; "
+                "call pda_workspace_reserve before capture", static_cast<long long>(need));
+  if (ws.ptr) {
+    e = hipStreamSynchronize(st);  // in-flight calls may still use the old buffer
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    e = hipFree(ws.ptr);
+    if (e != hipSuccess) return hip_fail(e, "hipFree");
+    ws.ptr = nullptr;
+    ws.bytes = 0;
+  }
+  const int64_t grow = need + need / 4;
+  e = hipMalloc(&ws.ptr, static_cast<size_t>(grow));
+  if (e != hipSuccess) {
+    ws.ptr = nullptr;
+    return hip_fail(e, "hipMalloc(workspace)");
+  }
+  ws.bytes = grow;
+  *out = ws.ptr;
+  return PDA_OK;
+}
+
+// ---------------------------------------------------------------- profiling
+struct Rec {
+  hipEvent_t a, b, c;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<Rec> g_prof_recs;
+std::vector<hipEvent_t> g_prof_pool;
+
+hipEvent_t prof_event() {
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pda_last_error(void) { return g_err.c_str(); }
+
+int32_t pda_version(void) { return PDA_VERSION; }
+
+int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+             int32_t page_size, int32_t max_pages_per_seq, int32_t num_cus, int32_t* grid_blocks,
+             int32_t* waves, int64_t* workspace_bytes) {
+  g_err.clear();
+  if (!grid_blocks || !waves || !workspace_bytes) return fail(PDA_ERR_NULL, "pda_plan: NULL output pointer");
+  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  if (rc) return rc;
+  if (num_cus <= 0) return fail(PDA_ERR_SHAPE, "num_cus must be positive");
+  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus);
+  *grid_blocks = batch ? pl.grid : 0;
+  *waves = batch ? pl.waves : 0;
+  *workspace_bytes = batch ? pl.bytes : 0;
+  return PDA_OK;
+}
+
+int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                          int32_t page_size, int32_t max_pages_per_seq, void* stream) {
+  g_err.clear();
+  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  if (rc) return rc;
+  if (batch == 0) return PDA_OK;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  if ((rc = device_cus(dev, &cus))) return rc;
+  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
+  void* ptr = nullptr;
+  return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, &ptr);
+}
+
+int pda_release_workspaces(void) {
+  g_err.clear();
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  int rc = PDA_OK;
+  for (auto& kv : g_ws) {
+    if (!kv.second.ptr) continue;
+    int cur = 0;
+    hipGetDevice(&cur);
+    hipSetDevice(kv.first.first);
+    hipError_t e = hipStreamSynchronize(kv.first.second);
+    if (e == hipSuccess) e = hipFree(kv.second.ptr);
+    hipSetDevice(cur);
+    if (e != hipSuccess) rc = hip_fail(e, "releasing a workspace");
+  }
+  g_ws.clear();
+  return rc;
+}
+
+int pda_set_option(int32_t option, int32_t value) {
+  g_err.clear();
+  switch (option) {
+    case PDA_OPT_BLOCKS_PER_CU:
+      if (value < 1 || value > kMaxBlocksPerCu)
+        return fail(PDA_ERR_SHAPE, "blocks per CU must be in [1, %d]", kMaxBlocksPerCu);
+      g_blocks_per_cu.store(value);
+      return PDA_OK;
+    case PDA_OPT_MIN_STEPS:
+      if (value < 1) return fail(PDA_ERR_SHAPE, "min steps per wave must be >= 1");
+      g_min_steps.store(value);
+      return PDA_OK;
+    default:
+      return fail(PDA_ERR_UNSUPPORTED, "unknown option %d", option);
+  }
+}
+
+int32_t pda_get_option(int32_t option) {
+  switch (option) {
+    case PDA_OPT_BLOCKS_PER_CU: return blocks_per_cu();
+    case PDA_OPT_MIN_STEPS: return min_steps_per_wave();
+    default: return -1;
+  }
+}
+
+int pda_profile_enable(int32_t on) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_prof_on = on != 0;
+  return PDA_OK;
+}
+
+int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls) {
+  g_err.clear();
+  if (!split_ms || !merge_ms || !calls) return fail(PDA_ERR_NULL, "pda_profile_read: NULL output pointer");
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  double s = 0, m = 0;
+  int rc = PDA_OK;
+  for (const Rec& r : g_prof_recs) {
+    float t1 = 0, t2 = 0;
+    hipError_t e = hipEventSynchronize(r.c);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t1, r.a, r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t2, r.b, r.c);
+    if (e != hipSuccess) rc = hip_fail(e, "reading profile events");
+    s += t1;
+    m += t2;
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+    g_prof_pool.push_back(r.c);
+  }
+  *split_ms = s;
+  *merge_ms = m;
+  *calls = static_cast<int64_t>(g_prof_recs.size());
+  g_prof_recs.clear();
+  return rc;
+}
+
+int paged_decode_attention(const void* q, const void* k_cache, const void* v_cache,
+                           const int32_t* block_table, const int32_t* context_lens, void* out,
+                           int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                           int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq, float scale,
+                           void* stream) {
+  g_err.clear();
+  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  if (rc) return rc;
+  if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
+  if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
+  if (batch == 0) return PDA_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !context_lens || !out)
+    return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+  if (misaligned(q, 16) || misaligned(k_cache, 16) || misaligned(v_cache, 16) || misaligned(out, 16))
+    return fail(PDA_ERR_ALIGN, "q, k_cache, v_cache and out must be 16-byte aligned");
+  if (misaligned(block_table, 4) || misaligned(context_lens, 4))
+    return fail(PDA_ERR_ALIGN, "block_table and context_lens must be 4-byte aligned");
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  if ((rc = device_cus(dev, &cus))) return rc;
+  const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;
+
+  pda::LaunchArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.bt = block_table;
+  a.lens = context_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.ws_acc = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_acc);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_ml);
+  a.ws_pref = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pl.off_pref);
+  a.batch = batch;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.group = num_q_heads / num_kv_heads;
+  a.head_dim = head_dim;
+  a.page_shift = log2i(page_size);
+  a.num_pages = num_pages;
+  a.maxp = max_pages_per_seq;
+  a.grid = pl.grid;
+  a.min_steps = min_steps_per_wave();
+  a.scale = scale;
+
+  Rec rec{nullptr, nullptr, nullptr};
+  bool prof = false;
+  {
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    if (g_prof_on) {
+      rec = Rec{prof_event(), prof_event(), prof_event()};
+      prof = rec.a && rec.b && rec.c;
+    }
+  }
+  if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = pda::launch_split_kernel(a, st)) != hipSuccess) return hip_fail(e, "split kernel launch");
+  if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = pda::launch_merge_kernel(a, st)) != hipSuccess) return hip_fail(e, "merge kernel launch");
+  if (prof) {
+    if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    std::lock_guard<std::mutex> lock(g_prof_mu);
+    g_prof_recs.push_back(rec);
+  }
+  return PDA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,51 @@
+"""Helpers for GPU tests: move a workload to the device, run the library,
+compare with the oracle."""
+import sys
+
+import numpy as np
+
+MAX_ABS = 1e-2   # spec tolerance vs the fp64 oracle
+MEAN_ABS = 1e-3
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def to_gpu(w, device="cuda"):
+    import torch
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(device)
+
+    return dict(q=bf(w.q), k=bf(w.k_cache), v=bf(w.v_cache),
+                bt=torch.from_numpy(np.ascontiguousarray(w.block_table)).to(device),
+                lens=torch.from_numpy(np.ascontiguousarray(w.context_lens)).to(device))
+
+
+def run(lib, w, dev=None, out=None, stream=None, fill=float("nan")):
+    """Run the library on workload w; returns out as float64 numpy [B, Hq, D]."""
+    import torch
+    if dev is None:
+        dev = to_gpu(w)
+    if out is None:
+        out = torch.full(tuple(w.q.shape), fill, dtype=torch.bfloat16, device=dev["q"].device)
+    lib.paged_decode_attention(dev["q"], dev["k"], dev["v"], dev["bt"], dev["lens"], out, float(w.scale),
+                               stream=stream)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy().astype(np.float64)
+
+
+def bf16_round(x):
+    import workloads as W
+    return W.bf16_bits_to_f32(W.f32_to_bf16_bits(np.asarray(x, dtype=np.float32))).astype(np.float64)
+
+
+def check(got, ref, what=""):
+    err = np.abs(got - ref)
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
+    log(f"  {what}: max|err|={mx:.3e} mean|err|={mean:.3e} (n={err.size})")
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max {mx:.3e} mean {mean:.3e}"
+    return mx, mean
