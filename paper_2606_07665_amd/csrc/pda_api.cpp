@@ -98,27 +98,33 @@ struct Plan {
   int grid = 0;
   int waves = 0;
   int64_t slots = 0;
-  int64_t off_acc = 0, off_ml = 0, off_pref = 0, bytes = 0;
+  int64_t counters = 0;
+  int64_t off_acc = 0, off_ml = 0, bytes = 0;
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t{255}; }
 
+// Workgroups of 4 waves: as many as fill the device (blocks_per_cu per CU),
+// but no more than give each wave min_steps 32-token steps at the largest
+// context the page table allows.  Partial slots: one per (workgroup,
+// sequence piece), at most grid + batch * hkv.
 Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus) {
   Plan pl;
   const int group = hq / hkv;
   const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
   const int64_t steps_max = static_cast<int64_t>(batch) * hkv * ((max_ctx + pda::kStep - 1) / pda::kStep);
-  const int64_t target = static_cast<int64_t>(num_cus) * blocks_per_cu() * pda::kWavesPerBlock;
-  int64_t waves = (steps_max + min_steps_per_wave() - 1) / min_steps_per_wave();
-  if (waves > target) waves = target;
-  if (waves < 1) waves = 1;
-  pl.grid = static_cast<int>((waves + pda::kWavesPerBlock - 1) / pda::kWavesPerBlock);
+  const int64_t per_block = static_cast<int64_t>(min_steps_per_wave()) * pda::kWavesPerBlock;
+  int64_t blocks = (steps_max + per_block - 1) / per_block;
+  const int64_t target = static_cast<int64_t>(num_cus) * blocks_per_cu();
+  if (blocks > target) blocks = target;
+  if (blocks < 1) blocks = 1;
+  pl.grid = static_cast<int>(blocks);
   pl.waves = pl.grid * pda::kWavesPerBlock;
-  pl.slots = static_cast<int64_t>(pl.waves) + static_cast<int64_t>(batch) * hkv;
+  pl.counters = static_cast<int64_t>(batch) * hkv;
+  pl.slots = static_cast<int64_t>(pl.grid) + pl.counters;
   pl.off_acc = 0;
   pl.off_ml = align256(pl.slots * group * d * 4);
-  pl.off_pref = pl.off_ml + align256(pl.slots * group * 2 * 4);
-  pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1) * 4);
+  pl.bytes = pl.off_ml + align256(pl.slots * group * 2 * 4);
   return pl;
 }
 
@@ -140,18 +146,24 @@ int device_cus(int dev, int* cus) {
 }
 
 // ---------------------------------------------------------------- workspaces
+// Per (device, stream): a data buffer for split partials and a separate
+// counter buffer that is zeroed once when allocated; the kernel returns
+// every counter it uses to zero, so counters stay zero between calls.
 struct Workspace {
   void* ptr = nullptr;
   int64_t bytes = 0;
+  int32_t* cnt = nullptr;
+  int64_t ncnt = 0;
 };
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
-int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
+int workspace_for(int dev, hipStream_t st, int64_t need, int64_t need_cnt, void** out, int32_t** cnt) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   Workspace& ws = g_ws[{dev, st}];
-  if (ws.bytes >= need) {
+  if (ws.bytes >= need && ws.ncnt >= need_cnt) {
     *out = ws.ptr;
+    *cnt = ws.cnt;
     return PDA_OK;
   }
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -160,22 +172,34 @@ int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
   if (cap != hipStreamCaptureStatusNone)
     return fail(PDA_ERR_HIP, "workspace must grow to %lld bytes while the stream is being captured; "
                 "call pda_workspace_reserve before capture", static_cast<long long>(need));
-  if (ws.ptr) {
-    e = hipStreamSynchronize(st);  // in-flight calls may still use the old buffer
-    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-    e = hipFree(ws.ptr);
-    if (e != hipSuccess) return hip_fail(e, "hipFree");
+  e = hipStreamSynchronize(st);  // in-flight calls may still use the old buffers
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  if (ws.bytes < need) {
+    if (ws.ptr && (e = hipFree(ws.ptr)) != hipSuccess) return hip_fail(e, "hipFree");
     ws.ptr = nullptr;
     ws.bytes = 0;
+    const int64_t grow = need + need / 4;
+    if ((e = hipMalloc(&ws.ptr, static_cast<size_t>(grow))) != hipSuccess) {
+      ws.ptr = nullptr;
+      return hip_fail(e, "hipMalloc(workspace)");
+    }
+    ws.bytes = grow;
   }
-  const int64_t grow = need + need / 4;
-  e = hipMalloc(&ws.ptr, static_cast<size_t>(grow));
-  if (e != hipSuccess) {
-    ws.ptr = nullptr;
-    return hip_fail(e, "hipMalloc(workspace)");
+  if (ws.ncnt < need_cnt) {
+    if (ws.cnt && (e = hipFree(ws.cnt)) != hipSuccess) return hip_fail(e, "hipFree");
+    ws.cnt = nullptr;
+    ws.ncnt = 0;
+    const int64_t grow = need_cnt + need_cnt / 4 + 64;
+    if ((e = hipMalloc(&ws.cnt, static_cast<size_t>(grow) * sizeof(int32_t))) != hipSuccess) {
+      ws.cnt = nullptr;
+      return hip_fail(e, "hipMalloc(counters)");
+    }
+    if ((e = hipMemsetAsync(ws.cnt, 0, static_cast<size_t>(grow) * sizeof(int32_t), st)) != hipSuccess)
+      return hip_fail(e, "hipMemsetAsync(counters)");
+    ws.ncnt = grow;
   }
-  ws.bytes = grow;
   *out = ws.ptr;
+  *cnt = ws.cnt;
   return PDA_OK;
 }
 
@@ -235,7 +259,8 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
   if ((rc = device_cus(dev, &cus))) return rc;
   Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
   void* ptr = nullptr;
-  return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, &ptr);
+  int32_t* cnt = nullptr;
+  return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, pl.counters, &ptr, &cnt);
 }
 
 int pda_release_workspaces(void) {
@@ -243,12 +268,13 @@ int pda_release_workspaces(void) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   int rc = PDA_OK;
   for (auto& kv : g_ws) {
-    if (!kv.second.ptr) continue;
+    if (!kv.second.ptr && !kv.second.cnt) continue;
     int cur = 0;
     hipGetDevice(&cur);
     hipSetDevice(kv.first.first);
     hipError_t e = hipStreamSynchronize(kv.first.second);
     if (e == hipSuccess) e = hipFree(kv.second.ptr);
+    if (e == hipSuccess && kv.second.cnt) e = hipFree(kv.second.cnt);
     hipSetDevice(cur);
     if (e != hipSuccess) rc = hip_fail(e, "releasing a workspace");
   }
@@ -339,7 +365,8 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
-  if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;
+  int32_t* cnt = nullptr;
+  if ((rc = workspace_for(dev, st, pl.bytes, pl.counters, &ws, &cnt))) return rc;
 
   pda::LaunchArgs a;
   a.q = static_cast<const uint16_t*>(q);
@@ -350,7 +377,7 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   a.out = static_cast<uint16_t*>(out);
   a.ws_acc = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_acc);
   a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_ml);
-  a.ws_pref = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pl.off_pref);
+  a.ws_cnt = cnt;
   a.batch = batch;
   a.hq = num_q_heads;
   a.hkv = num_kv_heads;
@@ -375,7 +402,6 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if ((e = pda::launch_split_kernel(a, st)) != hipSuccess) return hip_fail(e, "split kernel launch");
   if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if ((e = pda::launch_merge_kernel(a, st)) != hipSuccess) return hip_fail(e, "merge kernel launch");
   if (prof) {
     if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     std::lock_guard<std::mutex> lock(g_prof_mu);

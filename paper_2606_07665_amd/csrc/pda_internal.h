@@ -21,15 +21,14 @@ struct LaunchArgs {
   uint16_t* out;
   float* ws_acc;      // [slots, group, head_dim] partial accumulators
   float* ws_ml;       // [slots, group, 2] partial (max in log2 units, sum)
-  int32_t* ws_pref;   // [batch + 1] steps prefix written by the split kernel
+  int32_t* ws_cnt;    // [batch * hkv] arrival counters, zero between calls
   int batch, hq, hkv, group, head_dim, page_shift, num_pages, maxp;
-  int grid;           // workgroups of the split kernel
-  int min_steps;      // fewest 32-token steps a wave is given
+  int grid;           // workgroups of the kernel
+  int min_steps;      // fewest 32-token steps per wave of a workgroup
   float scale;
 };
 
 hipError_t launch_split_kernel(const LaunchArgs& a, hipStream_t st);
-hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st);
 size_t split_lds_bytes(int head_dim, int batch);
 
 }  // namespace pda

@@ -1,35 +1,46 @@
-// Paged decode attention kernels for MI355X (gfx950, CDNA4, wave64).
+// Paged decode attention kernel for MI355X (gfx950, CDNA4, wave64).
 //
 // What is computed: the paper's kernel family (iv), decode attention over a
 // paged KV cache with grouped-query heads (Method, "Principle-Driven LLM
 // Kernel Generator"): per sequence and kv head, an online softmax over the
-// cached tokens, split across many workers and merged by log-sum-exp
-// ("cross-CTA merging").  The CUDA design the paper sketches (appendix:
-// m16n8k16 fragments, ldmatrix, padded shared rows, a fence-based merge) is
-// prior art for another GPU; this file is laid out for CDNA4 instead:
+// cached tokens, split across many workers, then a log-sum-exp merge of the
+// splits done inside the same kernel ("fused cross-CTA merging"; the paper's
+// appendix describes a fence-based merge with no separate reduction kernel).
+// The CUDA design the paper sketches (m16n8k16 fragments, ldmatrix, padded
+// shared rows) is prior art for another GPU; this kernel is laid out for
+// CDNA4 instead:
 //
 //  * Work split (stream-K over the context).  The flattened space of
 //    (sequence b, kv head g, 32-token step) is cut into equal contiguous
-//    ranges, one per wave.  Every wave gets the same number of steps (+-1)
-//    whatever the length mix, so ragged batches stay balanced, and a wave
-//    that covers a whole (b, g) writes the final output itself.  A wave that
-//    covers part of one writes a partial (running max, sum, unnormalised
-//    accumulator) to a slot indexed wave + sequence, which is unique because
-//    each wave's range is contiguous.
+//    ranges, one per workgroup of four wave64 workers, so every workgroup
+//    gets the same amount of KV whatever the length mix.  Inside a range the
+//    four waves take interleaved steps, each running its own online softmax.
 //  * QK^T on the matrix cores: v_mfma_f32_16x16x32_bf16 with the 16 keys of
-//    a tile as the A rows (each lane loads 16 contiguous bytes of one key
-//    row straight from HBM, exactly the A-operand layout) and the query
-//    heads of the GQA group as the B columns (zero-padded to 16).  One K
-//    read serves every head of the group.
+//    a tile as A rows (each lane loads 16 contiguous bytes of one key row
+//    straight from HBM, which is the A-operand layout) and the query heads
+//    of the GQA group as B columns (zero-padded to 16).  One K read serves
+//    every head of the group.
 //  * The softmax runs in the MFMA result layout (lane = head column, four
-//    key rows per lane), which is lane-for-lane the B-operand layout the
-//    P.V product needs, so probabilities never move between lanes.
+//    key rows per lane), which is lane-for-lane the B operand of the P.V
+//    product, so probabilities never move between lanes.
 //  * V is staged through LDS (padded rows) and read back transposed with
-//    ds_read_b64_tr_b16 to form the A operand of O^T = V^T P^T, again on
-//    v_mfma_f32_16x16x32_bf16.  The output accumulator lands with the head
-//    in the lane column, so the online-softmax rescale is a per-lane scalar.
-//  * Merge: a second small kernel combines the partials of each (b, g) with
-//    exp2 weights.
+//    ds_read_b64_tr_b16 to form the A operand of O^T = V^T P^T.  The output
+//    accumulator has the head in the lane column, so the online-softmax
+//    rescale is one scalar per lane.
+//  * Software pipeline: the K/V loads of a wave's next step are issued
+//    before its current step is computed, and the page ids two steps ahead
+//    before that, so the loop body is one basic block whose waits are all
+//    satisfied by issue order.
+//  * Merge: at the end of a (b, g) piece the four waves combine in LDS.  If
+//    the workgroup covered the whole sequence it writes the output; else it
+//    writes one partial (max in log2 units, sum, unnormalised accumulator)
+//    to a slot indexed workgroup + sequence (unique because ranges are
+//    contiguous) with write-through agent-scope stores, waits for them to be
+//    acknowledged and bumps a per-sequence counter.  The workgroup that
+//    brings the counter to the number of pieces merges all pieces in slot
+//    order (so the result does not depend on arrival order), reading them
+//    from the agent coherence point, and resets the counter.  No L2-wide
+//    writeback or invalidate is issued (those cost more than the merge).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -38,9 +49,11 @@
 namespace pda {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
@@ -56,6 +69,12 @@ struct Shape {
   static constexpr int kVLoads = kStep / kRowsPerLoad;   // V loads per step
   static constexpr int kRowBytes = 2 * D + 32;  // padded LDS row of the V tile
   static constexpr int kTileBytes = kStep * kRowBytes;
+  static constexpr int kAccBytes = 64 * kDT * 16;        // one wave's accumulator in LDS
+  static_assert(kAccBytes <= kTileBytes, "accumulator exchange reuses the V tile");
+  // LDS layout: [4 V tiles][ml exchange 4 x 16 x 2 floats][flag][prefix]
+  static constexpr int kMlOff = kWavesPerBlock * kTileBytes;
+  static constexpr int kFlagOff = kMlOff + kWavesPerBlock * 16 * 2 * 4;
+  static constexpr int kPrefOff = kFlagOff + 16;
 };
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
@@ -66,6 +85,18 @@ __device__ __forceinline__ int clamp_len(int L, int max_ctx) {
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
+}
+
+// Split partials cross workgroups that may sit on different XCDs, whose L2
+// caches are not coherent with each other.  They are written and read only
+// with agent-scope relaxed atomic accesses (write-through stores and loads
+// from the agent coherence point, sc1 on gfx950), so no L2 writeback or
+// invalidate of the whole cache is needed around the arrival counter.
+__device__ __forceinline__ void store_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // physical page of logical page j of a sequence, clamped so that a bad page
@@ -82,12 +113,14 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
     const int32_t* __restrict__ lens, uint16_t* __restrict__ out,
-    float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_pref,
+    float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_cnt,
     int batch, int hq, int hkv, int group, int page_shift, int num_pages, int maxp,
     int min_steps, float scale_log2) {
   using S = Shape<D>;
   extern __shared__ __align__(16) unsigned char smem[];
-  int32_t* pref = reinterpret_cast<int32_t*>(smem + kWavesPerBlock * S::kTileBytes);
+  int32_t* pref = reinterpret_cast<int32_t*>(smem + S::kPrefOff);
+  float* ml_x = reinterpret_cast<float*>(smem + S::kMlOff);
+  int32_t* flag = reinterpret_cast<int32_t*>(smem + S::kFlagOff);
   int32_t* scan = reinterpret_cast<int32_t*>(smem);  // reuses the V tiles before the loop
 
   const int tid = threadIdx.x;
@@ -116,9 +149,15 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
     }
     if (tid == kBlockThreads - 1) pref[batch] = scan[tid];
     __syncthreads();
-    if (blockIdx.x == 0)
-      for (int b = tid; b <= batch; b += kBlockThreads) ws_pref[b] = pref[b];
-    __syncthreads();  // the scan area is overwritten by V tiles below
+  }
+  // empty sequences have no steps: block 0 writes their zero rows
+  if (blockIdx.x == 0) {
+    const int row16 = hq * D / 8;  // 16-byte stores per sequence
+    for (int b = 0; b < batch; ++b) {
+      if (pref[b + 1] != pref[b]) continue;
+      u32x4* orow = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(b) * hq * D);
+      for (int i = tid; i < row16; i += kBlockThreads) orow[i] = u32x4{0u, 0u, 0u, 0u};
+    }
   }
 
   const int lane = tid & 63;
@@ -126,15 +165,15 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
   const int g4 = lane >> 4;  // lane group: MFMA k block / C row block
   const int c = lane & 15;   // MFMA row (A) / column (B, C)
 
-  const int64_t total = static_cast<int64_t>(uniform(pref[batch])) * hkv;
+  const int64_t total = static_cast<int64_t>(pref[batch]) * hkv;
   if (total == 0) return;
-  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-  int64_t weff = (total + min_steps - 1) / min_steps;
-  weff = weff < nwaves ? weff : nwaves;
-  const int w = blockIdx.x * kWavesPerBlock + wid;
-  if (w >= weff) return;
-  int64_t x = (static_cast<int64_t>(w) * total) / weff;
-  const int64_t xend = (static_cast<int64_t>(w + 1) * total) / weff;
+  const int64_t per_block_min = static_cast<int64_t>(min_steps) * kWavesPerBlock;
+  int64_t beff = (total + per_block_min - 1) / per_block_min;
+  beff = beff < gridDim.x ? beff : gridDim.x;
+  const int blk = blockIdx.x;
+  if (blk >= beff) return;
+  int64_t x = (static_cast<int64_t>(blk) * total) / beff;
+  const int64_t xend = (static_cast<int64_t>(blk + 1) * total) / beff;
 
   // sequence containing step x: largest b with pref[b] * hkv <= x
   int b;
@@ -155,8 +194,14 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
   unsigned char* vtile = smem + wid * S::kTileBytes;
   const int vr = lane / S::kChunks;   // V row within one wave load
   const int vq = lane % S::kChunks;   // 16-byte chunk within the row
-  const int64_t tok_stride = static_cast<int64_t>(hkv) * D;       // elements per token
-  const int64_t page_stride = tok_stride << page_shift;            // elements per page
+  const int tok_stride = hkv * D;                                  // elements per token
+  const int64_t page_stride = static_cast<int64_t>(tok_stride) << page_shift;  // per page
+  // lane offsets (elements) inside a 16-token block of one page
+  const int koff = c * tok_stride + 8 * g4;
+  int voff[S::kVLoads];
+#pragma unroll
+  for (int i = 0; i < S::kVLoads; ++i)
+    voff[i] = (((S::kRowsPerLoad * i) & 15) + vr) * tok_stride + 8 * vq;
 
   while (true) {
     const int64_t remaining = xend - x;
@@ -164,6 +209,7 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
     const int L = uniform(clamp_len(lens[b], max_ctx));
     const int npages = (L + page - 1) >> page_shift;
     const int32_t* bt_row = bt + static_cast<int64_t>(b) * maxp;
+    const int seq = b * hkv + g;
 
     // query operand (B of QK^T): head c of the group, d = 32*kk + 8*g4 + e
     bf16x8 qop[S::kQK];
@@ -185,59 +231,79 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
     float m_run = -__builtin_inff();
     float l_lane = 0.f;
 
-    for (int s = s0; s < s1; ++s) {
-      const int t0 = s * kStep;
-      // ---------------- loads: 2 K tiles in A layout, V rows for LDS
-      u32x4 kreg[2][S::kQK];
-      u32x4 vreg[S::kVLoads];
+    // Page ids travel two steps ahead of use: the ids of step k+2 are loaded
+    // (one uniform-address load per 16-token half) before the K/V loads of
+    // step k+1 are issued, so every wait in the loop is satisfied in issue
+    // order and the loop body stays a single basic block.
+    const int sw = s0 + wid;  // this wave's first step; it takes sw, sw+4, ...
+    const int nsteps = sw < s1 ? (s1 - sw + kWavesPerBlock - 1) / kWavesPerBlock : 0;
+    auto step_of = [&](int k) {  // k-th step of this wave, clamped to its last one
+      k = k < nsteps ? k : nsteps - 1;
+      return sw + k * kWavesPerBlock;
+    };
+    auto load_pids = [&](int k, int& pa, int& pb) {
+      const int t0 = step_of(k) * kStep;
+      int ja = t0 >> page_shift, jb = (t0 + 16) >> page_shift;
+      ja = ja < npages ? ja : npages - 1;
+      jb = jb < npages ? jb : npages - 1;
+      pa = bt_row[ja];
+      pb = bt_row[jb];
+    };
+    auto clamp_pid = [&](int p) {
+      const unsigned u = static_cast<unsigned>(uniform(p));
+      return static_cast<int>(u < static_cast<unsigned>(num_pages) ? u : num_pages - 1);
+    };
+
+    auto issue = [&](int k, int pa_raw, int pb_raw, u32x4 (&kr)[2][S::kQK], u32x4 (&vv)[S::kVLoads]) {
+      const int t0 = step_of(k) * kStep;
       if constexpr (!kLanePages) {
         // pages of 16 or more tokens: each 16-token half of the step lies in one page
-        const int pA = uniform(page_at(bt_row, t0 >> page_shift, npages, num_pages));
-        const int pB = uniform(page_at(bt_row, (t0 + 16) >> page_shift, npages, num_pages));
+        const int pA = clamp_pid(pa_raw);
+        const int pB = clamp_pid(pb_raw);
+        const uint16_t* kA = kg + pA * page_stride + static_cast<int64_t>(t0 & (page - 1)) * tok_stride;
+        const uint16_t* kB = kg + pB * page_stride + static_cast<int64_t>((t0 + 16) & (page - 1)) * tok_stride;
+        const uint16_t* vA = vg + pA * page_stride + static_cast<int64_t>(t0 & (page - 1)) * tok_stride;
+        const uint16_t* vB = vg + pB * page_stride + static_cast<int64_t>((t0 + 16) & (page - 1)) * tok_stride;
 #pragma unroll
-        for (int T = 0; T < 2; ++T) {
-          const int tok = t0 + 16 * T + c;
-          const int64_t off = (T ? pB : pA) * page_stride + (tok & (page - 1)) * tok_stride + 8 * g4;
-#pragma unroll
-          for (int kk = 0; kk < S::kQK; ++kk) kreg[T][kk] = ld16(kg + off + 32 * kk);
+        for (int kk = 0; kk < S::kQK; ++kk) {
+          kr[0][kk] = ld16(kA + koff + 32 * kk);
+          kr[1][kk] = ld16(kB + koff + 32 * kk);
         }
 #pragma unroll
-        for (int i = 0; i < S::kVLoads; ++i) {
-          const int tau = S::kRowsPerLoad * i + vr;
-          const int tok = t0 + tau;
-          const int64_t off = ((tau >> 4) ? pB : pA) * page_stride + (tok & (page - 1)) * tok_stride + 8 * vq;
-          vreg[i] = ld16(vg + off);
-        }
+        for (int i = 0; i < S::kVLoads; ++i)
+          vv[i] = ld16(((S::kRowsPerLoad * i) >> 4 ? vB : vA) + voff[i]);
       } else {
         // small pages: every lane looks up the page of its own token
 #pragma unroll
         for (int T = 0; T < 2; ++T) {
           const int tok = t0 + 16 * T + c;
           const int pg = page_at(bt_row, tok >> page_shift, npages, num_pages);
-          const int64_t off = pg * page_stride + (tok & (page - 1)) * tok_stride + 8 * g4;
+          const int64_t off = pg * page_stride + static_cast<int64_t>(tok & (page - 1)) * tok_stride + 8 * g4;
 #pragma unroll
-          for (int kk = 0; kk < S::kQK; ++kk) kreg[T][kk] = ld16(kg + off + 32 * kk);
+          for (int kk = 0; kk < S::kQK; ++kk) kr[T][kk] = ld16(kg + off + 32 * kk);
         }
 #pragma unroll
         for (int i = 0; i < S::kVLoads; ++i) {
           const int tok = t0 + S::kRowsPerLoad * i + vr;
           const int pg = page_at(bt_row, tok >> page_shift, npages, num_pages);
-          const int64_t off = pg * page_stride + (tok & (page - 1)) * tok_stride + 8 * vq;
-          vreg[i] = ld16(vg + off);
+          const int64_t off = pg * page_stride + static_cast<int64_t>(tok & (page - 1)) * tok_stride + 8 * vq;
+          vv[i] = ld16(vg + off);
         }
       }
-      const bool tail = t0 + kStep > L;
+    };
 
-      // ---------------- V rows -> LDS (rows past the end are zeroed, never NaN*0)
+    auto compute = [&](int s, const u32x4 (&kr)[2][S::kQK], const u32x4 (&vv)[S::kVLoads]) {
+      const int t0 = s * kStep;
+      const bool tail = t0 + kStep > L;
+      // V rows -> LDS (rows past the end are zeroed: never NaN * 0)
 #pragma unroll
       for (int i = 0; i < S::kVLoads; ++i) {
         const int tau = S::kRowsPerLoad * i + vr;
-        u32x4 v = vreg[i];
+        u32x4 v = vv[i];
         if (tail && t0 + tau >= L) v = u32x4{0u, 0u, 0u, 0u};
         *reinterpret_cast<u32x4*>(vtile + tau * S::kRowBytes + 16 * vq) = v;
       }
-
-      // ---------------- S^T = K Q^T : rows = keys 16T + 4*g4 + i, column = head c
+      // S^T = K Q^T: rows = keys 16T + 4*g4 + i, column = head c
       f32x4 sacc[2];
 #pragma unroll
       for (int T = 0; T < 2; ++T) {
@@ -245,10 +311,9 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
 #pragma unroll
         for (int kk = 0; kk < S::kQK; ++kk)
           sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, kreg[T][kk]), qop[kk], sacc[T], 0, 0, 0);
+              __builtin_bit_cast(bf16x8, kr[T][kk]), qop[kk], sacc[T], 0, 0, 0);
       }
-
-      // ---------------- online softmax in log2 units
+      // online softmax in log2 units
       float sv[2][4];
       float mx = -__builtin_inff();
 #pragma unroll
@@ -278,56 +343,146 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
       l_lane = l_lane * alpha + psum;
 #pragma unroll
       for (int dt = 0; dt < S::kDT; ++dt) acc[dt] *= alpha;
-
-      // ---------------- O^T += V^T P^T ; V^T operand via transposed LDS reads
+      // O^T += V^T P^T ; V^T operand via transposed LDS reads
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      {
-        const unsigned char* r0 = vtile + (4 * g4 + (c >> 2)) * S::kRowBytes + 8 * (c & 3);
-        const unsigned char* r1 = r0 + 16 * S::kRowBytes;
+      const unsigned char* r0 = vtile + (4 * g4 + (c >> 2)) * S::kRowBytes + 8 * (c & 3);
+      const unsigned char* r1 = r0 + 16 * S::kRowBytes;
 #pragma unroll
-        for (int dt = 0; dt < S::kDT; ++dt) {
-          const i16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r0 + 32 * dt));
-          const i16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r1 + 32 * dt));
-          const i16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-          acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), pop,
-                                                             acc[dt], 0, 0, 0);
-        }
+      for (int dt = 0; dt < S::kDT; ++dt) {
+        const i16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r0 + 32 * dt));
+        const i16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r1 + 32 * dt));
+        const i16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), pop, acc[dt], 0,
+                                                           0, 0);
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    // ---- this wave's steps, K/V loads one step ahead, page ids two ahead
+    if (nsteps > 0) {
+      u32x4 kA[2][S::kQK], vA[S::kVLoads], kB[2][S::kQK], vB[S::kVLoads];
+      int pa0, pb0, pa1, pb1;
+      load_pids(0, pa0, pb0);
+      load_pids(1, pa1, pb1);
+      issue(0, pa0, pb0, kA, vA);
+      int k = 0;
+      for (; k + 2 < nsteps; k += 2) {
+        load_pids(k + 2, pa0, pb0);
+        issue(k + 1, pa1, pb1, kB, vB);
+        compute(step_of(k), kA, vA);
+        load_pids(k + 3, pa1, pb1);
+        issue(k + 2, pa0, pb0, kA, vA);
+        compute(step_of(k + 1), kB, vB);
+      }
+      if (k + 1 < nsteps) {
+        issue(k + 1, pa1, pb1, kB, vB);
+        compute(step_of(k), kA, vA);
+        compute(step_of(k + 1), kB, vB);
+      } else {
+        compute(step_of(k), kA, vA);
+      }
     }
 
-    // ---------------- epilogue for this (b, g) piece
+    // ---- combine the four waves in LDS
     float l_tot = l_lane + __shfl_xor(l_lane, 16);
     l_tot += __shfl_xor(l_tot, 32);
-    const bool whole = (s0 == 0) && (s1 == nb);
-    if (c < group) {
-      const int h = g * group + c;
-      if (whole) {
-        const float inv = 1.0f / l_tot;
-        uint16_t* orow = out + (static_cast<int64_t>(b) * hq + h) * D + 4 * g4;
+    f32x4* accx = reinterpret_cast<f32x4*>(smem);  // [wave][dt][lane], reuses the V tiles
+    __syncthreads();  // every wave is done with its V tile
 #pragma unroll
-        for (int dt = 0; dt < S::kDT; ++dt) {
-          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    for (int dt = 0; dt < S::kDT; ++dt) accx[(wid * S::kDT + dt) * 64 + lane] = acc[dt];
+    if (g4 == 0) {
+      ml_x[(wid * 16 + c) * 2 + 0] = m_run;
+      ml_x[(wid * 16 + c) * 2 + 1] = l_tot;
+    }
+    __syncthreads();
+    float mw[kWavesPerBlock], big_m = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      mw[w] = ml_x[(w * 16 + c) * 2];
+      big_m = fmaxf(big_m, mw[w]);
+    }
+    float fw[kWavesPerBlock], den = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      // a wave with no step in this piece has m = -inf and l = 0: weight 0
+      fw[w] = mw[w] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mw[w] - big_m);
+      den += fw[w] * ml_x[(w * 16 + c) * 2 + 1];
+    }
+    const bool whole = (s0 == 0) && (s1 == nb);
+    const int64_t slot = static_cast<int64_t>(blk) + seq;
+    // wave wid finalises d tiles wid, wid + 4, ...
+    for (int dt = wid; dt < S::kDT; dt += kWavesPerBlock) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < kWavesPerBlock; ++w) a += fw[w] * accx[(w * S::kDT + dt) * 64 + lane];
+      if (c < group) {
+        if (whole) {
+          const float inv = 1.0f / den;
           bf16x4 o;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(acc[dt][i] * inv);
-          *reinterpret_cast<u32x2*>(orow + 16 * dt) = __builtin_bit_cast(u32x2, o);
-        }
-      } else {
-        const int64_t slot = static_cast<int64_t>(w) + static_cast<int64_t>(b) * hkv + g;
-        float* arow = ws_acc + (slot * group + c) * D + 4 * g4;
+          for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(a[i] * inv);
+          uint16_t* orow = out + (static_cast<int64_t>(b) * hq + g * group + c) * D + 16 * dt + 4 * g4;
+          *reinterpret_cast<u32x2*>(orow) = __builtin_bit_cast(u32x2, o);
+        } else {
+          float* dst = ws_acc + (slot * group + c) * D + 16 * dt + 4 * g4;
 #pragma unroll
-        for (int dt = 0; dt < S::kDT; ++dt) *reinterpret_cast<f32x4*>(arow + 16 * dt) = acc[dt];
-        if (g4 == 0) {
-          ws_ml[(slot * group + c) * 2 + 0] = m_run;
-          ws_ml[(slot * group + c) * 2 + 1] = l_tot;
+          for (int i = 0; i < 4; ++i) store_agent(dst + i, a[i]);
         }
       }
     }
+    if (!whole) {
+      if (wid == 0 && g4 == 0 && c < group) {
+        store_agent(ws_ml + (slot * group + c) * 2 + 0, big_m);
+        store_agent(ws_ml + (slot * group + c) * 2 + 1, den);
+      }
+      // publish this piece (every store acknowledged before the barrier),
+      // count it, and let the workgroup of the last piece merge
+      __builtin_amdgcn_s_waitcnt(0);
+      __atomic_signal_fence(__ATOMIC_SEQ_CST);
+      __syncthreads();
+      const int64_t x0 = static_cast<int64_t>(pref[b]) * hkv + static_cast<int64_t>(g) * nb;
+      const int64_t b0 = ((x0 + 1) * beff - 1) / total;
+      const int64_t b1 = ((x0 + nb) * beff - 1) / total;
+      const int pieces = static_cast<int>(b1 - b0 + 1);
+      if (tid == 0)
+        *flag = __hip_atomic_fetch_add(ws_cnt + seq, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                pieces - 1;
+      __syncthreads();
+      if (*flag) {
+        const int n4 = group * D / 4;
+        for (int e4 = tid; e4 < n4; e4 += kBlockThreads) {
+          const int hh = (4 * e4) / D;
+          float mm = -__builtin_inff(), dd = 0.f;
+          f32x4 nn = {0.f, 0.f, 0.f, 0.f};
+          for (int64_t pb = b0; pb <= b1; ++pb) {
+            const int64_t sl = pb + seq;
+            const float* mlp = ws_ml + (sl * group + hh) * 2;
+            const float* ap = ws_acc + (sl * group) * D + 4 * e4;
+            const f32x2 mlv = {load_agent(mlp), load_agent(mlp + 1)};
+            const f32x4 av = {load_agent(ap), load_agent(ap + 1), load_agent(ap + 2), load_agent(ap + 3)};
+            const float m2 = fmaxf(mm, mlv[0]);
+            const float f_old = __builtin_amdgcn_exp2f(mm - m2);
+            const float f_new = __builtin_amdgcn_exp2f(mlv[0] - m2);
+            nn = nn * f_old + av * f_new;
+            dd = dd * f_old + mlv[1] * f_new;
+            mm = m2;
+          }
+          const float inv = 1.0f / dd;
+          bf16x4 o;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(nn[i] * inv);
+          uint16_t* orow = out + (static_cast<int64_t>(b) * hq + g * group) * D + 4 * e4;
+          *reinterpret_cast<u32x2*>(orow) = __builtin_bit_cast(u32x2, o);
+        }
+        if (tid == 0)  // ready for the next call
+          __hip_atomic_store(ws_cnt + seq, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    __syncthreads();  // LDS (V tiles, exchange, flag) is reused by the next piece
 
     x += s1 - s0;
     if (x >= xend) break;
@@ -342,66 +497,10 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
   }
 }
 
-// Combine the partials of one (b, g): out = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j.
-// Also writes the zero rows of empty sequences.
-template <int D>
-__global__ __launch_bounds__(kBlockThreads) void merge_kernel(
-    uint16_t* __restrict__ out, const float* __restrict__ ws_acc, const float* __restrict__ ws_ml,
-    const int32_t* __restrict__ ws_pref, int batch, int hq, int hkv, int group, int min_steps,
-    int split_waves) {
-  const int s = blockIdx.x;
-  const int b = s / hkv;
-  const int g = s - b * hkv;
-  const int nb = ws_pref[b + 1] - ws_pref[b];
-  const int tid = threadIdx.x;
-  constexpr int kQuads = D / 4;
-  constexpr int kHeadsPerPass = kBlockThreads / kQuads;
-  const int hh0 = tid / kQuads;
-  const int d4 = (tid % kQuads) * 4;
-  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-
-  if (nb == 0) {
-    for (int hh = hh0; hh < group; hh += kHeadsPerPass) {
-      uint16_t* orow = out + (static_cast<int64_t>(b) * hq + g * group + hh) * D + d4;
-      *reinterpret_cast<u32x2*>(orow) = u32x2{0u, 0u};
-    }
-    return;
-  }
-  const int64_t total = static_cast<int64_t>(ws_pref[batch]) * hkv;
-  int64_t weff = (total + min_steps - 1) / min_steps;
-  weff = weff < split_waves ? weff : split_waves;
-  const int64_t x0 = static_cast<int64_t>(ws_pref[b]) * hkv + static_cast<int64_t>(g) * nb;
-  const int64_t x1 = x0 + nb - 1;
-  const int64_t w0 = ((x0 + 1) * weff - 1) / total;
-  const int64_t w1 = ((x1 + 1) * weff - 1) / total;
-  if (w0 == w1) return;  // one wave covered the sequence and wrote it
-
-  for (int hh = hh0; hh < group; hh += kHeadsPerPass) {
-    float big_m = -__builtin_inff();
-    for (int64_t w = w0; w <= w1; ++w)
-      big_m = fmaxf(big_m, ws_ml[((w + s) * group + hh) * 2]);
-    float den = 0.f;
-    f32x4 num = {0.f, 0.f, 0.f, 0.f};
-    for (int64_t w = w0; w <= w1; ++w) {
-      const int64_t slot = w + s;
-      const float f = __builtin_amdgcn_exp2f(ws_ml[(slot * group + hh) * 2] - big_m);
-      den += f * ws_ml[(slot * group + hh) * 2 + 1];
-      num += f * *reinterpret_cast<const f32x4*>(ws_acc + (slot * group + hh) * D + d4);
-    }
-    const float inv = 1.0f / den;
-    bf16x4 o;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(num[i] * inv);
-    uint16_t* orow = out + (static_cast<int64_t>(b) * hq + g * group + hh) * D + d4;
-    *reinterpret_cast<u32x2*>(orow) = __builtin_bit_cast(u32x2, o);
-  }
-}
-
 template <int D, bool kLanePages>
 static hipError_t launch_split(const LaunchArgs& a, hipStream_t st) {
   using S = Shape<D>;
-  const size_t lds = static_cast<size_t>(kWavesPerBlock) * S::kTileBytes +
-                     static_cast<size_t>(a.batch + 1) * sizeof(int32_t);
+  const size_t lds = static_cast<size_t>(S::kPrefOff) + static_cast<size_t>(a.batch + 1) * sizeof(int32_t);
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_kernel<D, kLanePages>),
@@ -410,17 +509,9 @@ static hipError_t launch_split(const LaunchArgs& a, hipStream_t st) {
     attr_set = true;
   }
   hipLaunchKernelGGL((split_kernel<D, kLanePages>), dim3(a.grid), dim3(kBlockThreads), lds, st,
-                     a.q, a.k, a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.batch,
+                     a.q, a.k, a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_cnt, a.batch,
                      a.hq, a.hkv, a.group, a.page_shift, a.num_pages, a.maxp, a.min_steps,
                      a.scale * kLog2e);
-  return hipGetLastError();
-}
-
-template <int D>
-static hipError_t launch_merge(const LaunchArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((merge_kernel<D>), dim3(a.batch * a.hkv), dim3(kBlockThreads), 0, st, a.out,
-                     a.ws_acc, a.ws_ml, a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.min_steps,
-                     a.grid * kWavesPerBlock);
   return hipGetLastError();
 }
 
@@ -430,14 +521,9 @@ hipError_t launch_split_kernel(const LaunchArgs& a, hipStream_t st) {
   return lane_pages ? launch_split<64, true>(a, st) : launch_split<64, false>(a, st);
 }
 
-hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
-  if (a.head_dim == 128) return launch_merge<128>(a, st);
-  return launch_merge<64>(a, st);
-}
-
 size_t split_lds_bytes(int head_dim, int batch) {
-  const size_t tile = head_dim == 128 ? Shape<128>::kTileBytes : Shape<64>::kTileBytes;
-  return kWavesPerBlock * tile + static_cast<size_t>(batch + 1) * sizeof(int32_t);
+  const size_t base = head_dim == 128 ? Shape<128>::kPrefOff : Shape<64>::kPrefOff;
+  return base + static_cast<size_t>(batch + 1) * sizeof(int32_t);
 }
 
 }  // namespace pda
