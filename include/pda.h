@@ -136,7 +136,7 @@ int32_t pda_version(void);
  * batch's context over min(num_cus * blocks_per_cu * 4 waves,
  * ceil(total 32-token steps / min_steps)) waves.
  *   PDA_OPT_BLOCKS_PER_CU  workgroups of 4 waves per compute unit, 1..8
- *                          (default 2, env PDA_BLOCKS_PER_CU).
+ *                          (default 1, env PDA_BLOCKS_PER_CU).
  *   PDA_OPT_MIN_STEPS      fewest 32-token steps a wave is given, >= 1
  *                          (default 2, env PDA_MIN_STEPS); a large value
  *                          forces fewer splits, 1 the most.

@@ -54,7 +54,7 @@ std::atomic<int> g_min_steps{-1};
 int blocks_per_cu() {
   int v = g_blocks_per_cu.load();
   if (v < 0) {
-    v = env_int("PDA_BLOCKS_PER_CU", 2, 1, kMaxBlocksPerCu);
+    v = env_int("PDA_BLOCKS_PER_CU", 1, 1, kMaxBlocksPerCu);
     g_blocks_per_cu.store(v);
   }
   return v;

@@ -67,11 +67,18 @@ struct Shape {
   static constexpr int kChunks = D / 8;         // 16-byte chunks per key/value row
   static constexpr int kRowsPerLoad = 64 / kChunks;      // V rows per wave load
   static constexpr int kVLoads = kStep / kRowsPerLoad;   // V loads per step
-  static constexpr int kRowBytes = 2 * D + 32;  // padded LDS row of the V tile
-  static constexpr int kTileBytes = kStep * kRowBytes;
+  // Padded LDS rows.  K rows (stride 2D+16 bytes): the A-operand read of a
+  // 16-row tile (lane = row, 16 B each) then starts every row 4 banks apart.
+  // V rows (stride 2D+32 bytes): the transposed reads of 8 rows x 32 B start
+  // every row 8 banks apart.
+  static constexpr int kKRowBytes = 2 * D + 16;
+  static constexpr int kVRowBytes = 2 * D + 32;
+  static constexpr int kKTileBytes = kStep * kKRowBytes;
+  static constexpr int kVTileBytes = kStep * kVRowBytes;
+  static constexpr int kTileBytes = kKTileBytes + kVTileBytes;   // per wave
   static constexpr int kAccBytes = 64 * kDT * 16;        // one wave's accumulator in LDS
-  static_assert(kAccBytes <= kTileBytes, "accumulator exchange reuses the V tile");
-  // LDS layout: [4 V tiles][ml exchange 4 x 16 x 2 floats][flag][prefix]
+  static_assert(kAccBytes <= kTileBytes, "accumulator exchange reuses the K/V tiles");
+  // LDS layout: [4 x (K tile, V tile)][ml exchange 4 x 16 x 2 floats][flag][prefix]
   static constexpr int kMlOff = kWavesPerBlock * kTileBytes;
   static constexpr int kFlagOff = kMlOff + kWavesPerBlock * 16 * 2 * 4;
   static constexpr int kPrefOff = kFlagOff + 16;
@@ -85,6 +92,30 @@ __device__ __forceinline__ int clamp_len(int L, int max_ctx) {
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
+}
+
+// K and V are read exactly once per call, with raw buffer loads:
+//  * non-temporal (cache policy NT): on MI355X a plain streaming read runs at
+//    ~7.1 TB/s this way against ~6.1 TB/s with default loads;
+//  * the descriptor's base is the page (a wave-uniform 64-bit address) and
+//    its size covers only the valid token rows, so rows past the end of the
+//    sequence, or a whole step that does not exist, read as zeros without
+//    touching memory.
+constexpr int kBufferDword3 = 0x00020000;  // raw buffer, 32-bit data format (gfx9 family)
+constexpr int kCachePolicyNT = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t page_rsrc(const uint16_t* base, int bytes) {
+  // the base is wave-uniform; passing it through readfirstlane keeps the
+  // descriptor in SGPRs (a 64-bit VALU add would otherwise leave it in VGPRs
+  // and every load would be wrapped in a waterfall loop)
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
+  void* ub = reinterpret_cast<void*>((static_cast<uint64_t>(hi) << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, uniform(bytes), kBufferDword3);
+}
+__device__ __forceinline__ u32x4 ld16_stream(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCachePolicyNT);
 }
 
 // Split partials cross workgroups that may sit on different XCDs, whose L2
@@ -161,7 +192,7 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
   }
 
   const int lane = tid & 63;
-  const int wid = tid >> 6;
+  const int wid = uniform(tid >> 6);  // wave-uniform: lets the compiler keep per-wave values in SGPRs
   const int g4 = lane >> 4;  // lane group: MFMA k block / C row block
   const int c = lane & 15;   // MFMA row (A) / column (B, C)
 
@@ -191,17 +222,18 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
   int g = rel / nb;
   int s0 = rel - g * nb;
 
-  unsigned char* vtile = smem + wid * S::kTileBytes;
-  const int vr = lane / S::kChunks;   // V row within one wave load
+  unsigned char* ktile = smem + wid * S::kTileBytes;
+  unsigned char* vtile = ktile + S::kKTileBytes;
+  const int vr = lane / S::kChunks;   // row within one wave load (K and V alike)
   const int vq = lane % S::kChunks;   // 16-byte chunk within the row
   const int tok_stride = hkv * D;                                  // elements per token
   const int64_t page_stride = static_cast<int64_t>(tok_stride) << page_shift;  // per page
-  // lane offsets (elements) inside a 16-token block of one page
-  const int koff = c * tok_stride + 8 * g4;
-  int voff[S::kVLoads];
+  // byte offsets of this lane's loads inside a 16-token block of one page:
+  // load i covers rows kRowsPerLoad*i .. +kRowsPerLoad-1 of the step, 16 B per lane
+  int loff[S::kVLoads];
 #pragma unroll
   for (int i = 0; i < S::kVLoads; ++i)
-    voff[i] = (((S::kRowsPerLoad * i) & 15) + vr) * tok_stride + 8 * vq;
+    loff[i] = 2 * ((((S::kRowsPerLoad * i) & 15) + vr) * tok_stride + 8 * vq);
 
   while (true) {
     const int64_t remaining = xend - x;
@@ -254,64 +286,72 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
       return static_cast<int>(u < static_cast<unsigned>(num_pages) ? u : num_pages - 1);
     };
 
-    auto issue = [&](int k, int pa_raw, int pb_raw, u32x4 (&kr)[2][S::kQK], u32x4 (&vv)[S::kVLoads]) {
+    auto issue = [&](int k, int pa_raw, int pb_raw, u32x4 (&kr)[S::kVLoads], u32x4 (&vv)[S::kVLoads]) {
       const int t0 = step_of(k) * kStep;
+      // valid token rows in each 16-token half (0 for a step past the wave's last)
+      const int live = k < nsteps ? L - t0 : 0;
+      const int nA = live < 0 ? 0 : (live < 16 ? live : 16);
+      const int nB = live < 16 ? 0 : (live < 32 ? live - 16 : 16);
       if constexpr (!kLanePages) {
         // pages of 16 or more tokens: each 16-token half of the step lies in one page
         const int pA = clamp_pid(pa_raw);
         const int pB = clamp_pid(pb_raw);
-        const uint16_t* kA = kg + pA * page_stride + static_cast<int64_t>(t0 & (page - 1)) * tok_stride;
-        const uint16_t* kB = kg + pB * page_stride + static_cast<int64_t>((t0 + 16) & (page - 1)) * tok_stride;
-        const uint16_t* vA = vg + pA * page_stride + static_cast<int64_t>(t0 & (page - 1)) * tok_stride;
-        const uint16_t* vB = vg + pB * page_stride + static_cast<int64_t>((t0 + 16) & (page - 1)) * tok_stride;
+        const int64_t oA = pA * page_stride + static_cast<int64_t>(t0 & (page - 1)) * tok_stride;
+        const int64_t oB = pB * page_stride + static_cast<int64_t>((t0 + 16) & (page - 1)) * tok_stride;
+        const int bytesA = nA * tok_stride * 2, bytesB = nB * tok_stride * 2;
+        const __amdgpu_buffer_rsrc_t rkA = page_rsrc(kg + oA, bytesA), rkB = page_rsrc(kg + oB, bytesB);
+        const __amdgpu_buffer_rsrc_t rvA = page_rsrc(vg + oA, bytesA), rvB = page_rsrc(vg + oB, bytesB);
 #pragma unroll
-        for (int kk = 0; kk < S::kQK; ++kk) {
-          kr[0][kk] = ld16(kA + koff + 32 * kk);
-          kr[1][kk] = ld16(kB + koff + 32 * kk);
+        for (int i = 0; i < S::kVLoads; ++i) {
+          const bool hb = (S::kRowsPerLoad * i) >> 4;
+          kr[i] = ld16_stream(hb ? rkB : rkA, loff[i]);
+          vv[i] = ld16_stream(hb ? rvB : rvA, loff[i]);
         }
-#pragma unroll
-        for (int i = 0; i < S::kVLoads; ++i)
-          vv[i] = ld16(((S::kRowsPerLoad * i) >> 4 ? vB : vA) + voff[i]);
       } else {
         // small pages: every lane looks up the page of its own token
 #pragma unroll
-        for (int T = 0; T < 2; ++T) {
-          const int tok = t0 + 16 * T + c;
-          const int pg = page_at(bt_row, tok >> page_shift, npages, num_pages);
-          const int64_t off = pg * page_stride + static_cast<int64_t>(tok & (page - 1)) * tok_stride + 8 * g4;
-#pragma unroll
-          for (int kk = 0; kk < S::kQK; ++kk) kr[T][kk] = ld16(kg + off + 32 * kk);
-        }
-#pragma unroll
         for (int i = 0; i < S::kVLoads; ++i) {
-          const int tok = t0 + S::kRowsPerLoad * i + vr;
+          const int tau = S::kRowsPerLoad * i + vr;
+          const int tok = t0 + tau;
           const int pg = page_at(bt_row, tok >> page_shift, npages, num_pages);
           const int64_t off = pg * page_stride + static_cast<int64_t>(tok & (page - 1)) * tok_stride + 8 * vq;
-          vv[i] = ld16(vg + off);
+          // page_at keeps the address inside the pool; rows past the end are zeroed
+          const bool ok = tok < t0 + live;
+          const u32x4 zero = {0u, 0u, 0u, 0u};
+          const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kg + off));
+          const u32x4 vv_ = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vg + off));
+          kr[i] = ok ? kv : zero;
+          vv[i] = ok ? vv_ : zero;
         }
       }
     };
 
-    auto compute = [&](int s, const u32x4 (&kr)[2][S::kQK], const u32x4 (&vv)[S::kVLoads]) {
+    auto compute = [&](int s, const u32x4 (&kr)[S::kVLoads], const u32x4 (&vv)[S::kVLoads]) {
       const int t0 = s * kStep;
       const bool tail = t0 + kStep > L;
-      // V rows -> LDS (rows past the end are zeroed: never NaN * 0)
+      // K and V rows -> LDS (rows past the end arrived as zeros: never NaN * 0)
 #pragma unroll
       for (int i = 0; i < S::kVLoads; ++i) {
         const int tau = S::kRowsPerLoad * i + vr;
-        u32x4 v = vv[i];
-        if (tail && t0 + tau >= L) v = u32x4{0u, 0u, 0u, 0u};
-        *reinterpret_cast<u32x4*>(vtile + tau * S::kRowBytes + 16 * vq) = v;
+        *reinterpret_cast<u32x4*>(ktile + tau * S::kKRowBytes + 16 * vq) = kr[i];
+        *reinterpret_cast<u32x4*>(vtile + tau * S::kVRowBytes + 16 * vq) = vv[i];
       }
-      // S^T = K Q^T: rows = keys 16T + 4*g4 + i, column = head c
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // S^T = K Q^T: rows = keys 16T + 4*g4 + i, column = head c; the A operand
+      // (key row c, d = 32*kk + 8*g4 .. +7) is read back from the K tile
       f32x4 sacc[2];
 #pragma unroll
       for (int T = 0; T < 2; ++T) {
         sacc[T] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const unsigned char* krow = ktile + (16 * T + c) * S::kKRowBytes + 16 * g4;
 #pragma unroll
-        for (int kk = 0; kk < S::kQK; ++kk)
-          sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, kr[T][kk]), qop[kk], sacc[T], 0, 0, 0);
+        for (int kk = 0; kk < S::kQK; ++kk) {
+          const u32x4 a = *reinterpret_cast<const u32x4*>(krow + 64 * kk);
+          sacc[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), qop[kk],
+                                                             sacc[T], 0, 0, 0);
+        }
       }
       // online softmax in log2 units
       float sv[2][4];
@@ -344,11 +384,8 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
 #pragma unroll
       for (int dt = 0; dt < S::kDT; ++dt) acc[dt] *= alpha;
       // O^T += V^T P^T ; V^T operand via transposed LDS reads
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      const unsigned char* r0 = vtile + (4 * g4 + (c >> 2)) * S::kRowBytes + 8 * (c & 3);
-      const unsigned char* r1 = r0 + 16 * S::kRowBytes;
+      const unsigned char* r0 = vtile + (4 * g4 + (c >> 2)) * S::kVRowBytes + 8 * (c & 3);
+      const unsigned char* r1 = r0 + 16 * S::kVRowBytes;
 #pragma unroll
       for (int dt = 0; dt < S::kDT; ++dt) {
         const i16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r0 + 32 * dt));
@@ -364,7 +401,7 @@ __global__ __launch_bounds__(kBlockThreads, 2) void split_kernel(
 
     // ---- this wave's steps, K/V loads one step ahead, page ids two ahead
     if (nsteps > 0) {
-      u32x4 kA[2][S::kQK], vA[S::kVLoads], kB[2][S::kQK], vB[S::kVLoads];
+      u32x4 kA[S::kVLoads], vA[S::kVLoads], kB[S::kVLoads], vB[S::kVLoads];
       int pa0, pb0, pa1, pb1;
       load_pids(0, pa0, pb0);
       load_pids(1, pa1, pb1);
