@@ -42,7 +42,24 @@ def parse():
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic per launch (from rocprofv3 --pmc runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 1 GiB device-to-device copy (known HBM traffic) "
+                         "to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE")
     return ap.parse_args()
+
+
+def copy_calibration(reps=5):
+    """A plain copy of 1 GiB: reads 1 GiB and writes 1 GiB per launch."""
+    import torch
+    n = 1 << 29  # bf16 elements = 1 GiB
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read_per_launch": 2 * n, "bytes_written_per_launch": 2 * n,
+                      "launches": reps}), flush=True)
 
 
 def cpu_baseline(w, budget_s):
@@ -90,6 +107,10 @@ def main():
         print(f"bench.py: this path runs on one GPU; --gpus {args.gpus} is not supported "
               "(the kernel works on one GPU's share; sharding across GPUs is not built)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
 
     import torch
     import workloads as W

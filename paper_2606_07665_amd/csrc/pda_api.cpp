@@ -96,35 +96,48 @@ int check_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, in
 
 struct Plan {
   int grid = 0;
-  int waves = 0;
+  int waves = 0;   // per workgroup
+  int hgs = 0;     // kv heads per workgroup
   int64_t slots = 0;
-  int64_t counters = 0;
-  int64_t off_acc = 0, off_ml = 0, bytes = 0;
+  int64_t off_acc = 0, off_ml = 0, off_pref = 0, bytes = 0;
 };
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t{255}; }
 
-// Workgroups of 4 waves: as many as fill the device (blocks_per_cu per CU),
-// but no more than give each wave min_steps 32-token steps at the largest
+// Largest divisor of hkv that is at most kMaxWaves: the kv heads a workgroup
+// reads together from every page.
+int heads_per_group(int hkv) {
+  for (int d = pda::kMaxWaves; d > 1; --d)
+    if (hkv % d == 0) return d;
+  return 1;
+}
+
+// Workgroups: one wave per kv head of a group, times step phases up to 8
+// waves; as many workgroups as fill the device (blocks_per_cu per CU), but
+// none with fewer than min_steps 32-token steps per wave at the largest
 // context the page table allows.  Partial slots: one per (workgroup,
-// sequence piece), at most grid + batch * hkv.
+// sequence piece), at most grid + batch * kv-head groups.
 Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus) {
   Plan pl;
   const int group = hq / hkv;
+  pl.hgs = heads_per_group(hkv);
+  const int phases = pl.hgs >= pda::kMaxWaves ? 1 : pda::kMaxWaves / pl.hgs;
+  pl.waves = pl.hgs * phases;
+  const int64_t ngroups = hkv / pl.hgs;
   const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
-  const int64_t steps_max = static_cast<int64_t>(batch) * hkv * ((max_ctx + pda::kStep - 1) / pda::kStep);
-  const int64_t per_block = static_cast<int64_t>(min_steps_per_wave()) * pda::kWavesPerBlock;
+  const int64_t steps_max = static_cast<int64_t>(batch) * ngroups * ((max_ctx + pda::kStep - 1) / pda::kStep);
+  const int64_t per_block = static_cast<int64_t>(min_steps_per_wave()) * phases;
   int64_t blocks = (steps_max + per_block - 1) / per_block;
   const int64_t target = static_cast<int64_t>(num_cus) * blocks_per_cu();
   if (blocks > target) blocks = target;
   if (blocks < 1) blocks = 1;
   pl.grid = static_cast<int>(blocks);
-  pl.waves = pl.grid * pda::kWavesPerBlock;
-  pl.counters = static_cast<int64_t>(batch) * hkv;
-  pl.slots = static_cast<int64_t>(pl.grid) + pl.counters;
+  pl.slots = static_cast<int64_t>(pl.grid) + static_cast<int64_t>(batch) * ngroups;
+  const int64_t rows = pl.slots * pl.hgs * group;
   pl.off_acc = 0;
-  pl.off_ml = align256(pl.slots * group * d * 4);
-  pl.bytes = pl.off_ml + align256(pl.slots * group * 2 * 4);
+  pl.off_ml = align256(rows * d * 4);
+  pl.off_pref = pl.off_ml + align256(rows * 2 * 4);
+  pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1) * 4);
   return pl;
 }
 
@@ -146,24 +159,19 @@ int device_cus(int dev, int* cus) {
 }
 
 // ---------------------------------------------------------------- workspaces
-// Per (device, stream): a data buffer for split partials and a separate
-// counter buffer that is zeroed once when allocated; the kernel returns
-// every counter it uses to zero, so counters stay zero between calls.
+// Per (device, stream): one buffer for split partials and the steps prefix.
 struct Workspace {
   void* ptr = nullptr;
   int64_t bytes = 0;
-  int32_t* cnt = nullptr;
-  int64_t ncnt = 0;
 };
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
-int workspace_for(int dev, hipStream_t st, int64_t need, int64_t need_cnt, void** out, int32_t** cnt) {
+int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   Workspace& ws = g_ws[{dev, st}];
-  if (ws.bytes >= need && ws.ncnt >= need_cnt) {
+  if (ws.bytes >= need) {
     *out = ws.ptr;
-    *cnt = ws.cnt;
     return PDA_OK;
   }
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -172,34 +180,20 @@ int workspace_for(int dev, hipStream_t st, int64_t need, int64_t need_cnt, void*
   if (cap != hipStreamCaptureStatusNone)
     return fail(PDA_ERR_HIP, "workspace must grow to %lld bytes while the stream is being captured; "
                 "call pda_workspace_reserve before capture", static_cast<long long>(need));
-  e = hipStreamSynchronize(st);  // in-flight calls may still use the old buffers
-  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-  if (ws.bytes < need) {
-    if (ws.ptr && (e = hipFree(ws.ptr)) != hipSuccess) return hip_fail(e, "hipFree");
+  if (ws.ptr) {
+    e = hipStreamSynchronize(st);  // in-flight calls may still use the old buffer
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    if ((e = hipFree(ws.ptr)) != hipSuccess) return hip_fail(e, "hipFree");
     ws.ptr = nullptr;
     ws.bytes = 0;
-    const int64_t grow = need + need / 4;
-    if ((e = hipMalloc(&ws.ptr, static_cast<size_t>(grow))) != hipSuccess) {
-      ws.ptr = nullptr;
-      return hip_fail(e, "hipMalloc(workspace)");
-    }
-    ws.bytes = grow;
   }
-  if (ws.ncnt < need_cnt) {
-    if (ws.cnt && (e = hipFree(ws.cnt)) != hipSuccess) return hip_fail(e, "hipFree");
-    ws.cnt = nullptr;
-    ws.ncnt = 0;
-    const int64_t grow = need_cnt + need_cnt / 4 + 64;
-    if ((e = hipMalloc(&ws.cnt, static_cast<size_t>(grow) * sizeof(int32_t))) != hipSuccess) {
-      ws.cnt = nullptr;
-      return hip_fail(e, "hipMalloc(counters)");
-    }
-    if ((e = hipMemsetAsync(ws.cnt, 0, static_cast<size_t>(grow) * sizeof(int32_t), st)) != hipSuccess)
-      return hip_fail(e, "hipMemsetAsync(counters)");
-    ws.ncnt = grow;
+  const int64_t grow = need + need / 4;
+  if ((e = hipMalloc(&ws.ptr, static_cast<size_t>(grow))) != hipSuccess) {
+    ws.ptr = nullptr;
+    return hip_fail(e, "hipMalloc(workspace)");
   }
+  ws.bytes = grow;
   *out = ws.ptr;
-  *cnt = ws.cnt;
   return PDA_OK;
 }
 
@@ -241,7 +235,7 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
   if (num_cus <= 0) return fail(PDA_ERR_SHAPE, "num_cus must be positive");
   Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus);
   *grid_blocks = batch ? pl.grid : 0;
-  *waves = batch ? pl.waves : 0;
+  *waves = batch ? pl.grid * pl.waves : 0;
   *workspace_bytes = batch ? pl.bytes : 0;
   return PDA_OK;
 }
@@ -259,8 +253,7 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
   if ((rc = device_cus(dev, &cus))) return rc;
   Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
   void* ptr = nullptr;
-  int32_t* cnt = nullptr;
-  return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, pl.counters, &ptr, &cnt);
+  return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, &ptr);
 }
 
 int pda_release_workspaces(void) {
@@ -268,13 +261,12 @@ int pda_release_workspaces(void) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   int rc = PDA_OK;
   for (auto& kv : g_ws) {
-    if (!kv.second.ptr && !kv.second.cnt) continue;
+    if (!kv.second.ptr) continue;
     int cur = 0;
     hipGetDevice(&cur);
     hipSetDevice(kv.first.first);
     hipError_t e = hipStreamSynchronize(kv.first.second);
     if (e == hipSuccess) e = hipFree(kv.second.ptr);
-    if (e == hipSuccess && kv.second.cnt) e = hipFree(kv.second.cnt);
     hipSetDevice(cur);
     if (e != hipSuccess) rc = hip_fail(e, "releasing a workspace");
   }
@@ -365,8 +357,7 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
-  int32_t* cnt = nullptr;
-  if ((rc = workspace_for(dev, st, pl.bytes, pl.counters, &ws, &cnt))) return rc;
+  if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;
 
   pda::LaunchArgs a;
   a.q = static_cast<const uint16_t*>(q);
@@ -377,7 +368,7 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   a.out = static_cast<uint16_t*>(out);
   a.ws_acc = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_acc);
   a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_ml);
-  a.ws_cnt = cnt;
+  a.ws_pref = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pl.off_pref);
   a.batch = batch;
   a.hq = num_q_heads;
   a.hkv = num_kv_heads;
@@ -387,6 +378,8 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   a.num_pages = num_pages;
   a.maxp = max_pages_per_seq;
   a.grid = pl.grid;
+  a.waves = pl.waves;
+  a.hgs = pl.hgs;
   a.min_steps = min_steps_per_wave();
   a.scale = scale;
 
@@ -400,8 +393,11 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
     }
   }
   if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if ((e = pda::launch_split_kernel(a, st)) != hipSuccess) return hip_fail(e, "split kernel launch");
+  if ((e = pda::launch_attn_kernel(a, st)) != hipSuccess) return hip_fail(e, "attention kernel launch");
   if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  // with one workgroup every piece is a whole sequence: nothing to merge
+  if (pl.grid > 1 && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
+    return hip_fail(e, "merge kernel launch");
   if (prof) {
     if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     std::lock_guard<std::mutex> lock(g_prof_mu);

@@ -7,10 +7,11 @@
 
 namespace pda {
 
-constexpr int kBlockThreads = 256;            // 4 independent wave64 workers
-constexpr int kWavesPerBlock = kBlockThreads / 64;
-constexpr int kStep = 32;                     // tokens per pipeline step of a wave
-constexpr int kMaxLdsBytes = 160 * 1024;      // LDS per CU on gfx950
+constexpr int kStep = 32;                 // tokens per pipeline step of a wave
+constexpr int kMaxWaves = 8;              // waves per attention workgroup (at most)
+constexpr int kMaxBlockThreads = 64 * kMaxWaves;
+constexpr int kMergeThreads = 256;
+constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 
 struct LaunchArgs {
   const uint16_t* q;
@@ -19,16 +20,19 @@ struct LaunchArgs {
   const int32_t* bt;
   const int32_t* lens;
   uint16_t* out;
-  float* ws_acc;      // [slots, group, head_dim] partial accumulators
-  float* ws_ml;       // [slots, group, 2] partial (max in log2 units, sum)
-  int32_t* ws_cnt;    // [batch * hkv] arrival counters, zero between calls
+  float* ws_acc;      // [slots, hgs, group, head_dim] partial accumulators
+  float* ws_ml;       // [slots, hgs, group, 2] partial (max in log2 units, sum)
+  int32_t* ws_pref;   // [batch + 1] steps prefix, written by the attention kernel
   int batch, hq, hkv, group, head_dim, page_shift, num_pages, maxp;
-  int grid;           // workgroups of the kernel
-  int min_steps;      // fewest 32-token steps per wave of a workgroup
+  int hgs;            // kv heads per workgroup (a divisor of hkv, at most 8)
+  int waves;          // waves per workgroup: hgs x step phases
+  int grid;           // workgroups of the attention kernel
+  int min_steps;      // fewest 32-token steps per wave
   float scale;
 };
 
-hipError_t launch_split_kernel(const LaunchArgs& a, hipStream_t st);
-size_t split_lds_bytes(int head_dim, int batch);
+hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st);
+hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st);
+size_t attn_lds_bytes(int head_dim, int batch, int waves);
 
 }  // namespace pda
