@@ -222,7 +222,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-            "kernel": "split_kernel (online-softmax pass over the paged KV)",
+            "kernel": "attn_kernel (online-softmax pass over the paged KV)",
         },
     }
     if not args.no_cpu_baseline:

@@ -22,8 +22,9 @@
  * sequence with L_b = 0 gets a zero output row.
  *
  * Arithmetic: bf16 inputs, fp32 accumulation (scores, running max and sum,
- * the probability-times-value products via bf16 matrix cores with the
- * probabilities rounded to bf16), bf16 round-to-nearest-even output.
+ * the probability-times-value products on bf16 matrix cores with each
+ * probability carried as a sum of two bf16 values, ~2^-17 relative), bf16
+ * round-to-nearest-even output.
  *
  * Memory: every pointer argument of paged_decode_attention is a DEVICE
  * pointer on the current HIP device.  The caller allocates and owns all of

@@ -365,15 +365,20 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
-      bf16x8 pop;
+      // p = hi + lo in two bf16 operands: the P.V product then carries the
+      // probabilities to ~2^-17 instead of bf16's 2^-9 (one more MFMA per d
+      // tile on an otherwise idle matrix pipe)
+      bf16x8 pop, pop_lo;
       float psum = 0.f;
 #pragma unroll
       for (int T = 0; T < 2; ++T)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const __bf16 pb = static_cast<__bf16>(__builtin_amdgcn_exp2f(sv[T][i] - m_new));
-          pop[4 * T + i] = pb;
-          psum += static_cast<float>(pb);
+          const float pf = __builtin_amdgcn_exp2f(sv[T][i] - m_new);
+          const __bf16 hi = static_cast<__bf16>(pf);
+          pop[4 * T + i] = hi;
+          pop_lo[4 * T + i] = static_cast<__bf16>(pf - static_cast<float>(hi));
+          psum += pf;
         }
       l_lane = l_lane * alpha + psum;
 #pragma unroll
@@ -387,8 +392,9 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
         const i16x4 a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r0 + 32 * dt));
         const i16x4 a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(r1 + 32 * dt));
         const i16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), pop, acc[dt], 0,
-                                                           0, 0);
+        const bf16x8 va = __builtin_bit_cast(bf16x8, a);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pop, acc[dt], 0, 0, 0);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pop_lo, acc[dt], 0, 0, 0);
       }
       lds_order();
     };

@@ -4,7 +4,7 @@ import sys
 
 import numpy as np
 
-MAX_ABS = 1e-2   # spec tolerance vs the fp64 oracle
+MAX_ABS = 1e-2   # required tolerance vs the fp64 oracle (absolute, on bf16 outputs)
 MEAN_ABS = 1e-3
 
 
@@ -42,10 +42,22 @@ def bf16_round(x):
     return W.bf16_bits_to_f32(W.f32_to_bf16_bits(np.asarray(x, dtype=np.float32))).astype(np.float64)
 
 
-def check(got, ref, what=""):
+def bf16_ulps(got, ref, floor=2.0 ** -6):
+    """|got - ref| in bf16 spacings at max(|ref|, floor)."""
+    ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(ref), floor))) - 7)
+    return np.abs(got - ref) / ulp
+
+
+def check(got, ref, what="", max_ulps=1.0):
+    """Required tolerance (max 1e-2, mean 1e-3 absolute), and the stronger
+    property this path has: every bf16 output is within one bf16 spacing of
+    the fp64 value (the only rounding left is the output's own)."""
     err = np.abs(got - ref)
     assert np.isfinite(got).all(), f"{what}: non-finite output"
     mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
-    log(f"  {what}: max|err|={mx:.3e} mean|err|={mean:.3e} (n={err.size})")
+    ulps = float(bf16_ulps(got, ref).max()) if err.size else 0.0
+    log(f"  {what}: max|err|={mx:.3e} mean|err|={mean:.3e} max={ulps:.2f} bf16 ulp (n={err.size})")
     assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max {mx:.3e} mean {mean:.3e}"
+    if max_ulps is not None:
+        assert ulps <= max_ulps, f"{what}: {ulps:.2f} bf16 ulps"
     return mx, mean

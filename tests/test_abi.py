@@ -1,0 +1,104 @@
+"""The C-ABI library on the CPU: it loads, exports every function its header
+declares, and rejects bad arguments with the documented codes before making
+any HIP call (none of these calls touches a device)."""
+import ctypes
+import math
+
+import pytest
+
+from paper_2606_07665_amd import binding as B
+
+OK, NULL, SHAPE, UNSUPPORTED, SCALE, ALIGN = 0, 1, 2, 3, 4, 5
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return B.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = B.declared_symbols()
+    assert {"paged_decode_attention", "pda_plan", "pda_workspace_reserve", "pda_last_error"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in include/pda.h but not exported"
+    assert B.version() == 1
+
+
+def call(ptr=16, batch=2, hq=32, hkv=8, d=128, p=16, n=64, maxp=8, scale=0.088, ptrs=None):
+    ptrs = ptrs or [ptr] * 6
+    return B.raw_call(*ptrs, batch, hq, hkv, d, p, n, maxp, scale)
+
+
+@pytest.mark.parametrize("kwargs,code,text", [
+    (dict(ptr=0), NULL, "NULL"),
+    (dict(batch=-1), SHAPE, "batch"),
+    (dict(hkv=7), SHAPE, "multiple"),
+    (dict(hq=0), SHAPE, "positive"),
+    (dict(hq=64, hkv=2), UNSUPPORTED, "group"),
+    (dict(d=96), UNSUPPORTED, "head_dim"),
+    (dict(p=24), UNSUPPORTED, "page_size"),
+    (dict(p=2048), UNSUPPORTED, "page_size"),
+    (dict(p=0), SHAPE, "positive"),
+    (dict(maxp=0), SHAPE, "positive"),
+    (dict(batch=8193), UNSUPPORTED, "batch"),
+    (dict(n=0), SHAPE, "num_pages"),
+    (dict(scale=float("inf")), SCALE, "finite"),
+    (dict(scale=float("nan")), SCALE, "finite"),
+    (dict(ptrs=[16, 16, 24, 16, 16, 16]), ALIGN, "16-byte"),
+    (dict(ptrs=[16, 16, 16, 18, 16, 16]), ALIGN, "4-byte"),
+    (dict(maxp=1 << 27, p=16), SHAPE, "too large"),
+])
+def test_argument_errors(lib, kwargs, code, text):
+    rc = call(**kwargs)
+    assert rc == code, B.last_error()
+    assert text in B.last_error()
+
+
+def test_empty_batch_is_a_noop(lib):
+    # batch 0 returns before any pointer is used or any HIP call is made
+    assert call(ptr=0, batch=0) == OK
+    assert B.last_error() == ""
+
+
+def test_planner_fills_the_device_and_sizes_the_workspace(lib):
+    # long context: one workgroup per CU, 8 waves each, workspace covers the slots
+    g, w, ws = B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)
+    assert g == 256 and w == 256 * 8
+    slots = g + 4 * 1  # one kv-head group of 8 per sequence
+    assert ws >= slots * 8 * 8 * (128 + 2) * 4
+    # tiny problem: fewer workgroups than CUs (each wave gets >= 2 steps)
+    g, w, ws = B.plan(1, 8, 2, 64, 16, 16, num_cus=256)
+    assert g == 1 and w == 8
+    # kv-head group: largest divisor of Hkv <= 8, phases up to 8 waves
+    g, w, _ = B.plan(3, 12, 3, 64, 16, 10, num_cus=256)
+    assert w % 6 == 0
+    g, w, _ = B.plan(2, 16, 16, 128, 16, 100, num_cus=256)
+    assert w == 8 * g
+    with pytest.raises(B.PdaError):
+        B.plan(1, 8, 3, 64, 16, 16)
+    with pytest.raises(B.PdaError):
+        B.plan(1, 8, 2, 64, 16, 16, num_cus=0)
+
+
+def test_planner_grid_scales_with_options(lib):
+    try:
+        B.set_option(B.OPT_BLOCKS_PER_CU, 2)
+        assert B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)[0] == 512
+        B.set_option(B.OPT_BLOCKS_PER_CU, 1)
+        B.set_option(B.OPT_MIN_STEPS, 1 << 20)
+        assert B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)[0] == 1
+    finally:
+        B.set_option(B.OPT_BLOCKS_PER_CU, 1)
+        B.set_option(B.OPT_MIN_STEPS, 2)
+    assert B.get_option(B.OPT_MIN_STEPS) == 2
+    with pytest.raises(B.PdaError):
+        B.set_option(B.OPT_BLOCKS_PER_CU, 0)
+    with pytest.raises(B.PdaError):
+        B.set_option(99, 1)
+    assert B.get_option(99) == -1
+
+
+def test_profile_read_null_pointer(lib):
+    assert lib.pda_profile_read(None, None, None) == NULL
+    s, m, n = B.profile_read()
+    assert n == 0 and s == 0.0 and m == 0.0

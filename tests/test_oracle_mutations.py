@@ -1,0 +1,88 @@
+"""The oracle's pins are sharp: plant a plausible mistake in (a copy of) the
+oracle's arithmetic, on the CPU, and check that at least one pin fails."""
+import numpy as np
+import pytest
+
+import oracle
+import test_oracle as pins
+from _golden import cases as golden_cases
+
+
+def make_one_group(slot_swap=False, no_scale=False, no_shift=False, short=False,
+                   no_norm=False, neg=False, kv_swap=False, head_mod=False):
+    def _one_group(q_bits, k_bits, v_bits, bt_row, length, page_size, g, group, sigma):
+        d = q_bits.shape[-1]
+        if length == 0:
+            return np.zeros((group, d)), np.full(group, -np.inf), np.zeros((group, 0))
+        n = length - 1 if short else length
+        t = np.arange(n)
+        if slot_swap:
+            pages = np.asarray(bt_row)[np.minimum(t % page_size, len(bt_row) - 1)].astype(np.int64)
+            slots = np.minimum(t // page_size, page_size - 1)
+        else:
+            pages = np.asarray(bt_row)[t // page_size].astype(np.int64)
+            slots = t % page_size
+        kt = oracle.bf16_to_f64(k_bits[pages, slots, g, :])
+        vt = oracle.bf16_to_f64(v_bits[pages, slots, g, :])
+        if kv_swap:
+            kt, vt = vt, kt
+        hkv = k_bits.shape[2]
+        rows = q_bits[g::hkv] if head_mod else q_bits[g * group:(g + 1) * group]
+        qg = oracle.bf16_to_f64(rows)
+        s = (1.0 if no_scale else sigma) * (qg @ kt.T)
+        if neg:
+            s = -s
+        with np.errstate(over="ignore", invalid="ignore"):
+            m = np.zeros((group, 1)) if no_shift else s.max(axis=1, keepdims=True)
+            e = np.exp(s - m)
+            den = e.sum(axis=1, keepdims=True)
+            w = e if no_norm else e / den
+            return w @ vt, (m + np.log(den))[:, 0], w
+    return _one_group
+
+
+MUTANTS = {
+    "page/slot swapped": dict(slot_swap=True),
+    "scale dropped": dict(no_scale=True),
+    "no max shift": dict(no_shift=True),
+    "one token short": dict(short=True),
+    "weights not normalised": dict(no_norm=True),
+    "score sign flipped": dict(neg=True),
+    "K and V swapped": dict(kv_swap=True),
+    "head h -> kv head h % Hkv": dict(head_mod=True),
+}
+
+PIN_FUNCS = [
+    pins.test_length_one_returns_v_exactly,
+    pins.test_constant_v_returns_constant,
+    pins.test_zero_query_gives_mean_of_values,
+    pins.test_brute_force_dense_independent_gather,
+    pins.test_matches_torch_sdpa_fp64,
+    pins.test_gqa_mapping_probe,
+    pins.test_dominant_token_no_overflow,
+    pins.test_brute_force_fsum_tiny,
+]
+
+
+def test_unmutated_oracle_passes_every_pin():
+    for f in PIN_FUNCS:
+        f()
+
+
+@pytest.mark.parametrize("name", list(MUTANTS))
+def test_each_mutant_is_caught(name, monkeypatch):
+    monkeypatch.setattr(oracle, "_one_group", make_one_group(**MUTANTS[name]))
+    failed = []
+    for f in PIN_FUNCS:
+        try:
+            with np.errstate(all="ignore"):
+                f()
+        except (AssertionError, ValueError, IndexError, FloatingPointError):
+            failed.append(f.__name__)
+    for gname, w, expected in golden_cases():
+        try:
+            with np.errstate(all="ignore"):
+                pins.test_golden_closed_forms(gname, w, expected)
+        except (AssertionError, ValueError, IndexError):
+            failed.append("golden:" + gname)
+    assert failed, f"mutant '{name}' passed every pin"
