@@ -32,7 +32,7 @@
 //  * A piece that is a whole (b, kv head) sequence is normalised and written
 //    directly.  Otherwise the piece's (max in log2 units, sum, unnormalised
 //    accumulator) go to a workspace slot, and merge_kernel combines them in
-//    slot order (deterministic), one workgroup per (sequence, query head).
+//    slot order (deterministic).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -492,28 +492,31 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
   }
 }
 
-// Combine the pieces of one (sequence b, query head h):
+// Merge of split pieces: one workgroup per (sequence, kv-head group, chunk
+// of its query heads).  Per query head:
 //   out = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j,  M = max_j m_j,
-// in slot order.  Threads split the D/4 float4 columns x groups of pieces;
-// the piece groups are folded through LDS.
-template <int D>
+// over the pieces in slot order.  Threads split (head of the chunk, group of
+// pieces, float4 column); kPG piece groups are folded through LDS.  kPG = 8
+// suits plans where a sequence spans many workgroups (long contexts), kPG = 1
+// plans where it spans a few (then a workgroup covers more heads).
+template <int D, int kPG>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     uint16_t* __restrict__ out, const float* __restrict__ ws_acc, const float* __restrict__ ws_ml,
     const int32_t* __restrict__ ws_pref, int batch, int hq, int hkv, int group, int hgs, int min_steps,
     int phases, int grid_blocks) {
   constexpr int kCols = D / 4;
-  constexpr int kPG = kMergeThreads / kCols;  // piece groups
-  __shared__ f32x4 s_num[kPG][kCols];
-  __shared__ float s_m[kPG], s_l[kPG];
+  constexpr int kHPB = kMergeThreads / (kPG * kCols);  // query heads per workgroup
+  static_assert(kHPB >= 1 && kHPB * kPG * kCols == kMergeThreads, "merge layout");
+  __shared__ f32x4 s_num[kHPB][kPG][kCols];
+  __shared__ float s_m[kHPB][kPG], s_l[kHPB][kPG];
 
-  const int bh = blockIdx.x;
-  const int b = bh / hq;
-  const int h = bh - b * hq;
-  const int g = h / group;
-  const int c = h - g * group;
   const int ngroups = hkv / hgs;
-  const int hg = g / hgs;
-  const int hi_w = g - hg * hgs;
+  const int heads = hgs * group;  // query heads of one kv-head group
+  const int chunks = (heads + kHPB - 1) / kHPB;
+  const int e = blockIdx.x / chunks;
+  const int chunk = blockIdx.x - e * chunks;
+  const int b = e / ngroups;
+  const int hg = e - b * ngroups;
   const int nb = ws_pref[b + 1] - ws_pref[b];
   if (nb == 0) return;  // zero row written by the attention kernel
   const int64_t total = static_cast<int64_t>(ws_pref[batch]) * ngroups;
@@ -526,45 +529,58 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   if (w0 == w1) return;  // one workgroup covered the sequence and wrote it
 
   const int tid = threadIdx.x;
+  const int hs = tid / (kPG * kCols);
+  const int pg = (tid / kCols) % kPG;
   const int col = tid % kCols;
-  const int pg = tid / kCols;
+  const int hh = chunk * kHPB + hs;  // query head within the kv-head group
+  const bool active = hh < heads;
   const int64_t base = static_cast<int64_t>(b) * ngroups + hg;
   float mm = -__builtin_inff(), ll = 0.f;
   f32x4 nn = {0.f, 0.f, 0.f, 0.f};
-  for (int64_t w = w0 + pg; w <= w1; w += kPG) {
-    const int64_t row = ((w + base) * hgs + hi_w) * group + c;
-    const f32x2 mlv = *reinterpret_cast<const f32x2*>(ws_ml + row * 2);
-    const f32x4 av = *reinterpret_cast<const f32x4*>(ws_acc + row * D + 4 * col);
-    const float m2 = fmaxf(mm, mlv[0]);
-    const float fo = __builtin_amdgcn_exp2f(mm - m2);
-    const float fn = __builtin_amdgcn_exp2f(mlv[0] - m2);
-    nn = nn * fo + av * fn;
-    ll = ll * fo + mlv[1] * fn;
-    mm = m2;
+  if (active) {
+    const int hi_w = hh / group, c = hh - (hh / group) * group;
+#pragma unroll 4
+    for (int64_t w = w0 + pg; w <= w1; w += kPG) {
+      const int64_t row = ((w + base) * hgs + hi_w) * group + c;
+      const f32x2 mlv = *reinterpret_cast<const f32x2*>(ws_ml + row * 2);
+      const f32x4 av = *reinterpret_cast<const f32x4*>(ws_acc + row * D + 4 * col);
+      const float m2 = fmaxf(mm, mlv[0]);
+      const float fo = __builtin_amdgcn_exp2f(mm - m2);
+      const float fn = __builtin_amdgcn_exp2f(mlv[0] - m2);
+      nn = nn * fo + av * fn;
+      ll = ll * fo + mlv[1] * fn;
+      mm = m2;
+    }
   }
-  s_num[pg][col] = nn;
-  if (col == 0) {
-    s_m[pg] = mm;
-    s_l[pg] = ll;
-  }
-  __syncthreads();
-  if (pg != 0) return;
-  float big_m = -__builtin_inff();
+  if (kPG > 1) {
+    s_num[hs][pg][col] = nn;
+    if (col == 0) {
+      s_m[hs][pg] = mm;
+      s_l[hs][pg] = ll;
+    }
+    __syncthreads();
+    if (pg != 0) return;
+    float big_m = -__builtin_inff();
 #pragma unroll
-  for (int p = 0; p < kPG; ++p) big_m = fmaxf(big_m, s_m[p]);
-  float den = 0.f;
-  f32x4 num = {0.f, 0.f, 0.f, 0.f};
+    for (int p = 0; p < kPG; ++p) big_m = fmaxf(big_m, s_m[hs][p]);
+    float den = 0.f;
+    f32x4 num = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int p = 0; p < kPG; ++p) {
-    // a piece group that got no piece has m = -inf: weight 0
-    const float f = s_m[p] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(s_m[p] - big_m);
-    den += f * s_l[p];
-    num += f * s_num[p][col];
+    for (int p = 0; p < kPG; ++p) {
+      // a piece group that got no piece has m = -inf: weight 0
+      const float f = s_m[hs][p] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(s_m[hs][p] - big_m);
+      den += f * s_l[hs][p];
+      num += f * s_num[hs][p][col];
+    }
+    nn = num;
+    ll = den;
   }
-  const float inv = 1.0f / den;
+  if (!active) return;
+  const float inv = 1.0f / ll;
   bf16x4 o;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(num[i] * inv);
+  for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(nn[i] * inv);
+  const int h = hg * heads + hh;
   *reinterpret_cast<u32x2*>(out + (static_cast<int64_t>(b) * hq + h) * D + 4 * col) = __builtin_bit_cast(u32x2, o);
 }
 
@@ -590,15 +606,23 @@ hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
   return lane_pages ? launch_attn<64, true>(a, st) : launch_attn<64, false>(a, st);
 }
 
-hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
-  const dim3 grid(a.batch * a.hq);
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL((merge_kernel<128>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml,
-                       a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.hgs, a.min_steps, a.waves / a.hgs, a.grid);
-  else
-    hipLaunchKernelGGL((merge_kernel<64>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml,
-                       a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.hgs, a.min_steps, a.waves / a.hgs, a.grid);
+template <int D, int kPG>
+static hipError_t launch_merge(const LaunchArgs& a, hipStream_t st) {
+  constexpr int kHPB = kMergeThreads / (kPG * (D / 4));
+  const int heads = a.hgs * a.group;
+  const int chunks = (heads + kHPB - 1) / kHPB;
+  const dim3 grid(a.batch * (a.hkv / a.hgs) * chunks);
+  hipLaunchKernelGGL((merge_kernel<D, kPG>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml,
+                     a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.hgs, a.min_steps, a.waves / a.hgs, a.grid);
   return hipGetLastError();
+}
+
+hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
+  // expected pieces per split sequence: workgroups per kv-head-group sequence
+  const int64_t seqs = static_cast<int64_t>(a.batch) * (a.hkv / a.hgs);
+  const bool many = a.grid >= 8 * seqs;
+  if (a.head_dim == 128) return many ? launch_merge<128, 8>(a, st) : launch_merge<128, 1>(a, st);
+  return many ? launch_merge<64, 8>(a, st) : launch_merge<64, 1>(a, st);
 }
 
 size_t attn_lds_bytes(int head_dim, int batch, int waves) {
