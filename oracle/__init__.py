@@ -27,6 +27,10 @@ A sequence with L_b = 0 yields a zero row (lse = -inf).
 denominator and unnormalised accumulator, then the log-sum-exp merge of the
 chunks.  It is pinned against :func:`attend` for arbitrary chunkings.
 
+:func:`kv_append` is the step before attention in the paper's decode loop:
+the new token's key and value are scattered into their page slot and the
+length already counts that token.
+
 Readings where the paper is silent (it prints no attention formula, page
 size, layout or tolerance): standard scaled dot-product softmax with no other
 mask than the length, KV pool layout [num_pages, P, Hkv, D], lengths that
@@ -41,7 +45,7 @@ from typing import Iterable, List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = ["bf16_to_f64", "attend", "attend_pairs", "weights", "split_merge",
-           "brute_force_tiny"]
+           "brute_force_tiny", "kv_append"]
 
 
 def bf16_to_f64(bits) -> np.ndarray:
@@ -219,3 +223,30 @@ def brute_force_tiny(q, k_cache, v_cache, block_table, context_lens, scale):
             rows.append(row)
         result.append(rows)
     return result
+
+
+def kv_append(k_cache, v_cache, k_new, v_new, block_table, context_lens):
+    """The KV append that precedes decode attention (Method, "Kernel
+    Customization and Multi-Request Adaptation": a scatter kernel writes the
+    new key and value vectors, and attention then runs with the sequence
+    length advanced by one).
+
+    ``context_lens`` already counts the new token, so sequence b's new key
+    and value (``k_new[b]``, ``v_new[b]``: [Hkv, D] bf16 bits) land at
+    position L_b - 1: page ``block_table[b, (L_b - 1) // P]``, slot
+    ``(L_b - 1) % P``, every kv head.  Sequences with L_b = 0 write nothing.
+    Returns new (k_cache, v_cache) arrays; the inputs are not modified.
+    """
+    k = np.array(k_cache, copy=True)
+    v = np.array(v_cache, copy=True)
+    page_size = k.shape[1]
+    for b in range(len(context_lens)):
+        length = int(context_lens[b])
+        if length == 0:
+            continue
+        t = length - 1
+        page = int(block_table[b][t // page_size])
+        k[page, t % page_size] = k_new[b]
+        v[page, t % page_size] = v_new[b]
+    return k, v
+

@@ -206,3 +206,44 @@ def test_attend_pairs_matches_full():
     res = oracle.attend_pairs(w.q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale,
                               [(1, 1), (0, 0)])
     assert np.array_equal(res[(1, 1)][0], out[1, 4:8]) and np.array_equal(res[(0, 0)][1], lse[0, 0:4])
+
+
+# ---------------------------------------------------------------- kv append
+def test_kv_append_writes_exactly_the_new_slot():
+    w = small([1, 16, 17, 0, 40], hq=8, hkv=2, d=64, pool="holes:0.3", seed=31)
+    rng = np.random.default_rng(0)
+    kn = rng.integers(0, 1 << 15, size=(5, 2, 64)).astype(np.uint16)
+    vn = rng.integers(0, 1 << 15, size=(5, 2, 64)).astype(np.uint16)
+    k2, v2 = oracle.kv_append(w.k_cache, w.v_cache, kn, vn, w.block_table, w.context_lens)
+    changed = np.zeros(w.k_cache.shape[:2], dtype=bool)
+    for b, L in enumerate(w.context_lens):
+        if L == 0:
+            continue
+        t = int(L) - 1
+        page, slot = w.block_table[b, t // 16], t % 16
+        assert np.array_equal(k2[page, slot], kn[b]) and np.array_equal(v2[page, slot], vn[b])
+        changed[page, slot] = True
+    assert np.array_equal(k2[~changed], w.k_cache[~changed])
+    assert np.array_equal(v2[~changed], w.v_cache[~changed])
+    assert changed.sum() == 4
+
+
+def test_append_then_attend_equals_attend_on_the_full_cache():
+    # blank the newest token of every sequence, append it back, attend
+    w = small([3, 33, 100, 0, 257], hq=8, hkv=2, d=64, seed=32)
+    kn = np.zeros((w.batch, 2, 64), dtype=np.uint16)
+    vn = np.zeros_like(kn)
+    kb, vb = w.k_cache.copy(), w.v_cache.copy()
+    for b, L in enumerate(w.context_lens):
+        if L == 0:
+            continue
+        t = int(L) - 1
+        page, slot = w.block_table[b, t // 16], t % 16
+        kn[b], vn[b] = kb[page, slot], vb[page, slot]
+        kb[page, slot] = 0x7FC0
+        vb[page, slot] = 0x7FC0
+    k2, v2 = oracle.kv_append(kb, vb, kn, vn, w.block_table, w.context_lens)
+    a, _ = oracle.attend(w.q, k2, v2, w.block_table, w.context_lens, w.scale)
+    ref, _ = run(w)
+    assert np.array_equal(a, ref)
+
