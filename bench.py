@@ -183,6 +183,37 @@ def main():
         torch.cuda.synchronize()
         graph_us = g0.elapsed_time(g1) / (reps * 20) * 1e3
 
+    # ---- the KV append of the same decode step (alone, and append-then-attend)
+    rng = np.random.default_rng(1234)
+    kv_shape = (w.batch, w.num_kv_heads, w.head_dim)
+    k_new = bf(W.f32_to_bf16_bits(rng.standard_normal(kv_shape, dtype=np.float32)))
+    v_new = bf(W.f32_to_bf16_bits(rng.standard_normal(kv_shape, dtype=np.float32)))
+
+    def timed(fn):
+        for _ in range(5):
+            fn()
+        a0 = torch.cuda.Event(enable_timing=True)
+        a1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        a1.record(stream)
+        torch.cuda.synchronize()
+        return a0.elapsed_time(a1) / args.steps * 1e3
+
+    append_us = timed(lambda: pda.kv_append(k_new, v_new, k, v, bt, lens))
+    append_graph_us = None
+    if not args.no_graph:
+        # device-side cost without the host launch path: 20 appends in a graph
+        ga = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(ga, stream=s):
+            for _ in range(20):
+                pda.kv_append(k_new, v_new, k, v, bt, lens)
+        append_graph_us = timed(ga.replay) / 20
+    append_attend_us = timed(lambda: pda.paged_decode_attention_append(q, k_new, v_new, k, v, bt, lens, out, scale))
+    append_bytes = 8 * w.batch * w.num_kv_heads * w.head_dim + 8 * w.batch
+
     nbytes = w.algorithmic_bytes()
     value = nbytes / (ms_per_step * 1e-3) / 1e9
     achieved = nbytes / (split_ms * 1e-3) / 1e9
@@ -219,6 +250,11 @@ def main():
         },
         "kernels_ms": {"split": round(split_ms, 5), "merge": round(merge_ms, 5)},
         "graph_us_per_call": None if graph_us is None else round(graph_us, 2),
+        "kv_append": {
+            "us_per_call": round(append_us, 2), "bytes_per_call": append_bytes,
+            "graph_us_per_call": None if append_graph_us is None else round(append_graph_us, 2),
+            "append_then_attend_us_per_call": round(append_attend_us, 2),
+        },
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,

@@ -66,6 +66,7 @@ enum pda_status {
 #define PDA_MAX_BATCH 8192
 #define PDA_MAX_GROUP 16      /* num_q_heads / num_kv_heads                */
 #define PDA_MAX_PAGE_SIZE 1024
+#define PDA_MAX_KV_HEADS 1024
 
 /*
  * paged_decode_attention -- the decode-attention step described above.
@@ -99,6 +100,43 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
                            int32_t head_dim, int32_t page_size, int32_t num_pages,
                            int32_t max_pages_per_seq,
                            float scale, void* stream);
+
+/*
+ * pda_kv_append -- write each sequence's newest key and value into its page:
+ * the step before attention in the paper's decode loop (Method, "Kernel
+ * Customization and Multi-Request Adaptation": a small scatter kernel writes
+ * the new K/V vectors and attention then runs with the sequence length
+ * advanced by one).
+ *
+ *   k_new, v_new  bf16 [batch, num_kv_heads, head_dim], contiguous, 16-B aligned.
+ *   k_cache, v_cache, block_table, num_pages, page_size, max_pages_per_seq
+ *                 as for paged_decode_attention; the caches are written in place.
+ *   context_lens  int32 [batch] on the device, already counting the new token:
+ *                 sequence b's vectors go to position L_b - 1, i.e. page
+ *                 block_table[b, (L_b-1) / page_size], slot (L_b-1) % page_size,
+ *                 every kv head.  L_b = 0 writes nothing.
+ * Only those slots change.  Two sequences whose page tables send their new
+ * token to the same slot race (the page table must not do that).
+ * Asynchronous on `stream`; no workspace, no allocation (graph-capturable).
+ * Errors as for paged_decode_attention.
+ */
+int pda_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                  const int32_t* block_table, const int32_t* context_lens,
+                  int32_t batch, int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                  int32_t num_pages, int32_t max_pages_per_seq, void* stream);
+
+/*
+ * paged_decode_attention_append -- pda_kv_append followed by
+ * paged_decode_attention on the same stream: append the step's key/value,
+ * then attend with the length that counts them.  Arguments as for the two
+ * calls; q and out as for paged_decode_attention.
+ */
+int paged_decode_attention_append(const void* q, const void* k_new, const void* v_new,
+                                  void* k_cache, void* v_cache, const int32_t* block_table,
+                                  const int32_t* context_lens, void* out,
+                                  int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t page_size, int32_t num_pages,
+                                  int32_t max_pages_per_seq, float scale, void* stream);
 
 /*
  * pda_plan -- host-only dry run of the split planner: how the context of the

@@ -34,6 +34,10 @@ def _declare(lib: ctypes.CDLL) -> None:
     i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
     lib.paged_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp]
     lib.paged_decode_attention.restype = ctypes.c_int
+    lib.pda_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
+    lib.pda_kv_append.restype = ctypes.c_int
+    lib.paged_decode_attention_append.argtypes = [vp] * 8 + [i32] * 7 + [f32, vp]
+    lib.paged_decode_attention_append.restype = ctypes.c_int
     lib.pda_plan.argtypes = [i32, i32, i32, i32, i32, i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32),
                              ctypes.POINTER(i64)]
     lib.pda_plan.restype = ctypes.c_int
@@ -130,6 +134,54 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, 
     _check(raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
                     context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1],
                     float(scale), _stream_ptr(stream)))
+    return out
+
+
+def _check_cache_args(k_cache, v_cache, block_table, context_lens, extra):
+    import torch
+    for name, t, dt in (("k_cache", k_cache, torch.bfloat16), ("v_cache", v_cache, torch.bfloat16),
+                        ("block_table", block_table, torch.int32), ("context_lens", context_lens, torch.int32),
+                        *extra):
+        if t.dtype != dt:
+            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if k_cache.dim() != 4 or v_cache.shape != k_cache.shape or block_table.dim() != 2:
+        raise ValueError("shapes: k_cache/v_cache [N,P,Hkv,D], block_table [B,maxp]")
+
+
+def kv_append(k_new, v_new, k_cache, v_cache, block_table, context_lens, stream=None):
+    """Scatter each sequence's new key/value ([B, Hkv, D] bf16) into its page
+    slot at position context_lens[b] - 1 (the length counts the new token)."""
+    import torch
+    _check_cache_args(k_cache, v_cache, block_table, context_lens,
+                      (("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)))
+    n, p, hkv, d = k_cache.shape
+    b = block_table.shape[0]
+    if k_new.shape != (b, hkv, d) or v_new.shape != (b, hkv, d) or context_lens.shape != (b,):
+        raise ValueError("k_new/v_new must be [B, Hkv, D] and context_lens [B]")
+    _check(load().pda_kv_append(k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                block_table.data_ptr(), context_lens.data_ptr(), b, hkv, d, p, n,
+                                block_table.shape[1], _stream_ptr(stream)))
+
+
+def paged_decode_attention_append(q, k_new, v_new, k_cache, v_cache, block_table, context_lens, out, scale,
+                                  stream=None):
+    """kv_append then paged_decode_attention on the same stream."""
+    import torch
+    _check_cache_args(k_cache, v_cache, block_table, context_lens,
+                      (("q", q, torch.bfloat16), ("out", out, torch.bfloat16),
+                       ("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)))
+    b, hq, d = q.shape
+    n, p, hkv, d2 = k_cache.shape
+    if d2 != d or out.shape != q.shape or k_new.shape != (b, hkv, d) or v_new.shape != (b, hkv, d):
+        raise ValueError("inconsistent shapes")
+    _check(load().paged_decode_attention_append(
+        q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+        block_table.data_ptr(), context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n,
+        block_table.shape[1], ctypes.c_float(float(scale)), _stream_ptr(stream)))
     return out
 
 

@@ -16,6 +16,7 @@
 #include <vector>
 
 #include "pda.h"
+#include "pda_append.h"
 #include "pda_internal.h"
 
 namespace {
@@ -79,6 +80,8 @@ int check_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, in
   if (batch < 0) return fail(PDA_ERR_SHAPE, "batch must be >= 0 (got %d)", batch);
   if (hq <= 0 || hkv <= 0) return fail(PDA_ERR_SHAPE, "head counts must be positive (q %d, kv %d)", hq, hkv);
   if (hq % hkv) return fail(PDA_ERR_SHAPE, "num_q_heads %d is not a multiple of num_kv_heads %d", hq, hkv);
+  if (hkv > PDA_MAX_KV_HEADS)
+    return fail(PDA_ERR_UNSUPPORTED, "num_kv_heads %d exceeds %d", hkv, PDA_MAX_KV_HEADS);
   if (hq / hkv > PDA_MAX_GROUP)
     return fail(PDA_ERR_UNSUPPORTED, "query group %d exceeds %d", hq / hkv, PDA_MAX_GROUP);
   if (d != 64 && d != 128) return fail(PDA_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", d);
@@ -328,6 +331,60 @@ int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls) {
   *calls = static_cast<int64_t>(g_prof_recs.size());
   g_prof_recs.clear();
   return rc;
+}
+
+int pda_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                  const int32_t* block_table, const int32_t* context_lens, int32_t batch, int32_t num_kv_heads,
+                  int32_t head_dim, int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
+                  void* stream) {
+  g_err.clear();
+  int rc = check_shape(batch, num_kv_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  if (rc) return rc;
+  if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
+  if (batch == 0) return PDA_OK;
+  if (!k_new || !v_new || !k_cache || !v_cache || !block_table || !context_lens)
+    return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+  if (misaligned(k_new, 16) || misaligned(v_new, 16) || misaligned(k_cache, 16) || misaligned(v_cache, 16))
+    return fail(PDA_ERR_ALIGN, "k_new, v_new, k_cache and v_cache must be 16-byte aligned");
+  if (misaligned(block_table, 4) || misaligned(context_lens, 4))
+    return fail(PDA_ERR_ALIGN, "block_table and context_lens must be 4-byte aligned");
+  pda::AppendArgs a;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.k = static_cast<uint16_t*>(k_cache);
+  a.v = static_cast<uint16_t*>(v_cache);
+  a.bt = block_table;
+  a.lens = context_lens;
+  a.batch = batch;
+  a.hkv = num_kv_heads;
+  a.head_dim = head_dim;
+  a.page_shift = log2i(page_size);
+  a.num_pages = num_pages;
+  a.maxp = max_pages_per_seq;
+  hipError_t e = pda::launch_append_kernel(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "append kernel launch");
+  return PDA_OK;
+}
+
+int paged_decode_attention_append(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                                  void* v_cache, const int32_t* block_table, const int32_t* context_lens,
+                                  void* out, int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                  int32_t head_dim, int32_t page_size, int32_t num_pages,
+                                  int32_t max_pages_per_seq, float scale, void* stream) {
+  g_err.clear();
+  // validate the attention arguments first so that nothing is written on error
+  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  if (rc) return rc;
+  if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
+  if (batch > 0 && (!q || !out)) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if ((reinterpret_cast<uintptr_t>(q) & 15) || (reinterpret_cast<uintptr_t>(out) & 15))
+    return fail(PDA_ERR_ALIGN, "q, k_cache, v_cache and out must be 16-byte aligned");
+  if ((rc = pda_kv_append(k_new, v_new, k_cache, v_cache, block_table, context_lens, batch, num_kv_heads,
+                          head_dim, page_size, num_pages, max_pages_per_seq, stream)))
+    return rc;
+  return paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, batch, num_q_heads,
+                                num_kv_heads, head_dim, page_size, num_pages, max_pages_per_seq, scale, stream);
 }
 
 int paged_decode_attention(const void* q, const void* k_cache, const void* v_cache,

@@ -1,0 +1,69 @@
+// KV append for MI355X (gfx950): the step before decode attention in the
+// paper's decode loop (Method, "Kernel Customization and Multi-Request
+// Adaptation": a small scatter kernel writes the step's new key and value
+// vectors into the paged cache, and attention then runs with the sequence
+// length advanced by one).
+//
+// The length already counts the new token, so sequence b's vectors land at
+// position L_b - 1: page block_table[b, (L_b-1) / P], slot (L_b-1) % P, every
+// kv head.  Pure data movement of 4*Hkv*D bytes per sequence (read and
+// write), far below anything HBM-bound: the kernel is one launch of one
+// thread per 16-byte chunk, so each (sequence, kv head) row of D bf16 is
+// moved by D/8 consecutive lanes with 16-byte accesses.
+//
+// Page ids and lengths read from device memory are clamped into range (a
+// length into [0, maxp*P], a page id into [0, num_pages)), so bad device
+// contents cannot address outside the pool.
+#include "pda_append.h"
+
+namespace pda {
+namespace {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+__global__ __launch_bounds__(kAppendThreads) void append_kernel(
+    const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new, uint16_t* __restrict__ kc,
+    uint16_t* __restrict__ vc, const int32_t* __restrict__ bt, const int32_t* __restrict__ lens, int batch,
+    int hkv, int page_shift, int num_pages, int maxp) {
+  constexpr int kChunks = D / 8;                    // 16-byte chunks per row
+  const int64_t per_seq = 2 * static_cast<int64_t>(hkv) * kChunks;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * kAppendThreads + threadIdx.x;
+  if (i >= static_cast<int64_t>(batch) * per_seq) return;
+  const int b = static_cast<int>(i / per_seq);
+  const int r = static_cast<int>(i - b * per_seq);  // (K|V, kv head, chunk)
+  const int which = r / (hkv * kChunks);
+  const int g = (r / kChunks) % hkv;
+  const int chunk = r % kChunks;
+
+  const int max_ctx = maxp << page_shift;
+  int L = lens[b];
+  L = L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
+  if (L == 0) return;
+  const int t = L - 1;
+  const unsigned raw = static_cast<unsigned>(bt[static_cast<int64_t>(b) * maxp + (t >> page_shift)]);
+  const int64_t page = raw < static_cast<unsigned>(num_pages) ? raw : num_pages - 1;
+  const int slot = t & ((1 << page_shift) - 1);
+
+  const int64_t dst = (((page << page_shift) + slot) * hkv + g) * D + 8 * chunk;
+  const int64_t src = (static_cast<int64_t>(b) * hkv + g) * D + 8 * chunk;
+  const uint16_t* from = which ? v_new : k_new;
+  uint16_t* to = which ? vc : kc;
+  *reinterpret_cast<u32x4*>(to + dst) = *reinterpret_cast<const u32x4*>(from + src);
+}
+
+}  // namespace
+
+hipError_t launch_append_kernel(const AppendArgs& a, hipStream_t st) {
+  const int64_t n = static_cast<int64_t>(a.batch) * 2 * a.hkv * (a.head_dim / 8);
+  const dim3 grid(static_cast<unsigned>((n + kAppendThreads - 1) / kAppendThreads));
+  if (a.head_dim == 128)
+    hipLaunchKernelGGL((append_kernel<128>), grid, dim3(kAppendThreads), 0, st, a.k_new, a.v_new, a.k, a.v,
+                       a.bt, a.lens, a.batch, a.hkv, a.page_shift, a.num_pages, a.maxp);
+  else
+    hipLaunchKernelGGL((append_kernel<64>), grid, dim3(kAppendThreads), 0, st, a.k_new, a.v_new, a.k, a.v,
+                       a.bt, a.lens, a.batch, a.hkv, a.page_shift, a.num_pages, a.maxp);
+  return hipGetLastError();
+}
+
+}  // namespace pda

@@ -34,6 +34,7 @@ def call(ptr=16, batch=2, hq=32, hkv=8, d=128, p=16, n=64, maxp=8, scale=0.088, 
     (dict(batch=-1), SHAPE, "batch"),
     (dict(hkv=7), SHAPE, "multiple"),
     (dict(hq=0), SHAPE, "positive"),
+    (dict(hq=2048, hkv=2048), UNSUPPORTED, "num_kv_heads"),
     (dict(hq=64, hkv=2), UNSUPPORTED, "group"),
     (dict(d=96), UNSUPPORTED, "head_dim"),
     (dict(p=24), UNSUPPORTED, "page_size"),
@@ -102,3 +103,50 @@ def test_profile_read_null_pointer(lib):
     assert lib.pda_profile_read(None, None, None) == NULL
     s, m, n = B.profile_read()
     assert n == 0 and s == 0.0 and m == 0.0
+
+
+def append_call(ptr=16, batch=2, hkv=8, d=128, p=16, n=64, maxp=8, ptrs=None):
+    ptrs = ptrs or [ptr] * 6
+    return B.load().pda_kv_append(*ptrs, batch, hkv, d, p, n, maxp, None)
+
+
+@pytest.mark.parametrize("kwargs,code,text", [
+    (dict(ptr=0), NULL, "NULL"),
+    (dict(ptrs=[16, 16, 16, 16, 0, 16]), NULL, "NULL"),
+    (dict(batch=-1), SHAPE, "batch"),
+    (dict(hkv=0), SHAPE, "positive"),
+    (dict(d=96), UNSUPPORTED, "head_dim"),
+    (dict(hkv=1025), UNSUPPORTED, "num_kv_heads"),
+    (dict(p=24), UNSUPPORTED, "page_size"),
+    (dict(maxp=0), SHAPE, "positive"),
+    (dict(n=0), SHAPE, "num_pages"),
+    (dict(batch=8193), UNSUPPORTED, "batch"),
+    (dict(ptrs=[16, 24, 16, 16, 16, 16]), ALIGN, "16-byte"),
+    (dict(ptrs=[16, 16, 16, 40, 16, 16]), ALIGN, "16-byte"),
+    (dict(ptrs=[16, 16, 16, 16, 16, 18]), ALIGN, "4-byte"),
+])
+def test_kv_append_argument_errors(lib, kwargs, code, text):
+    rc = append_call(**kwargs)
+    assert rc == code, B.last_error()
+    assert text in B.last_error()
+
+
+def test_kv_append_empty_batch_is_a_noop(lib):
+    assert append_call(ptr=0, batch=0) == OK
+    assert B.last_error() == ""
+
+
+def test_append_then_attend_validates_attention_arguments_first(lib):
+    # the attention arguments are checked before the append kernel could run
+    f = B.load().paged_decode_attention_append
+    rc = f(16, 16, 16, 16, 16, 16, 16, 16, 2, 32, 7, 128, 16, 64, 8, ctypes.c_float(0.1), None)
+    assert rc == SHAPE and "multiple" in B.last_error()
+    rc = f(16, 16, 16, 16, 16, 16, 16, 16, 2, 32, 8, 128, 16, 64, 8, ctypes.c_float(math.inf), None)
+    assert rc == SCALE
+    rc = f(0, 16, 16, 16, 16, 16, 16, 16, 2, 32, 8, 128, 16, 64, 8, ctypes.c_float(0.1), None)
+    assert rc == NULL
+    rc = f(16, 16, 16, 16, 16, 16, 16, 24, 2, 32, 8, 128, 16, 64, 8, ctypes.c_float(0.1), None)
+    assert rc == ALIGN
+    rc = f(16, 0, 16, 16, 16, 16, 16, 16, 2, 32, 8, 128, 16, 64, 8, ctypes.c_float(0.1), None)
+    assert rc == NULL
+    assert f(0, 0, 0, 0, 0, 0, 0, 0, 0, 32, 8, 128, 16, 64, 8, ctypes.c_float(0.1), None) == OK

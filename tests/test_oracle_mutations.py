@@ -86,3 +86,45 @@ def test_each_mutant_is_caught(name, monkeypatch):
         except (AssertionError, ValueError, IndexError):
             failed.append("golden:" + gname)
     assert failed, f"mutant '{name}' passed every pin"
+
+
+def make_kv_append(at_len=False, slot_swap=False, kv_swap=False, write_empty=False):
+    def kv_append(k_cache, v_cache, k_new, v_new, block_table, context_lens):
+        k = np.array(k_cache, copy=True)
+        v = np.array(v_cache, copy=True)
+        p = k.shape[1]
+        for b in range(len(context_lens)):
+            length = int(context_lens[b])
+            if length == 0 and not write_empty:
+                continue
+            t = length if at_len else length - 1
+            j, r = (t % p, t // p) if slot_swap else (t // p, t % p)
+            j = min(j, block_table.shape[1] - 1)
+            r = min(r, p - 1)
+            page = int(block_table[b][j])
+            k[page, r], v[page, r] = (v_new[b], k_new[b]) if kv_swap else (k_new[b], v_new[b])
+        return k, v
+    return kv_append
+
+
+APPEND_MUTANTS = {
+    "position L instead of L-1": dict(at_len=True),
+    "page/slot swapped": dict(slot_swap=True),
+    "K and V swapped": dict(kv_swap=True),
+    "empty sequences written": dict(write_empty=True),
+}
+APPEND_PINS = [pins.test_kv_append_writes_exactly_the_new_slot,
+               pins.test_append_then_attend_equals_attend_on_the_full_cache]
+
+
+@pytest.mark.parametrize("name", list(APPEND_MUTANTS))
+def test_each_append_mutant_is_caught(name, monkeypatch):
+    monkeypatch.setattr(oracle, "kv_append", make_kv_append(**APPEND_MUTANTS[name]))
+    failed = []
+    for f in APPEND_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                f()
+        except (AssertionError, ValueError, IndexError):
+            failed.append(f.__name__)
+    assert failed, f"mutant '{name}' passed every pin"
