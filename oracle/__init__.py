@@ -31,6 +31,12 @@ chunks.  It is pinned against :func:`attend` for arbitrary chunkings.
 the new token's key and value are scattered into their page slot and the
 length already counts that token.
 
+:func:`attend_masked` is the same definition with a key range per query:
+several query tokens per sequence (the decode steps that the paper's engine
+mixes with chunked prefill, each seeing only keys up to its own position)
+and an optional sliding window (the Mistral adaptation in the paper's table
+of model-specific adaptations).
+
 Readings where the paper is silent (it prints no attention formula, page
 size, layout or tolerance): standard scaled dot-product softmax with no other
 mask than the length, KV pool layout [num_pages, P, Hkv, D], lengths that
@@ -45,7 +51,7 @@ from typing import Iterable, List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = ["bf16_to_f64", "attend", "attend_pairs", "weights", "split_merge",
-           "brute_force_tiny", "kv_append"]
+           "brute_force_tiny", "kv_append", "attend_masked", "visible_range"]
 
 
 def bf16_to_f64(bits) -> np.ndarray:
@@ -60,9 +66,10 @@ def _sigma(scale) -> float:
     return float(np.float32(scale))
 
 
-def _gather(cache_bits, block_table_row, length, page_size, g) -> np.ndarray:
-    """[L, D] fp64 rows of kv head g for tokens 0..L-1 of one sequence."""
-    t = np.arange(length)
+def _gather(cache_bits, block_table_row, length, page_size, g, start=0) -> np.ndarray:
+    """[L - start, D] fp64 rows of kv head g for tokens start..L-1 of one
+    sequence."""
+    t = np.arange(start, length)
     pages = np.asarray(block_table_row)[t // page_size].astype(np.int64)
     slots = t % page_size
     return bf16_to_f64(cache_bits[pages, slots, g, :])
@@ -250,3 +257,56 @@ def kv_append(k_cache, v_cache, k_new, v_new, block_table, context_lens):
         v[page, t % page_size] = v_new[b]
     return k, v
 
+
+
+def visible_range(length, num_queries, j, window):
+    """Keys [lo, hi) that query j of ``num_queries`` sees in a sequence of
+    ``length`` cached tokens (readings where the paper is silent):
+
+    * the queries are the sequence's last ``num_queries`` tokens, so query j
+      sits at position p = length - num_queries + j and sees keys t <= p
+      (causal, as in a decode step or a chunk of prefill);
+    * a sliding window of W > 0 tokens keeps keys p - W < t <= p (W keys
+      counting the query's own token); W = 0 means no window.
+
+    A query at a negative position (length < num_queries) sees nothing.
+    """
+    p = int(length) - int(num_queries) + int(j)
+    hi = p + 1
+    lo = max(0, hi - int(window)) if window > 0 else 0
+    return lo, max(hi, lo)
+
+
+def attend_masked(q, k_cache, v_cache, block_table, context_lens, scale, window=0):
+    """Decode attention with several query tokens per sequence and an
+    optional sliding window, in fp64.
+
+    q: uint16 [B, Tq, Hq, D] (Tq query tokens per sequence, in position
+    order); caches, block_table, context_lens, scale as for :func:`attend`.
+    For sequence b, query j and head h (kv head g = h // G), the softmax runs
+    over the keys of :func:`visible_range`; a query that sees no key gets a
+    zero row (lse = -inf).  Returns (out float64 [B, Tq, Hq, D], lse [B, Tq, Hq]).
+    """
+    bsz, tq, hq, d = q.shape
+    _, page_size, hkv, _ = k_cache.shape
+    group = hq // hkv
+    sigma = _sigma(scale)
+    out = np.zeros((bsz, tq, hq, d))
+    lse = np.full((bsz, tq, hq), -np.inf)
+    for b in range(bsz):
+        length = int(context_lens[b])
+        for j in range(tq):
+            lo, hi = visible_range(length, tq, j, window)
+            if hi == lo:
+                continue
+            for g in range(hkv):
+                kt = _gather(k_cache, block_table[b], hi, page_size, g, start=lo)
+                vt = _gather(v_cache, block_table[b], hi, page_size, g, start=lo)
+                qg = bf16_to_f64(q[b, j, g * group:(g + 1) * group, :])
+                s = sigma * (qg @ kt.T)
+                m = s.max(axis=1, keepdims=True)
+                e = np.exp(s - m)
+                den = e.sum(axis=1, keepdims=True)
+                out[b, j, g * group:(g + 1) * group] = (e / den) @ vt
+                lse[b, j, g * group:(g + 1) * group] = (m + np.log(den))[:, 0]
+    return out, lse

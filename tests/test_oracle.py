@@ -247,3 +247,89 @@ def test_append_then_attend_equals_attend_on_the_full_cache():
     ref, _ = run(w)
     assert np.array_equal(a, ref)
 
+
+
+# ------------------------------------------- several query tokens, sliding window
+def masked(w, window=None):
+    q = w.q if w.q.ndim == 4 else w.q[:, None]
+    return oracle.attend_masked(q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale,
+                                w.window if window is None else window)
+
+
+def test_masked_single_query_without_window_is_attend():
+    w = small([1, 33, 300, 0, 17], seed=40)
+    ref, lse_ref = run(w)
+    out, lse = masked(w, 0)
+    assert np.array_equal(out[:, 0], ref) and np.array_equal(lse[:, 0], lse_ref)
+    out, _ = masked(w, 300)  # a window as long as the longest sequence cuts nothing
+    assert np.array_equal(out[:, 0], ref)
+
+
+def test_masked_queries_are_causal_prefixes():
+    # query j of Tq equals one query over the first L - Tq + 1 + j tokens
+    tq = 3
+    w = small([2, 40, 77, 129], hq=8, hkv=2, num_queries=tq, seed=41, poison=False)
+    out, _ = masked(w, 0)
+    for j in range(tq):
+        lens = np.maximum(w.context_lens - tq + 1 + j, 0).astype(np.int32)
+        ref, _ = oracle.attend(np.ascontiguousarray(w.q[:, j]), w.k_cache, w.v_cache, w.block_table, lens,
+                               w.scale)
+        np.testing.assert_allclose(out[:, j], ref, rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("tq,window", [(1, 5), (2, 16), (4, 1), (3, 40), (2, 0)])
+def test_masked_matches_torch_sdpa_with_boolean_mask(tq, window):
+    w = small([3, 50, 97, 200], hq=8, hkv=2, d=64, num_queries=tq, window=window, seed=42, poison=False)
+    out, _ = masked(w)
+    dense = flat_gather_dense(w)
+    q4 = w.q if w.q.ndim == 4 else w.q[:, None]
+    for b in range(w.batch):
+        L = int(w.context_lens[b])
+        kd, vd = dense[b]
+        pos = torch.arange(tq, dtype=torch.int64)[:, None] + (L - tq)   # query positions
+        key = torch.arange(L, dtype=torch.int64)[None, :]
+        allowed = key <= pos
+        if window:
+            allowed &= key > pos - window
+        qd = torch.from_numpy(oracle.bf16_to_f64(q4[b])).permute(1, 0, 2)        # [Hq, Tq, D]
+        kt = torch.from_numpy(kd).permute(1, 0, 2)                               # [Hq, L, D]
+        vt = torch.from_numpy(vd).permute(1, 0, 2)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            qd, kt, vt, attn_mask=allowed, scale=float(np.float32(w.scale))).permute(1, 0, 2).numpy()
+        rows = allowed.any(dim=1).numpy()
+        np.testing.assert_allclose(out[b][rows], ref[rows], rtol=0, atol=1e-12)
+        assert np.array_equal(out[b][~rows], np.zeros_like(out[b][~rows]))
+
+
+def test_window_of_one_returns_the_own_value():
+    w = small([5, 16, 33], hq=8, hkv=2, num_queries=2, window=1, seed=43, poison=False)
+    out, _ = masked(w)
+    g = 4
+    for b in range(w.batch):
+        L = int(w.context_lens[b])
+        for j in range(2):
+            t = L - 2 + j
+            page, slot = w.block_table[b, t // 16], t % 16
+            for h in range(8):
+                assert np.array_equal(out[b, j, h], oracle.bf16_to_f64(w.v_cache[page, slot, h // g]))
+
+
+def test_window_released_pages_are_never_read():
+    lens = [100, 300, 47, 64]
+    clean = small(lens, num_queries=2, window=40, seed=44, poison=False)
+    dirty = small(lens, num_queries=2, window=40, seed=44, poison=True)
+    assert (dirty.block_table[1, :10] == -1).all()   # tokens < 259 are outside every window
+    a, _ = masked(clean)
+    b_, _ = masked(dirty)
+    assert np.isfinite(b_).all() and np.array_equal(a, b_)
+
+
+def test_queries_before_the_first_token_are_zero():
+    w = small([0, 1, 2, 5], hq=4, hkv=2, num_queries=3, seed=45)
+    out, lse = masked(w, 0)
+    for b, L in enumerate(w.context_lens):
+        for j in range(3):
+            if L - 3 + j < 0:
+                assert np.array_equal(out[b, j], np.zeros_like(out[b, j])) and np.isneginf(lse[b, j]).all()
+            else:
+                assert np.isfinite(lse[b, j]).all()

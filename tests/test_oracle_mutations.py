@@ -1,5 +1,7 @@
 """The oracle's pins are sharp: plant a plausible mistake in (a copy of) the
 oracle's arithmetic, on the CPU, and check that at least one pin fails."""
+import functools
+
 import numpy as np
 import pytest
 
@@ -127,4 +129,53 @@ def test_each_append_mutant_is_caught(name, monkeypatch):
                 f()
         except (AssertionError, ValueError, IndexError):
             failed.append(f.__name__)
+    assert failed, f"mutant '{name}' passed every pin"
+
+
+def make_visible_range(window_off=False, causal_off=False, from_start=False):
+    def visible_range(length, num_queries, j, window):
+        p = int(j) if from_start else int(length) - int(num_queries) + int(j)
+        hi = p if causal_off else p + 1
+        if window > 0:
+            lo = max(0, hi - int(window) + (1 if window_off else 0))
+        else:
+            lo = 0
+        return lo, max(hi, lo)
+    return visible_range
+
+
+def reversed_queries(orig):
+    def attend_masked(q, *args, **kw):
+        return orig(np.ascontiguousarray(q[:, ::-1]), *args, **kw)
+    return attend_masked
+
+
+MASK_PINS = [
+    pins.test_masked_single_query_without_window_is_attend,
+    pins.test_masked_queries_are_causal_prefixes,
+    *[functools.partial(pins.test_masked_matches_torch_sdpa_with_boolean_mask, tq, wdw)
+      for tq, wdw in [(1, 5), (2, 16), (4, 1), (3, 40), (2, 0)]],
+    pins.test_window_of_one_returns_the_own_value,
+    pins.test_window_released_pages_are_never_read,
+    pins.test_queries_before_the_first_token_are_zero,
+]
+MASK_MUTANTS = {
+    "window one token short": ("visible_range", make_visible_range(window_off=True)),
+    "query sees its own token excluded": ("visible_range", make_visible_range(causal_off=True)),
+    "query positions from the start": ("visible_range", make_visible_range(from_start=True)),
+    "query tokens in reverse order": ("attend_masked", reversed_queries(oracle.attend_masked)),
+}
+
+
+@pytest.mark.parametrize("name", list(MASK_MUTANTS))
+def test_each_masked_mutant_is_caught(name, monkeypatch):
+    attr, fn = MASK_MUTANTS[name]
+    monkeypatch.setattr(oracle, attr, fn)
+    failed = []
+    for f in MASK_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                f()
+        except (AssertionError, ValueError, IndexError):
+            failed.append(getattr(f, "__name__", str(f)))
     assert failed, f"mutant '{name}' passed every pin"

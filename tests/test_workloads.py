@@ -77,3 +77,26 @@ def test_permute_pages_keeps_logical_kv():
             a = w.k_cache[w.block_table[b, t // 16], t % 16]
             c = w2.k_cache[w2.block_table[b, t // 16], t % 16]
             assert np.array_equal(a, c)
+
+
+def test_variant_workloads_shapes_and_bytes():
+    lens = W.lengths_of("window")
+    assert (lens == 16384).all()
+    w = W.build([100, 5, 0], 8, 2, 64, 16, seed=3, num_queries=3, window=10, poison=False)
+    assert w.q.shape == (3, 3, 8, 64) and w.num_queries == 3 and w.window == 10
+    assert w.num_q_heads == 8 and w.head_dim == 64
+    # union of the visible ranges: [L - Tq + 1 - W, L) clipped at 0
+    assert W.window_start(100, 3, 10) == 88 and W.window_start(5, 3, 10) == 0
+    live = (100 - 88) + 5
+    pages = (7 - 88 // 16) + 1
+    assert w.algorithmic_bytes() == 4 * 64 * 2 * live + 4 * 3 * 3 * 8 * 64 + 4 * pages + 4 * 3
+
+
+def test_window_poison_releases_whole_pages_only():
+    w = W.build([100, 40], 8, 2, 64, 16, seed=4, num_queries=2, window=20)
+    # sequence 0 sees tokens 79..99: pages 0..3 (tokens < 64) are released, page 4 holds 79
+    assert (w.block_table[0, :4] == -1).all() and (w.block_table[0, 4:7] >= 0).all()
+    page4 = w.block_table[0, 4]
+    assert not np.isnan(W.bf16_bits_to_f32(w.k_cache[page4, :16])).any()   # live page: all finite
+    # sequence 1 (L = 40) sees tokens 19..39: only page 0 (tokens < 16) is released
+    assert w.block_table[1, 0] == -1 and (w.block_table[1, 1:3] >= 0).all()

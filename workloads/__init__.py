@@ -94,6 +94,8 @@ class Config:
     pool: str               # "perm:<pool_pages>", "exact", "holes:<frac>"
     q_std: float = 1.0
     description: str = ""
+    num_queries: int = 1    # query tokens per sequence (causal among them)
+    window: int = 0         # sliding window in tokens, 0 = none
 
     @property
     def group(self) -> int:
@@ -122,33 +124,60 @@ CONFIGS: Dict[str, Config] = {
         description="batch 256, 40:8 heads (G=5), D=128, L~Zipf(1.2) clipped "
                     "to [16,32768] and never a multiple of 32, P=32, shuffled "
                     "pool with 10% unused holes"),
+    # variants of the same path (not among the five workloads above)
+    "window": Config(
+        "window", 64, 32, 8, 128, 16, 5, "fixed:16384", "exact", window=4096,
+        description="Mistral-7B-shaped layer with a 4096-token sliding window, "
+                    "batch 64, 32:8 heads, D=128, L=16384, P=16"),
+    "multiq": Config(
+        "multiq", 64, 32, 8, 128, 16, 6, "uniform:128:8192", "exact", num_queries=4,
+        description="batch 64, 32:8 heads, D=128, L~U[128,8192], P=16, four "
+                    "causal query tokens per sequence (G x 4 = 16 columns)"),
+    "gqa16": Config(
+        "gqa16", 32, 32, 2, 128, 16, 7, "fixed:32768", "exact",
+        description="GLM-4-shaped 32:2 heads (G=16), batch 32, D=128, "
+                    "L=32768, P=16"),
 }
 CONFIG_ORDER = ["tiny", "llama8b", "batched", "long70b", "ragged"]
+VARIANT_ORDER = ["window", "multiq", "gqa16"]
+
+
+def window_start(length: int, num_queries: int, window: int) -> int:
+    """First token any query of the sequence can see: with a window W > 0
+    the earliest query (position L - Tq) sees keys from L - Tq + 1 - W on."""
+    if window <= 0:
+        return 0
+    return max(0, int(length) - int(num_queries) + 1 - int(window))
 
 
 @dataclasses.dataclass
 class Workload:
     """Inputs of one paged decode-attention call (host numpy arrays)."""
 
-    q: np.ndarray             # uint16 [B, Hq, D]
+    q: np.ndarray             # uint16 [B, Hq, D], or [B, Tq, Hq, D] with several query tokens
     k_cache: np.ndarray       # uint16 [N, P, Hkv, D]
     v_cache: np.ndarray       # uint16 [N, P, Hkv, D]
     block_table: np.ndarray   # int32 [B, maxp]
     context_lens: np.ndarray  # int32 [B]
     scale: np.float32
     name: str = "custom"
+    window: int = 0           # sliding window in tokens, 0 = none
 
     @property
     def batch(self) -> int:
         return self.q.shape[0]
 
     @property
+    def num_queries(self) -> int:
+        return self.q.shape[1] if self.q.ndim == 4 else 1
+
+    @property
     def num_q_heads(self) -> int:
-        return self.q.shape[1]
+        return self.q.shape[-2]
 
     @property
     def head_dim(self) -> int:
-        return self.q.shape[2]
+        return self.q.shape[-1]
 
     @property
     def num_kv_heads(self) -> int:
@@ -167,13 +196,16 @@ class Workload:
         return self.block_table.shape[1]
 
     def algorithmic_bytes(self) -> int:
-        """Bytes the operation must move at minimum: each cached K and V
-        element of the live tokens once (shared by the GQA group), q in, out
-        out, the used page ids and the lengths."""
+        """Bytes the operation must move at minimum: each K and V element
+        that some query sees once (shared by the GQA group and the query
+        tokens), q in, out out, the page ids of those tokens and the lengths."""
         lens = self.context_lens.astype(np.int64)
         d, hkv, hq, b = self.head_dim, self.num_kv_heads, self.num_q_heads, self.batch
-        pages = int(np.sum((lens + self.page_size - 1) // self.page_size))
-        return int(4 * d * hkv * int(lens.sum()) + 2 * 2 * b * hq * d + 4 * pages + 4 * b)
+        p, tq = self.page_size, self.num_queries
+        start = np.array([window_start(x, tq, self.window) for x in lens], dtype=np.int64)
+        live = np.maximum(lens - start, 0)
+        pages = int(np.sum(np.where(lens > 0, (lens + p - 1) // p - start // p, 0)))
+        return int(4 * d * hkv * int(live.sum()) + 2 * 2 * b * tq * hq * d + 4 * pages + 4 * b)
 
 
 def _draw_lengths(cfg: Config, rng: np.random.Generator) -> np.ndarray:
@@ -207,6 +239,8 @@ def build(
     max_pages: Optional[int] = None,
     name: str = "custom",
     rng: Optional[np.random.Generator] = None,
+    num_queries: int = 1,
+    window: int = 0,
 ) -> Workload:
     """Build a workload for explicit lengths.
 
@@ -216,6 +250,12 @@ def build(
     sequence order from a random permutation, the rest unused).
     With ``poison`` every pool slot that no live token uses (unused pages
     and the tail slots of each last page) holds bf16 NaN.
+
+    ``num_queries`` > 1 makes q ``[B, Tq, Hq, D]``.  With a sliding
+    ``window`` and ``poison``, pages that lie wholly before the first token
+    any query sees are released: their page-table entries become -1 and,
+    unless another sequence uses them, their contents NaN (a serving engine
+    may hand such pages to other requests).
     """
     if rng is None:
         rng = np.random.Generator(np.random.PCG64(seed))
@@ -248,13 +288,19 @@ def build(
     for i in range(b):
         bt[i, : npages[i]] = perm[cursor: cursor + npages[i]]
         cursor += int(npages[i])
-    q = _normal_bf16(rng, (b, num_q_heads, head_dim), q_std)
+    qshape = (b, num_q_heads, head_dim) if num_queries == 1 else (b, num_queries, num_q_heads, head_dim)
+    q = _normal_bf16(rng, qshape, q_std)
     k = _normal_bf16(rng, (n_pool, page_size, num_kv_heads, head_dim))
     v = _normal_bf16(rng, (n_pool, page_size, num_kv_heads, head_dim))
     if poison:
+        if window > 0:
+            for i in range(b):
+                first = window_start(int(lens[i]), num_queries, window) // page_size
+                bt[i, :first] = -1
         used = np.zeros(n_pool, dtype=bool)
         for i in range(b):
-            used[bt[i, : npages[i]]] = True
+            row = bt[i, : npages[i]]
+            used[row[row >= 0]] = True
             tail = int(lens[i] % page_size)
             if tail:
                 last = bt[i, npages[i] - 1]
@@ -265,7 +311,8 @@ def build(
     if scale is None:
         scale = 1.0 / math.sqrt(head_dim)
     return Workload(q=q, k_cache=k, v_cache=v, block_table=bt,
-                    context_lens=lens.astype(np.int32), scale=np.float32(scale), name=name)
+                    context_lens=lens.astype(np.int32), scale=np.float32(scale), name=name,
+                    window=int(window))
 
 
 def make(name: str, *, poison: bool = True, seed: Optional[int] = None) -> Workload:
@@ -274,7 +321,8 @@ def make(name: str, *, poison: bool = True, seed: Optional[int] = None) -> Workl
     rng = np.random.Generator(np.random.PCG64(cfg.seed if seed is None else seed))
     lens = _draw_lengths(cfg, rng)
     return build(lens, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.page_size,
-                 cfg.seed, pool=cfg.pool, q_std=cfg.q_std, poison=poison, name=name, rng=rng)
+                 cfg.seed, pool=cfg.pool, q_std=cfg.q_std, poison=poison, name=name, rng=rng,
+                 num_queries=cfg.num_queries, window=cfg.window)
 
 
 def lengths_of(name: str, seed: Optional[int] = None) -> np.ndarray:
