@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long70b",
-                    choices=["tiny", "llama8b", "batched", "long70b", "ragged"])
+                    choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the oracle cpu_baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -67,6 +67,7 @@ def cpu_baseline(w, budget_s):
     same workload until the budget is used; report GB/s of algorithmic bytes
     processed."""
     import oracle
+    variant = w.num_queries > 1 or w.window > 0
     try:
         from threadpoolctl import threadpool_limits
         limiter = threadpool_limits(limits=1)
@@ -79,13 +80,30 @@ def cpu_baseline(w, budget_s):
     rng.shuffle(pairs)
     done, nbytes = [], 0
     t0 = time.perf_counter()
-    for b, kv in pairs:
-        oracle.attend_pairs(w.q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale, [(b, kv)])
-        L = int(w.context_lens[b])
-        nbytes += 4 * d * L + 4 * g * d + 4 * ((L + w.page_size - 1) // w.page_size) + 4
-        done.append((b, kv))
-        if time.perf_counter() - t0 >= budget_s:
-            break
+    if variant:
+        # whole sequences through the masked definition (all kv heads at once)
+        import workloads as W
+        pairs = list(range(w.batch))
+        rng.shuffle(pairs)
+        q4 = w.q if w.q.ndim == 4 else w.q[:, None]
+        for b in pairs:
+            oracle.attend_masked(q4[b:b + 1], w.k_cache, w.v_cache, w.block_table[b:b + 1],
+                                 w.context_lens[b:b + 1], w.scale, w.window)
+            L = int(w.context_lens[b])
+            lo = W.window_start(L, w.num_queries, w.window)
+            nbytes += (4 * d * w.num_kv_heads * (L - lo) + 4 * w.num_queries * w.num_q_heads * d
+                       + 4 * ((L + w.page_size - 1) // w.page_size - lo // w.page_size) + 4)
+            done.append(b)
+            if time.perf_counter() - t0 >= budget_s:
+                break
+    else:
+        for b, kv in pairs:
+            oracle.attend_pairs(w.q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale, [(b, kv)])
+            L = int(w.context_lens[b])
+            nbytes += 4 * d * L + 4 * g * d + 4 * ((L + w.page_size - 1) // w.page_size) + 4
+            done.append((b, kv))
+            if time.perf_counter() - t0 >= budget_s:
+                break
     dt = time.perf_counter() - t0
     if limiter is not None:
         limiter.unregister() if hasattr(limiter, "unregister") else None
@@ -95,7 +113,8 @@ def cpu_baseline(w, budget_s):
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": f"{len(done)} of {total_pairs} (sequence, kv head) pairs of the same workload, "
+        "sample": f"{len(done)} of {total_pairs} {'sequences' if variant else '(sequence, kv head) pairs'} "
+                  f"of the same workload, "
                   f"{dt:.1f} s single-threaded fp64 numpy; host has {os.cpu_count()} logical cpus",
         "us_per_call_equiv": round(dt / len(done) * total_pairs * 1e6, 1),
     }
@@ -133,8 +152,17 @@ def main():
     scale = float(w.scale)
     stream = torch.cuda.current_stream()
 
+    variant = w.num_queries > 1 or w.window > 0
+    if variant:
+        if q.dim() == 3:
+            q = q.unsqueeze(1).contiguous()
+        out = torch.empty(tuple(q.shape), dtype=torch.bfloat16, device=dev)
+
     def call():
-        pda.paged_decode_attention(q, k, v, bt, lens, out, scale)
+        if variant:
+            pda.paged_decode_attention_ext(q, k, v, bt, lens, out, scale, window=w.window)
+        else:
+            pda.paged_decode_attention(q, k, v, bt, lens, out, scale)
 
     for _ in range(args.warmup):
         call()
@@ -170,7 +198,7 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=s):
             for _ in range(20):
-                pda.paged_decode_attention(q, k, v, bt, lens, out, scale)
+                call()
         g.replay()
         torch.cuda.synchronize()
         reps = max(1, args.steps // 20)
@@ -211,7 +239,10 @@ def main():
             for _ in range(20):
                 pda.kv_append(k_new, v_new, k, v, bt, lens)
         append_graph_us = timed(ga.replay) / 20
-    append_attend_us = timed(lambda: pda.paged_decode_attention_append(q, k_new, v_new, k, v, bt, lens, out, scale))
+    append_attend_us = None
+    if not variant:
+        append_attend_us = timed(
+            lambda: pda.paged_decode_attention_append(q, k_new, v_new, k, v, bt, lens, out, scale))
     append_bytes = 8 * w.batch * w.num_kv_heads * w.head_dim + 8 * w.batch
 
     nbytes = w.algorithmic_bytes()
@@ -245,6 +276,7 @@ def main():
             "workload": args.workload,
             "batch": w.batch, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
             "head_dim": w.head_dim, "page_size": w.page_size,
+            "num_queries": w.num_queries, "window": w.window,
             "total_context_tokens": int(w.context_lens.astype(np.int64).sum()),
             "algorithmic_bytes": nbytes, "parallelism": "single GPU", "device": gpu_name,
         },
@@ -253,7 +285,7 @@ def main():
         "kv_append": {
             "us_per_call": round(append_us, 2), "bytes_per_call": append_bytes,
             "graph_us_per_call": None if append_graph_us is None else round(append_graph_us, 2),
-            "append_then_attend_us_per_call": round(append_attend_us, 2),
+            "append_then_attend_us_per_call": None if append_attend_us is None else round(append_attend_us, 2),
         },
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",

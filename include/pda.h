@@ -102,6 +102,39 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
                            float scale, void* stream);
 
 /*
+ * paged_decode_attention_ext -- the same step with a key range per query:
+ * several query tokens per sequence and an optional sliding window.  The
+ * paper's engine mixes chunked prefill with decode steps (Method, "Kernel
+ * Customization and Multi-Request Adaptation") and adapts attention to a
+ * sliding window for Mistral (its table of model-specific adaptations); it
+ * defines neither, so this is the reading implemented:
+ *
+ *   q, out        bf16 [batch, num_queries, num_q_heads, head_dim], contiguous.
+ *                 The num_queries query tokens are the sequence's last ones:
+ *                 query j sits at position L_b - num_queries + j and sees keys
+ *                 t <= that position (causal).  The new tokens must already be
+ *                 in the cache and counted in context_lens.
+ *   window        0: no window.  W > 0: the query at position p sees only
+ *                 keys p - W < t <= p (W keys, its own included).  Pages that
+ *                 lie wholly before the first key any query of the sequence
+ *                 sees are never read: their block_table entries may be stale
+ *                 or -1.
+ *   num_queries   1 .. 16, with num_queries * (num_q_heads / num_kv_heads) <= 16
+ *                 (one matrix-core column per query token and head);
+ *                 otherwise PDA_ERR_UNSUPPORTED.
+ * A query that sees no key (L_b < num_queries, or L_b = 0) gets a zero row.
+ * Everything else -- layout, ownership, errors, workspace, capture -- is as
+ * for paged_decode_attention, which is this call with num_queries = 1 and
+ * window = 0.
+ */
+int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v_cache,
+                               const int32_t* block_table, const int32_t* context_lens, void* out,
+                               int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                               int32_t head_dim, int32_t page_size, int32_t num_pages,
+                               int32_t max_pages_per_seq, int32_t num_queries, int32_t window,
+                               float scale, void* stream);
+
+/*
  * pda_kv_append -- write each sequence's newest key and value into its page:
  * the step before attention in the paper's decode loop (Method, "Kernel
  * Customization and Multi-Request Adaptation": a small scatter kernel writes
@@ -145,7 +178,8 @@ int paged_decode_attention_append(const void* q, const void* k_new, const void* 
  *   num_cus      compute units of the target device (256 on MI355X).
  *   grid_blocks  out: workgroups of the split kernel.
  *   waves        out: waves (workers) in that grid.
- *   workspace_bytes out: device workspace the call needs for this shape.
+ *   workspace_bytes out: device workspace a call with this shape may need,
+ *                for any num_queries of paged_decode_attention_ext.
  * Returns PDA_OK or an argument error as paged_decode_attention would.
  */
 int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
@@ -154,8 +188,8 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
 
 /*
  * pda_workspace_reserve -- grow the workspace of (current device, stream) so
- * that a later call with this shape allocates nothing (e.g. before graph
- * capture).  Synchronous; may call hipMalloc.
+ * that a later call with this shape (any num_queries and window) allocates
+ * nothing (e.g. before graph capture).  Synchronous; may call hipMalloc.
  */
 int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t head_dim, int32_t page_size, int32_t max_pages_per_seq,

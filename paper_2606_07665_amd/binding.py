@@ -34,6 +34,8 @@ def _declare(lib: ctypes.CDLL) -> None:
     i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
     lib.paged_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp]
     lib.paged_decode_attention.restype = ctypes.c_int
+    lib.paged_decode_attention_ext.argtypes = [vp] * 6 + [i32] * 9 + [f32, vp]
+    lib.paged_decode_attention_ext.restype = ctypes.c_int
     lib.pda_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
     lib.pda_kv_append.restype = ctypes.c_int
     lib.paged_decode_attention_append.argtypes = [vp] * 8 + [i32] * 7 + [f32, vp]
@@ -134,6 +136,31 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, 
     _check(raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
                     context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1],
                     float(scale), _stream_ptr(stream)))
+    return out
+
+
+def paged_decode_attention_ext(q, k_cache, v_cache, block_table, context_lens, out, scale, window=0,
+                               stream=None):
+    """Several causal query tokens per sequence and an optional sliding window.
+
+    q, out: bf16 [B, Tq, Hq, D] (the sequence's last Tq tokens; query j sits
+    at position L - Tq + j and sees keys up to it); ``window`` 0 = none, W > 0
+    = the last W keys up to the query's position.  Other arguments as for
+    :func:`paged_decode_attention`.
+    """
+    import torch
+    _check_cache_args(k_cache, v_cache, block_table, context_lens,
+                      (("q", q, torch.bfloat16), ("out", out, torch.bfloat16)))
+    if q.dim() != 4 or out.shape != q.shape:
+        raise ValueError("q and out must be [B, Tq, Hq, D]")
+    b, tq, hq, d = q.shape
+    n, p, hkv, d2 = k_cache.shape
+    if d2 != d or block_table.shape[0] != b or context_lens.shape != (b,):
+        raise ValueError("inconsistent shapes between q, caches, block_table and context_lens")
+    _check(load().paged_decode_attention_ext(
+        q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(),
+        out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1], tq, int(window), ctypes.c_float(float(scale)),
+        _stream_ptr(stream)))
     return out
 
 

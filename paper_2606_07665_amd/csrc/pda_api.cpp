@@ -119,10 +119,11 @@ int heads_per_group(int hkv) {
 // waves; as many workgroups as fill the device (blocks_per_cu per CU), but
 // none with fewer than min_steps 32-token steps per wave at the largest
 // context the page table allows.  Partial slots: one per (workgroup,
-// sequence piece), at most grid + batch * kv-head groups.
-Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus) {
+// sequence piece), at most grid + batch * kv-head groups, each holding `cols`
+// (query token, head) rows per kv head.
+Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus,
+               int cols) {
   Plan pl;
-  const int group = hq / hkv;
   pl.hgs = heads_per_group(hkv);
   const int phases = pl.hgs >= pda::kMaxWaves ? 1 : pda::kMaxWaves / pl.hgs;
   pl.waves = pl.hgs * phases;
@@ -136,7 +137,7 @@ Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int
   if (blocks < 1) blocks = 1;
   pl.grid = static_cast<int>(blocks);
   pl.slots = static_cast<int64_t>(pl.grid) + static_cast<int64_t>(batch) * ngroups;
-  const int64_t rows = pl.slots * pl.hgs * group;
+  const int64_t rows = pl.slots * pl.hgs * cols;
   pl.off_acc = 0;
   pl.off_ml = align256(rows * d * 4);
   pl.off_pref = pl.off_ml + align256(rows * 2 * 4);
@@ -236,7 +237,8 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
   int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (num_cus <= 0) return fail(PDA_ERR_SHAPE, "num_cus must be positive");
-  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus);
+  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus,
+                      pda::kMaxCols);
   *grid_blocks = batch ? pl.grid : 0;
   *waves = batch ? pl.grid * pl.waves : 0;
   *workspace_bytes = batch ? pl.bytes : 0;
@@ -254,7 +256,9 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   int cus = 0;
   if ((rc = device_cus(dev, &cus))) return rc;
-  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
+  // sized for the most (query token, head) columns, so any num_queries fits
+  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
+                      pda::kMaxCols);
   void* ptr = nullptr;
   return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, &ptr);
 }
@@ -392,10 +396,25 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
                            int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                            int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq, float scale,
                            void* stream) {
+  return paged_decode_attention_ext(q, k_cache, v_cache, block_table, context_lens, out, batch, num_q_heads,
+                                    num_kv_heads, head_dim, page_size, num_pages, max_pages_per_seq, 1, 0,
+                                    scale, stream);
+}
+
+int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v_cache,
+                               const int32_t* block_table, const int32_t* context_lens, void* out,
+                               int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                               int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
+                               int32_t num_queries, int32_t window, float scale, void* stream) {
   g_err.clear();
   int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
+  if (num_queries < 1) return fail(PDA_ERR_SHAPE, "num_queries must be >= 1 (got %d)", num_queries);
+  if (window < 0) return fail(PDA_ERR_SHAPE, "window must be >= 0 (got %d)", window);
+  if (num_queries > pda::kMaxCols || num_queries * (num_q_heads / num_kv_heads) > pda::kMaxCols)
+    return fail(PDA_ERR_UNSUPPORTED, "num_queries %d x query group %d exceeds %d", num_queries,
+                num_q_heads / num_kv_heads, pda::kMaxCols);
   if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
   if (batch == 0) return PDA_OK;
   if (!q || !k_cache || !v_cache || !block_table || !context_lens || !out)
@@ -411,7 +430,8 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   int cus = 0;
   if ((rc = device_cus(dev, &cus))) return rc;
-  const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
+  const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
+                            num_queries * (num_q_heads / num_kv_heads));
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
   if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;
@@ -439,6 +459,8 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
   a.hgs = pl.hgs;
   a.min_steps = min_steps_per_wave();
   a.scale = scale;
+  a.nq = num_queries;
+  a.window = window;
 
   Rec rec{nullptr, nullptr, nullptr};
   bool prof = false;

@@ -12,6 +12,7 @@ constexpr int kMaxWaves = 8;              // waves per attention workgroup (at m
 constexpr int kMaxBlockThreads = 64 * kMaxWaves;
 constexpr int kMergeThreads = 256;
 constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per CU on gfx950
+constexpr int kMaxCols = 16;              // MFMA columns: query tokens x heads of a kv head
 
 struct LaunchArgs {
   const uint16_t* q;
@@ -20,8 +21,8 @@ struct LaunchArgs {
   const int32_t* bt;
   const int32_t* lens;
   uint16_t* out;
-  float* ws_acc;      // [slots, hgs, group, head_dim] partial accumulators
-  float* ws_ml;       // [slots, hgs, group, 2] partial (max in log2 units, sum)
+  float* ws_acc;      // [slots, hgs, nq * group, head_dim] partial accumulators
+  float* ws_ml;       // [slots, hgs, nq * group, 2] partial (max in log2 units, sum)
   int32_t* ws_pref;   // [batch + 1] steps prefix, written by the attention kernel
   int batch, hq, hkv, group, head_dim, page_shift, num_pages, maxp;
   int hgs;            // kv heads per workgroup (a divisor of hkv, at most 8)
@@ -29,6 +30,8 @@ struct LaunchArgs {
   int grid;           // workgroups of the attention kernel
   int min_steps;      // fewest 32-token steps per wave
   float scale;
+  int nq;      // query tokens per sequence (causal among them)
+  int window;  // sliding window in tokens, 0 = none
 };
 
 hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st);

@@ -81,6 +81,21 @@ __device__ __forceinline__ int clamp_len(int L, int max_ctx) {
   return L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
 }
 
+// Key range of a sequence.  Its nq query tokens are its last nq tokens:
+// query j sits at position L - nq + j and sees keys up to that position, and
+// with a sliding window of W > 0 tokens only the W keys ending there.  The
+// first key any query sees is seq_start; the steps of the sequence are the
+// 32-token steps from the one holding seq_start to the end.
+__device__ __forceinline__ int seq_start(int L, int nq, int window) {
+  if (window <= 0) return 0;
+  const int s = L - nq + 1 - window;
+  return s > 0 ? s : 0;
+}
+
+__device__ __forceinline__ int seq_steps(int L, int nq, int window) {
+  return (L + kStep - 1) / kStep - seq_start(L, nq, window) / kStep;
+}
+
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
@@ -131,13 +146,14 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
     const int32_t* __restrict__ lens, uint16_t* __restrict__ out,
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_pref,
     int batch, int hq, int hkv, int group, int hgs, int page_shift, int num_pages, int maxp,
-    int min_steps, float scale_log2) {
+    int min_steps, float scale_log2, int nq, int window) {
   using S = Shape<D>;
   extern __shared__ __align__(16) unsigned char smem[];
   const int nthreads = blockDim.x;
   const int nwaves = nthreads >> 6;
   const int phases = nwaves / hgs;  // waves per kv head, interleaving steps
   const int ngroups = hkv / hgs;    // kv-head groups per sequence
+  const int ncols = group * nq;     // MFMA columns in use: (query token, head of the group)
   int32_t* pref = reinterpret_cast<int32_t*>(smem + pref_offset<D>(nwaves));
   float* ml_x = reinterpret_cast<float*>(smem + ml_offset<D>(nwaves));
   int32_t* scan = reinterpret_cast<int32_t*>(smem);  // reuses the tiles before the loop
@@ -152,7 +168,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
     const int lo = tid * per;
     const int hi = min(batch, lo + per);
     int sum = 0;
-    for (int b = lo; b < hi; ++b) sum += (clamp_len(lens[b], max_ctx) + kStep - 1) / kStep;
+    for (int b = lo; b < hi; ++b) sum += seq_steps(clamp_len(lens[b], max_ctx), nq, window);
     scan[tid] = sum;
     __syncthreads();
     for (int off = 1; off < nthreads; off <<= 1) {
@@ -164,7 +180,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
     int run = scan[tid] - sum;
     for (int b = lo; b < hi; ++b) {
       pref[b] = run;
-      run += (clamp_len(lens[b], max_ctx) + kStep - 1) / kStep;
+      run += seq_steps(clamp_len(lens[b], max_ctx), nq, window);
     }
     if (tid == nthreads - 1) pref[batch] = scan[tid];
     __syncthreads();
@@ -172,10 +188,10 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
   if (blockIdx.x == 0) {
     // the merge kernel reads the same prefix; empty sequences get zero rows here
     for (int b = tid; b <= batch; b += nthreads) ws_pref[b] = pref[b];
-    const int row16 = hq * D / 8;  // 16-byte stores per sequence
+    const int row16 = nq * hq * D / 8;  // 16-byte stores per sequence
     for (int b = 0; b < batch; ++b) {
       if (pref[b + 1] != pref[b]) continue;
-      u32x4* orow = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(b) * hq * D);
+      u32x4* orow = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(b) * nq * hq * D);
       for (int i = tid; i < row16; i += nthreads) orow[i] = u32x4{0u, 0u, 0u, 0u};
     }
   }
@@ -187,6 +203,10 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
   const int ph = wid / hgs;           // step phase of this wave
   const int g4 = lane >> 4;           // lane group: MFMA k block / C row block
   const int c = lane & 15;            // MFMA row (A) / column (B, C)
+  // column c = query token qj, head qh of the group (padding columns c >= ncols
+  // take the last token's key range and a zero query)
+  const int qj = c < ncols ? c / group : nq - 1;
+  const int qh = c - (c / group) * group;
 
   const int64_t total = static_cast<int64_t>(pref[batch]) * ngroups;
   if (total == 0) return;
@@ -231,17 +251,24 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
     const int s1 = remaining < nb - s0 ? s0 + static_cast<int>(remaining) : nb;
     const int L = uniform(clamp_len(lens[b], max_ctx));
     const int npages = (L + page - 1) >> page_shift;
+    const int lo_seq = uniform(seq_start(L, nq, window));
+    const int sb = lo_seq / kStep;                  // first step of the sequence
+    // keys [lo_c, hi_c) of this lane's column; steps that cross a bound mask
+    const int hi_c = L - nq + 1 + qj;
+    const int lo_c = window > 0 ? max(0, hi_c - window) : 0;
+    const int hi_min = L - nq + 1;                   // bound of the first query
+    const int lo_max = window > 0 ? max(0, L - window) : 0;  // start of the last
     const int32_t* bt_row = bt + static_cast<int64_t>(b) * maxp;
     const int g = hg * hgs + hi_w;  // this wave's kv head
 
-    // query operand (B of QK^T): head c of the group, d = 32*kk + 8*g4 + e
+    // query operand (B of QK^T): column c, d = 32*kk + 8*g4 + e
     bf16x8 qop[S::kQK];
     {
-      const uint16_t* qrow = q + (static_cast<int64_t>(b) * hq + g * group + c) * D + 8 * g4;
+      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * nq + qj) * hq + g * group + qh) * D + 8 * g4;
 #pragma unroll
       for (int kk = 0; kk < S::kQK; ++kk) {
         u32x4 v = {0u, 0u, 0u, 0u};
-        if (c < group) v = ld16(qrow + 32 * kk);
+        if (c < ncols) v = ld16(qrow + 32 * kk);
         qop[kk] = __builtin_bit_cast(bf16x8, v);
       }
     }
@@ -258,9 +285,9 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
     // loop body is a single basic block whose waits are met in issue order.
     const int sw = s0 + ph;  // this wave's first step; it takes sw, sw + phases, ...
     const int nsteps = sw < s1 ? (s1 - sw + phases - 1) / phases : 0;
-    auto step_of = [&](int k) {  // k-th step of this wave, clamped to its last one
+    auto step_of = [&](int k) {  // k-th step of this wave (absolute), clamped to its last one
       k = k < nsteps ? k : nsteps - 1;
-      return sw + k * phases;
+      return sb + sw + k * phases;
     };
     auto load_pids = [&](int k, int& pa, int& pb) {
       const int t0 = step_of(k) * kStep;
@@ -279,7 +306,8 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       const int t0 = step_of(k) * kStep;
       // valid token rows in each 16-token half (0 for a step past the wave's last)
       const int live = k < nsteps ? L - t0 : 0;
-      const int nA = live < 0 ? 0 : (live < 16 ? live : 16);
+      // a half wholly before the first key is not read (its page may be released)
+      const int nA = (live < 0 || t0 + 16 <= lo_seq) ? 0 : (live < 16 ? live : 16);
       const int nB = live < 16 ? 0 : (live < 32 ? live - 16 : 16);
       if constexpr (!kLanePages) {
         // pages of 16 or more tokens: each 16-token half of the step lies in one page
@@ -305,7 +333,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
           const int pg = page_at(bt_row, tok >> page_shift, npages, num_pages);
           const int64_t off = pg * page_stride + static_cast<int64_t>(tok & (page - 1)) * tok_stride + 8 * vq;
           // page_at keeps the address inside the pool; rows past the end are zeroed
-          const bool ok = tok < t0 + live;
+          const bool ok = tok < t0 + live && tok >= lo_seq;
           const u32x4 zero = {0u, 0u, 0u, 0u};
           const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kg + off));
           const u32x4 vv_ = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vg + off));
@@ -323,7 +351,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
 
     auto compute = [&](int s, const u32x4 (&kr)[S::kLoads], const u32x4 (&vv)[S::kLoads]) {
       const int t0 = s * kStep;
-      const bool tail = t0 + kStep > L;
+      const bool edge = t0 + kStep > hi_min || t0 < lo_max;  // some key of the step is masked
       // K rows -> tile; rows past the end arrived as zeros
 #pragma unroll
       for (int i = 0; i < S::kLoads; ++i)
@@ -356,14 +384,17 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           float v = sacc[T][i] * scale_log2;
-          if (tail && t0 + 16 * T + 4 * g4 + i >= L) v = -__builtin_inff();
+          const int t = t0 + 16 * T + 4 * g4 + i;
+          if (edge && (t >= hi_c || t < lo_c)) v = -__builtin_inff();
           sv[T][i] = v;
           mx = fmaxf(mx, v);
         }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      // a column that has seen no key yet keeps m = -inf: exponents then use 0
+      const float m_ref = m_new == -__builtin_inff() ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
       m_run = m_new;
       // p = hi + lo in two bf16 operands: the P.V product then carries the
       // probabilities to ~2^-17 instead of bf16's 2^-9 (one more MFMA per d
@@ -374,7 +405,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       for (int T = 0; T < 2; ++T)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float pf = __builtin_amdgcn_exp2f(sv[T][i] - m_new);
+          const float pf = __builtin_amdgcn_exp2f(sv[T][i] - m_ref);
           const __bf16 hi = static_cast<__bf16>(pf);
           pop[4 * T + i] = hi;
           pop_lo[4 * T + i] = static_cast<__bf16>(pf - static_cast<float>(hi));
@@ -455,11 +486,11 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
         }
       }
     }
-    if (ph == 0 && c < group) {
+    if (ph == 0 && c < ncols) {
       const bool whole = (s0 == 0) && (s1 == nb);
       if (whole) {
-        const float inv = 1.0f / den;
-        uint16_t* orow = out + (static_cast<int64_t>(b) * hq + g * group + c) * D + 4 * g4;
+        const float inv = den > 0.f ? 1.0f / den : 0.f;  // a query that sees no key: zero row
+        uint16_t* orow = out + ((static_cast<int64_t>(b) * nq + qj) * hq + g * group + qh) * D + 4 * g4;
 #pragma unroll
         for (int dt = 0; dt < S::kDT; ++dt) {
           bf16x4 o;
@@ -470,7 +501,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       } else {
         // slot (workgroup + sequence group) is unique: workgroup ranges are contiguous
         const int64_t slot = static_cast<int64_t>(blk) + static_cast<int64_t>(b) * ngroups + hg;
-        const int64_t row = (slot * hgs + hi_w) * group + c;
+        const int64_t row = (slot * hgs + hi_w) * ncols + c;
         float* arow = ws_acc + row * D + 4 * g4;
 #pragma unroll
         for (int dt = 0; dt < S::kDT; ++dt) *reinterpret_cast<f32x4*>(arow + 16 * dt) = acc[dt];
@@ -503,7 +534,7 @@ template <int D, int kPG>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     uint16_t* __restrict__ out, const float* __restrict__ ws_acc, const float* __restrict__ ws_ml,
     const int32_t* __restrict__ ws_pref, int batch, int hq, int hkv, int group, int hgs, int min_steps,
-    int phases, int grid_blocks) {
+    int phases, int grid_blocks, int nq) {
   constexpr int kCols = D / 4;
   constexpr int kHPB = kMergeThreads / (kPG * kCols);  // query heads per workgroup
   static_assert(kHPB >= 1 && kHPB * kPG * kCols == kMergeThreads, "merge layout");
@@ -511,7 +542,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   __shared__ float s_m[kHPB][kPG], s_l[kHPB][kPG];
 
   const int ngroups = hkv / hgs;
-  const int heads = hgs * group;  // query heads of one kv-head group
+  const int ncols = group * nq;   // (query token, head) columns per kv head
+  const int heads = hgs * ncols;  // query rows of one kv-head group
   const int chunks = (heads + kHPB - 1) / kHPB;
   const int e = blockIdx.x / chunks;
   const int chunk = blockIdx.x - e * chunks;
@@ -538,15 +570,16 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   float mm = -__builtin_inff(), ll = 0.f;
   f32x4 nn = {0.f, 0.f, 0.f, 0.f};
   if (active) {
-    const int hi_w = hh / group, c = hh - (hh / group) * group;
+    const int hi_w = hh / ncols, c = hh - (hh / ncols) * ncols;
 #pragma unroll 4
     for (int64_t w = w0 + pg; w <= w1; w += kPG) {
-      const int64_t row = ((w + base) * hgs + hi_w) * group + c;
+      const int64_t row = ((w + base) * hgs + hi_w) * ncols + c;
       const f32x2 mlv = *reinterpret_cast<const f32x2*>(ws_ml + row * 2);
       const f32x4 av = *reinterpret_cast<const f32x4*>(ws_acc + row * D + 4 * col);
       const float m2 = fmaxf(mm, mlv[0]);
-      const float fo = __builtin_amdgcn_exp2f(mm - m2);
-      const float fn = __builtin_amdgcn_exp2f(mlv[0] - m2);
+      const float mref = m2 == -__builtin_inff() ? 0.f : m2;  // pieces that saw no key
+      const float fo = __builtin_amdgcn_exp2f(mm - mref);
+      const float fn = __builtin_amdgcn_exp2f(mlv[0] - mref);
       nn = nn * fo + av * fn;
       ll = ll * fo + mlv[1] * fn;
       mm = m2;
@@ -576,12 +609,15 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     ll = den;
   }
   if (!active) return;
-  const float inv = 1.0f / ll;
+  const float inv = ll > 0.f ? 1.0f / ll : 0.f;  // a query that sees no key: zero row
   bf16x4 o;
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(nn[i] * inv);
-  const int h = hg * heads + hh;
-  *reinterpret_cast<u32x2*>(out + (static_cast<int64_t>(b) * hq + h) * D + 4 * col) = __builtin_bit_cast(u32x2, o);
+  const int hi_w = hh / ncols, c = hh - hi_w * ncols;
+  const int j = c / group;
+  const int h = (hg * hgs + hi_w) * group + (c - j * group);
+  *reinterpret_cast<u32x2*>(out + ((static_cast<int64_t>(b) * nq + j) * hq + h) * D + 4 * col) =
+      __builtin_bit_cast(u32x2, o);
 }
 
 template <int D, bool kLanePages>
@@ -596,7 +632,7 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   }
   hipLaunchKernelGGL((attn_kernel<D, kLanePages>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
                      a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.batch, a.hq, a.hkv, a.group,
-                     a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e);
+                     a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e, a.nq, a.window);
   return hipGetLastError();
 }
 
@@ -609,11 +645,12 @@ hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
 template <int D, int kPG>
 static hipError_t launch_merge(const LaunchArgs& a, hipStream_t st) {
   constexpr int kHPB = kMergeThreads / (kPG * (D / 4));
-  const int heads = a.hgs * a.group;
+  const int heads = a.hgs * a.group * a.nq;
   const int chunks = (heads + kHPB - 1) / kHPB;
   const dim3 grid(a.batch * (a.hkv / a.hgs) * chunks);
   hipLaunchKernelGGL((merge_kernel<D, kPG>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml,
-                     a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.hgs, a.min_steps, a.waves / a.hgs, a.grid);
+                     a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.hgs, a.min_steps, a.waves / a.hgs, a.grid,
+                     a.nq);
   return hipGetLastError();
 }
 

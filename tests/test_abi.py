@@ -150,3 +150,35 @@ def test_append_then_attend_validates_attention_arguments_first(lib):
     rc = f(16, 0, 16, 16, 16, 16, 16, 16, 2, 32, 8, 128, 16, 64, 8, ctypes.c_float(0.1), None)
     assert rc == NULL
     assert f(0, 0, 0, 0, 0, 0, 0, 0, 0, 32, 8, 128, 16, 64, 8, ctypes.c_float(0.1), None) == OK
+
+
+def ext_call(batch=2, hq=32, hkv=8, tq=1, window=0, ptrs=None):
+    ptrs = ptrs or [16] * 6
+    return B.load().paged_decode_attention_ext(*ptrs, batch, hq, hkv, 128, 16, 64, 8, tq, window,
+                                               ctypes.c_float(0.1), None)
+
+
+@pytest.mark.parametrize("kwargs,code,text", [
+    (dict(tq=0), SHAPE, "num_queries"),
+    (dict(window=-1), SHAPE, "window"),
+    (dict(tq=5), UNSUPPORTED, "exceeds 16"),          # 5 x group 4 = 20 columns
+    (dict(hq=16, hkv=1, tq=2), UNSUPPORTED, "exceeds 16"),
+    (dict(hq=8, hkv=8, tq=17), UNSUPPORTED, "exceeds 16"),
+    (dict(ptrs=[0, 16, 16, 16, 16, 16]), NULL, "NULL"),
+    (dict(hkv=7), SHAPE, "multiple"),
+])
+def test_ext_argument_errors(lib, kwargs, code, text):
+    rc = ext_call(**kwargs)
+    assert rc == code, B.last_error()
+    assert text in B.last_error()
+
+
+def test_ext_accepts_the_full_column_budget(lib):
+    # 4 query tokens x group 4 and 16 x group 1 both fill the 16 columns; batch 0 is a no-op
+    assert ext_call(batch=0, tq=4) == OK and ext_call(batch=0, hq=8, hkv=8, tq=16, window=3) == OK
+
+
+def test_workspace_covers_every_num_queries(lib):
+    _, _, ws = B.plan(4, 32, 8, 128, 16, 512, num_cus=256)
+    g, _, _ = B.plan(4, 32, 8, 128, 16, 512, num_cus=256)
+    assert ws >= (g + 4) * 8 * 16 * (128 + 2) * 4
