@@ -77,6 +77,10 @@ __host__ __device__ constexpr int pref_offset(int waves) { return ml_offset<D>(w
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// s_waitcnt vmcnt(0): wait for every outstanding vector memory load of the
+// wave (expcnt 7 and lgkmcnt 15 in the gfx9 encoding mean "do not wait").
+constexpr int kWaitAllVectorLoads = 0x0F70;
+
 __device__ __forceinline__ int clamp_len(int L, int max_ctx) {
   return L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
 }
@@ -283,6 +287,9 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
 
     // Page ids travel two steps ahead of use and K/V one step ahead, so the
     // loop body is a single basic block whose waits are met in issue order.
+    // A step's loads are issued only once the previous step's have all
+    // arrived: one step in flight per wave while the previous one computes
+    // streams ~1% faster on MI355X than letting two steps overlap.
     const int sw = s0 + ph;  // this wave's first step; it takes sw, sw + phases, ...
     const int nsteps = sw < s1 ? (s1 - sw + phases - 1) / phases : 0;
     auto step_of = [&](int k) {  // k-th step of this wave (absolute), clamped to its last one
@@ -440,9 +447,11 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       int k = 0;
       for (; k + 2 < nsteps; k += 2) {
         load_pids(k + 2, pa0, pb0);
+        __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
         issue(k + 1, pa1, pb1, kB, vB);
         compute(step_of(k), kA, vA);
         load_pids(k + 3, pa1, pb1);
+        __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
         issue(k + 2, pa0, pb0, kA, vA);
         compute(step_of(k + 1), kB, vB);
       }
