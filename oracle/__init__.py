@@ -31,6 +31,11 @@ chunks.  It is pinned against :func:`attend` for arbitrary chunkings.
 the new token's key and value are scattered into their page slot and the
 length already counts that token.
 
+:func:`prelude` is the attention prelude that produces this step's q, k and
+v (Method, "Principle-Driven LLM Kernel Generator", kernel family (i): QKV
+projection plus rotary position embedding, optionally with a per-head
+RMSNorm of q and k).
+
 :func:`attend_masked` is the same definition with a key range per query:
 several query tokens per sequence (the decode steps that the paper's engine
 mixes with chunked prefill, each seeing only keys up to its own position)
@@ -51,7 +56,8 @@ from typing import Iterable, List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = ["bf16_to_f64", "attend", "attend_pairs", "weights", "split_merge",
-           "brute_force_tiny", "kv_append", "attend_masked", "visible_range"]
+           "brute_force_tiny", "kv_append", "attend_masked", "visible_range",
+           "prelude", "rms_norm", "rope"]
 
 
 def bf16_to_f64(bits) -> np.ndarray:
@@ -310,3 +316,71 @@ def attend_masked(q, k_cache, v_cache, block_table, context_lens, scale, window=
                 out[b, j, g * group:(g + 1) * group] = (e / den) @ vt
                 lse[b, j, g * group:(g + 1) * group] = (m + np.log(den))[:, 0]
     return out, lse
+
+
+def rms_norm(t, weight_bits, eps):
+    """RMSNorm over the last axis: t / sqrt(mean(t^2) + eps) * w, in fp64
+    (w: bf16 bits; eps: the fp32 value the kernel receives)."""
+    t = np.asarray(t, dtype=np.float64)
+    ms = np.mean(t * t, axis=-1, keepdims=True)
+    return t / np.sqrt(ms + float(np.float32(eps))) * bf16_to_f64(weight_bits)
+
+
+def rope(t, positions, theta, rotary_dim, interleaved=False):
+    """Rotary position embedding of the last axis, in fp64.
+
+    t: [B, H, D]; positions: [B].  Pair i < rotary_dim / 2 turns by the angle
+    p * theta^(-2i / rotary_dim): the pair is (i, i + rotary_dim / 2) in the
+    rotate-half convention, or (2i, 2i + 1) when ``interleaved``; dimensions
+    at or beyond ``rotary_dim`` pass through.  (x_a, x_b) becomes
+    (x_a cos - x_b sin, x_b cos + x_a sin).  ``theta`` is the fp32 value the
+    kernel receives.
+    """
+    t = np.array(t, dtype=np.float64, copy=True)
+    half = rotary_dim // 2
+    base = float(np.float32(theta))
+    for i in range(half):
+        a, b = (2 * i, 2 * i + 1) if interleaved else (i, i + half)
+        ang = np.asarray(positions, dtype=np.float64) * base ** (-2.0 * i / rotary_dim)
+        c = np.cos(ang)[:, None]
+        s_ = np.sin(ang)[:, None]
+        xa, xb = t[..., a].copy(), t[..., b].copy()
+        t[..., a] = xa * c - xb * s_
+        t[..., b] = xb * c + xa * s_
+    return t
+
+
+def prelude(x, w_qkv, num_q_heads, num_kv_heads, head_dim, context_lens, theta, *, bias=None,
+            q_norm=None, k_norm=None, eps=1e-6, rotary_dim=None, interleaved=False):
+    """Attention prelude of one decode step, in fp64 (kernel family (i) of
+    Method, "Principle-Driven LLM Kernel Generator").
+
+    x: bf16 bits [B, H] (the normalised hidden state of the new token);
+    w_qkv: bf16 bits [N, H] with N = (Hq + 2 Hkv) D, rows ordered q heads,
+    then k heads, then v heads; bias: bf16 bits [N] or None; q_norm, k_norm:
+    bf16 bits [D] or None (per-head RMSNorm weights, applied before the
+    rotation).  The new token of sequence b sits at position
+    max(context_lens[b] - 1, 0) (the length counts it).
+    y = W x (+ bias); q, k, v are its head blocks; q and k are normalised
+    (when weights are given) and rotated; v is left as is.
+    Returns (q [B, Hq, D], k [B, Hkv, D], v [B, Hkv, D]) as float64.
+    """
+    hq, hkv, d = int(num_q_heads), int(num_kv_heads), int(head_dim)
+    xf = bf16_to_f64(x)
+    wf = bf16_to_f64(w_qkv)
+    y = xf @ wf.T
+    if bias is not None:
+        y = y + bf16_to_f64(bias)[None, :]
+    bsz = y.shape[0]
+    q = y[:, :hq * d].reshape(bsz, hq, d)
+    k = y[:, hq * d:(hq + hkv) * d].reshape(bsz, hkv, d)
+    v = y[:, (hq + hkv) * d:].reshape(bsz, hkv, d)
+    if q_norm is not None:
+        q = rms_norm(q, q_norm, eps)
+    if k_norm is not None:
+        k = rms_norm(k, k_norm, eps)
+    pos = np.maximum(np.asarray(context_lens, dtype=np.int64) - 1, 0)
+    rd = d if rotary_dim is None else int(rotary_dim)
+    q = rope(q, pos, theta, rd, interleaved)
+    k = rope(k, pos, theta, rd, interleaved)
+    return q, k, v.copy()

@@ -179,3 +179,79 @@ def test_each_masked_mutant_is_caught(name, monkeypatch):
         except (AssertionError, ValueError, IndexError):
             failed.append(getattr(f, "__name__", str(f)))
     assert failed, f"mutant '{name}' passed every pin"
+
+
+# ------------------------------------------------------------------ prelude
+import test_oracle_prelude as ppins  # noqa: E402
+
+_rope, _rms, _prelude = oracle.rope, oracle.rms_norm, oracle.prelude
+
+
+def rope_mutant(sign=1.0, swap_pairs=False, exponent=2.0):
+    def rope(t, positions, theta, rotary_dim, interleaved=False):
+        t = np.array(t, dtype=np.float64, copy=True)
+        half = rotary_dim // 2
+        inter = (not interleaved) if swap_pairs else interleaved
+        for i in range(half):
+            a, b = (2 * i, 2 * i + 1) if inter else (i, i + half)
+            ang = np.asarray(positions, dtype=np.float64) * float(np.float32(theta)) ** (-exponent * i / rotary_dim)
+            c, s_ = np.cos(ang)[:, None], sign * np.sin(ang)[:, None]
+            xa, xb = t[..., a].copy(), t[..., b].copy()
+            t[..., a] = xa * c - xb * s_
+            t[..., b] = xb * c + xa * s_
+        return t
+    return rope
+
+
+def rms_mutant(t, weight_bits, eps):
+    t = np.asarray(t, dtype=np.float64)
+    return t / np.sqrt(np.sum(t * t, axis=-1, keepdims=True) + float(np.float32(eps))) * oracle.bf16_to_f64(weight_bits)
+
+
+def prelude_kv_swapped(*a, **kw):
+    q, k, v = _prelude(*a, **kw)
+    return q, v, k
+
+
+def prelude_norm_after_rope(x, w, hq, hkv, d, lens, theta, **kw):
+    qn, kn, eps = kw.pop("q_norm", None), kw.pop("k_norm", None), kw.get("eps", 1e-6)
+    q, k, v = _prelude(x, w, hq, hkv, d, lens, theta, **kw)
+    if qn is not None:
+        q, k = _rms(q, qn, eps), _rms(k, kn, eps)
+    return q, k, v
+
+
+PRELUDE_PINS = [
+    ppins.test_integer_projection_is_exact_and_blocks_are_ordered_q_k_v,
+    ppins.test_bias_adds_to_every_row,
+    *[functools.partial(ppins.test_rope_is_complex_multiplication, i, rd) for i in (False, True) for rd in (16, 8)],
+    ppins.test_rope_scores_depend_only_on_relative_position,
+    ppins.test_rope_at_position_zero_is_identity_and_keeps_pair_norms,
+    ppins.test_rms_norm_matches_torch,
+    *[functools.partial(ppins.test_prelude_matches_independent_torch_formulation, kw)
+      for kw in (dict(), dict(qk_norm=True), dict(bias=True, rotary_dim=8, interleaved=True),
+                 dict(qk_norm=True, rotary_dim=8))],
+    ppins.test_position_is_length_minus_one_and_empty_slots_use_zero,
+]
+PRELUDE_MUTANTS = {
+    "rotation the other way": ("rope", rope_mutant(sign=-1.0)),
+    "pairs of the other convention": ("rope", rope_mutant(swap_pairs=True)),
+    "frequency exponent halved": ("rope", rope_mutant(exponent=1.0)),
+    "norm by the sum of squares": ("rms_norm", rms_mutant),
+    "k and v blocks swapped": ("prelude", prelude_kv_swapped),
+    "norm applied after the rotation": ("prelude", prelude_norm_after_rope),
+}
+
+
+@pytest.mark.parametrize("name", list(PRELUDE_MUTANTS))
+def test_each_prelude_mutant_is_caught(name, monkeypatch):
+    attr, fn = PRELUDE_MUTANTS[name]
+    monkeypatch.setattr(oracle, attr, fn)
+    failed = []
+    for f in PRELUDE_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                f()
+        except (AssertionError, ValueError, IndexError):
+            failed.append(getattr(f, "__name__", str(f)))
+    assert failed, f"mutant '{name}' passed every pin"

@@ -346,3 +346,127 @@ def permute_pages(w: Workload, seed: int) -> Workload:
     live = bt >= 0
     bt[live] = new_of_old[bt[live]].astype(np.int32)
     return dataclasses.replace(w, k_cache=k, v_cache=v, block_table=bt)
+
+
+
+# ------------------------------------------------------------------ prelude
+@dataclasses.dataclass(frozen=True)
+class PreludeConfig:
+    """One synthetic attention-prelude workload (QKV projection + RoPE)."""
+
+    name: str
+    batch: int
+    hidden: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    seed: int
+    lengths: str                 # as for Config: the new token sits at L - 1
+    theta: float
+    qk_norm: bool = False
+    bias: bool = False
+    rotary_dim: int = 0          # 0 = head_dim
+    interleaved: bool = False
+    description: str = ""
+
+
+PRELUDE_CONFIGS: Dict[str, PreludeConfig] = {
+    "prelude_qwen3_4b": PreludeConfig(
+        "prelude_qwen3_4b", 1, 2560, 32, 8, 128, 10, "fixed:4096", 1.0e6, qk_norm=True,
+        description="Qwen3-4B-shaped prelude, batch 1, hidden 2560, 32:8 heads, D=128, "
+                    "per-head Q/K RMSNorm, theta 1e6"),
+    "prelude_llama8b": PreludeConfig(
+        "prelude_llama8b", 64, 4096, 32, 8, 128, 11, "uniform:128:8192", 5.0e5,
+        description="Llama-3-8B-shaped prelude, batch 64, hidden 4096, 32:8 heads, D=128, "
+                    "theta 5e5"),
+    "prelude_70b": PreludeConfig(
+        "prelude_70b", 4, 8192, 64, 8, 128, 12, "fixed:131072", 5.0e5,
+        description="70B-shaped prelude, batch 4, hidden 8192, 64:8 heads, D=128, theta 5e5, "
+                    "positions 131071"),
+    "prelude_glm4": PreludeConfig(
+        "prelude_glm4", 8, 4096, 32, 2, 128, 13, "uniform:16:32768", 1.0e4, bias=True,
+        rotary_dim=64, interleaved=True,
+        description="GLM-4-9B-shaped prelude, batch 8, hidden 4096, 32:2 heads, D=128, QKV "
+                    "bias, rotary on the first 64 dims in interleaved pairs, theta 1e4"),
+    "prelude_falcon3": PreludeConfig(
+        "prelude_falcon3", 16, 3072, 12, 4, 256, 14, "uniform:16:32768", 1000042.0,
+        description="Falcon3-7B-shaped prelude, batch 16, hidden 3072, 12:4 heads, D=256, "
+                    "theta 1000042"),
+}
+
+
+@dataclasses.dataclass
+class PreludeWorkload:
+    """Inputs of one attention-prelude call (host numpy arrays, bf16 bits)."""
+
+    x: np.ndarray                 # [B, H]
+    w_qkv: np.ndarray             # [(Hq + 2 Hkv) D, H], rows: q heads, k heads, v heads
+    bias: Optional[np.ndarray]    # [N] or None
+    q_norm: Optional[np.ndarray]  # [D] or None
+    k_norm: Optional[np.ndarray]  # [D] or None
+    context_lens: np.ndarray      # int32 [B]; the new token sits at L - 1
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    theta: np.float32
+    eps: np.float32
+    rotary_dim: int
+    interleaved: bool
+    name: str = "custom"
+
+    @property
+    def batch(self) -> int:
+        return self.x.shape[0]
+
+    @property
+    def hidden(self) -> int:
+        return self.x.shape[1]
+
+    @property
+    def rows(self) -> int:
+        return self.w_qkv.shape[0]
+
+    def algorithmic_bytes(self) -> int:
+        """Weights once, x in, q/k/v out, bias and norm weights, lengths."""
+        n, h, b = self.rows, self.hidden, self.batch
+        extra = (2 * n if self.bias is not None else 0) + 2 * self.head_dim * (
+            (self.q_norm is not None) + (self.k_norm is not None))
+        return int(2 * n * h + 2 * b * h + 2 * b * n + extra + 4 * b)
+
+
+def build_prelude(batch, hidden, num_q_heads, num_kv_heads, head_dim, seed, *, lengths=None,
+                  theta=1.0e4, qk_norm=False, bias=False, rotary_dim=0, interleaved=False,
+                  eps=1e-6, name="custom", rng=None) -> PreludeWorkload:
+    """Seeded prelude inputs.  Draw order: lengths (by the caller), x, W,
+    bias, q_norm, k_norm.  x ~ N(0, 1) (a normalised hidden state); W ~
+    N(0, 1/hidden) so that q, k, v are O(1); bias ~ N(0, 0.1^2); norm
+    weights ~ 1 + N(0, 0.1^2)."""
+    if rng is None:
+        rng = np.random.Generator(np.random.PCG64(seed))
+    n = (num_q_heads + 2 * num_kv_heads) * head_dim
+    if lengths is None:
+        lengths = np.full(batch, 1, dtype=np.int64)
+    x = _normal_bf16(rng, (batch, hidden), 1.0)
+    w = _normal_bf16(rng, (n, hidden), 1.0 / math.sqrt(hidden))
+    bvec = _normal_bf16(rng, (n,), 0.1) if bias else None
+    qn = kn = None
+    if qk_norm:
+        one = bf16_bits_to_f32(_normal_bf16(rng, (2, head_dim), 0.1)) + np.float32(1.0)
+        qn, kn = f32_to_bf16_bits(one[0]), f32_to_bf16_bits(one[1])
+    return PreludeWorkload(x=x, w_qkv=w, bias=bvec, q_norm=qn, k_norm=kn,
+                           context_lens=np.asarray(lengths, dtype=np.int32), num_q_heads=num_q_heads,
+                           num_kv_heads=num_kv_heads, head_dim=head_dim, theta=np.float32(theta),
+                           eps=np.float32(eps), rotary_dim=int(rotary_dim or head_dim),
+                           interleaved=bool(interleaved), name=name)
+
+
+def make_prelude(name: str, seed: Optional[int] = None) -> PreludeWorkload:
+    """Build one of the named prelude workloads with its fixed seed."""
+    cfg = PRELUDE_CONFIGS[name]
+    rng = np.random.Generator(np.random.PCG64(cfg.seed if seed is None else seed))
+    shim = Config(cfg.name, cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, 16, cfg.seed,
+                  cfg.lengths, "exact")
+    lens = _draw_lengths(shim, rng)
+    return build_prelude(cfg.batch, cfg.hidden, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.seed,
+                         lengths=lens, theta=cfg.theta, qk_norm=cfg.qk_norm, bias=cfg.bias,
+                         rotary_dim=cfg.rotary_dim, interleaved=cfg.interleaved, name=name, rng=rng)
