@@ -206,9 +206,9 @@ int32_t pda_version(void);
 
 /*
  * Planner options (tuning and testing).  The split planner spreads the
- * batch's context over min(num_cus * blocks_per_cu * 4 waves,
- * ceil(total 32-token steps / min_steps)) waves.
- *   PDA_OPT_BLOCKS_PER_CU  workgroups of 4 waves per compute unit, 1..8
+ * batch's context over min(num_cus * blocks_per_cu, ceil(total 32-token
+ * steps / (min_steps * step phases))) workgroups of up to 8 waves.
+ *   PDA_OPT_BLOCKS_PER_CU  workgroups per compute unit, 1..8
  *                          (default 1, env PDA_BLOCKS_PER_CU).
  *   PDA_OPT_MIN_STEPS      fewest 32-token steps a wave is given, >= 1
  *                          (default 2, env PDA_MIN_STEPS); a large value
@@ -231,6 +231,82 @@ int32_t pda_get_option(int32_t option);
  */
 int pda_profile_enable(int32_t on);
 int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls);
+
+/*
+ * ---------------------------------------------------------------------------
+ * Attention prelude: the paper's kernel family (i) (Method, "Principle-Driven
+ * LLM Kernel Generator"): the QKV projection of the new token's hidden
+ * state plus rotary position embedding, optionally with a per-head RMSNorm
+ * of q and k, producing this decode step's q, k and v.
+ *
+ *   y = W x (+ bias), W [N, H] with N = (Hq + 2 Hkv) * D, rows ordered q
+ *   heads, k heads, v heads; each q and k head t (D values) becomes
+ *   t / sqrt(mean(t^2) + eps) * w when norm weights are given, and then
+ *   pair i < rotary_dim / 2 turns by the angle p * theta^(-2 i / rotary_dim),
+ *   p = max(context_lens[b] - 1, 0) (the position of the new token; the
+ *   length counts it): (a, b) -> (a cos - b sin, b cos + a sin), with pairs
+ *   (i, i + rotary_dim / 2), or (2i, 2i + 1) when interleaved; dimensions at
+ *   or beyond rotary_dim pass through.  v is only projected.  Intermediates
+ *   stay fp32 (angles fp64); outputs are rounded once to bf16.
+ * ---------------------------------------------------------------------------
+ */
+typedef struct {
+  int32_t batch;         /* sequences, 0 .. 64                                  */
+  int32_t hidden;        /* H: a positive multiple of 256, at most 65536        */
+  int32_t num_q_heads;   /* Hq, a multiple of num_kv_heads                      */
+  int32_t num_kv_heads;  /* Hkv                                                 */
+  int32_t head_dim;      /* D: 64, 128 or 256                                   */
+  int32_t rotary_dim;    /* 0 (no rotation) or even, 2 .. head_dim              */
+  int32_t interleaved;   /* 0: pairs (i, i + rotary_dim/2); 1: pairs (2i, 2i+1) */
+  float rope_theta;      /* base of the rotary frequencies, finite and > 0      */
+  float eps;             /* RMSNorm epsilon, finite and >= 0                    */
+} pda_prelude_dims;
+
+/*
+ * pda_pack_weights -- copy a bf16 [rows, cols] row-major weight matrix into
+ * the packed order the prelude reads (16-row x 32-column tiles of 1 KB in
+ * matrix-core operand order).  rows a multiple of 16, cols a multiple of 32;
+ * w and w_packed (rows * cols bf16, caller-owned, not overlapping) 16-byte
+ * aligned.  Asynchronous on `stream`; done once per weight at load time.
+ */
+int pda_pack_weights(const void* w, void* w_packed, int32_t rows, int32_t cols, void* stream);
+
+/*
+ * pda_attention_prelude -- the prelude described above.
+ *   x             bf16 [batch, hidden], 16-byte aligned.
+ *   w_packed      packed bf16 [N, hidden] (pda_pack_weights), 16-byte aligned.
+ *   bias          bf16 [N] or NULL.
+ *   q_norm, k_norm  bf16 [head_dim] each, or both NULL (no norm).
+ *   context_lens  int32 [batch] on the device (positions, see above).
+ *   q_out         bf16 [batch, Hq, D]; k_out, v_out bf16 [batch, Hkv, D];
+ *                 16-byte aligned.
+ * Uses the (device, stream) workspace of paged_decode_attention for the fp32
+ * projection (grown on demand; pda_prelude_workspace_reserve before graph
+ * capture).  Asynchronous.  Errors: PDA_ERR_NULL, PDA_ERR_SHAPE,
+ * PDA_ERR_UNSUPPORTED (dims outside the ranges above), PDA_ERR_ALIGN,
+ * PDA_ERR_SCALE (theta or eps not finite / out of range), PDA_ERR_HIP.
+ */
+int pda_attention_prelude(const void* x, const void* w_packed, const void* bias, const void* q_norm,
+                          const void* k_norm, const int32_t* context_lens, void* q_out, void* k_out,
+                          void* v_out, const pda_prelude_dims* dims, void* stream);
+
+/*
+ * pda_attention_prelude_append -- the prelude with the KV append fused in:
+ * k and v of sequence b are written (bf16) straight into the paged caches at
+ * position context_lens[b] - 1, as pda_kv_append would, and q to q_out.
+ * k_cache, v_cache, block_table, page_size, num_pages and max_pages_per_seq
+ * as for paged_decode_attention (caches written in place, only those slots);
+ * sequences with length 0 append nothing.  Other arguments and errors as
+ * for pda_attention_prelude.
+ */
+int pda_attention_prelude_append(const void* x, const void* w_packed, const void* bias,
+                                 const void* q_norm, const void* k_norm, const int32_t* context_lens,
+                                 void* q_out, void* k_cache, void* v_cache, const int32_t* block_table,
+                                 int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
+                                 const pda_prelude_dims* dims, void* stream);
+
+/* Grow the (current device, stream) workspace for a prelude of these dims. */
+int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream);
 
 #ifdef __cplusplus
 }

@@ -30,12 +30,28 @@ class PdaError(RuntimeError):
         self.code = code
 
 
+class PreludeDims(ctypes.Structure):
+    """pda_prelude_dims of include/pda.h."""
+    _fields_ = [("batch", ctypes.c_int32), ("hidden", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("rotary_dim", ctypes.c_int32),
+                ("interleaved", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("eps", ctypes.c_float)]
+
+
 def _declare(lib: ctypes.CDLL) -> None:
     i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
     lib.paged_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp]
     lib.paged_decode_attention.restype = ctypes.c_int
     lib.paged_decode_attention_ext.argtypes = [vp] * 6 + [i32] * 9 + [f32, vp]
     lib.paged_decode_attention_ext.restype = ctypes.c_int
+    dims_p = ctypes.POINTER(PreludeDims)
+    lib.pda_pack_weights.argtypes = [vp, vp, i32, i32, vp]
+    lib.pda_pack_weights.restype = ctypes.c_int
+    lib.pda_attention_prelude.argtypes = [vp] * 9 + [dims_p, vp]
+    lib.pda_attention_prelude.restype = ctypes.c_int
+    lib.pda_attention_prelude_append.argtypes = [vp] * 10 + [i32, i32, i32, dims_p, vp]
+    lib.pda_attention_prelude_append.restype = ctypes.c_int
+    lib.pda_prelude_workspace_reserve.argtypes = [dims_p, vp]
+    lib.pda_prelude_workspace_reserve.restype = ctypes.c_int
     lib.pda_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
     lib.pda_kv_append.restype = ctypes.c_int
     lib.paged_decode_attention_append.argtypes = [vp] * 8 + [i32] * 7 + [f32, vp]
@@ -210,6 +226,70 @@ def paged_decode_attention_append(q, k_new, v_new, k_cache, v_cache, block_table
         block_table.data_ptr(), context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n,
         block_table.shape[1], ctypes.c_float(float(scale)), _stream_ptr(stream)))
     return out
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _check_bf16(**tensors):
+    import torch
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous bf16 GPU tensor")
+
+
+def pack_weights(w, stream=None):
+    """Pack a bf16 [rows, cols] weight into the prelude's tile order; returns
+    a new tensor of the same shape holding the packed data."""
+    import torch
+    _check_bf16(w=w)
+    if w.dim() != 2:
+        raise ValueError("w must be 2-D")
+    out = torch.empty_like(w)
+    _check(load().pda_pack_weights(w.data_ptr(), out.data_ptr(), w.shape[0], w.shape[1], _stream_ptr(stream)))
+    return out
+
+
+def prelude_dims(batch, hidden, hq, hkv, d, rotary_dim, interleaved, theta, eps) -> PreludeDims:
+    return PreludeDims(int(batch), int(hidden), int(hq), int(hkv), int(d), int(rotary_dim), int(bool(interleaved)),
+                       float(theta), float(eps))
+
+
+def attention_prelude(x, w_packed, context_lens, q_out, k_out, v_out, *, num_q_heads, num_kv_heads, head_dim,
+                      rope_theta, rotary_dim=None, interleaved=False, bias=None, q_norm=None, k_norm=None,
+                      eps=1e-6, stream=None):
+    """QKV projection + optional per-head Q/K RMSNorm + RoPE of this step's
+    token (x: bf16 [B, H]; w_packed from :func:`pack_weights`)."""
+    _check_bf16(x=x, w_packed=w_packed, q_out=q_out, k_out=k_out, v_out=v_out, bias=bias, q_norm=q_norm,
+                k_norm=k_norm)
+    dims = prelude_dims(x.shape[0], x.shape[1], num_q_heads, num_kv_heads, head_dim,
+                        head_dim if rotary_dim is None else rotary_dim, interleaved, rope_theta, eps)
+    _check(load().pda_attention_prelude(x.data_ptr(), w_packed.data_ptr(), _ptr(bias), _ptr(q_norm), _ptr(k_norm),
+                                        context_lens.data_ptr(), q_out.data_ptr(), k_out.data_ptr(),
+                                        v_out.data_ptr(), ctypes.byref(dims), _stream_ptr(stream)))
+
+
+def attention_prelude_append(x, w_packed, context_lens, q_out, k_cache, v_cache, block_table, *, num_q_heads,
+                             num_kv_heads, head_dim, rope_theta, rotary_dim=None, interleaved=False, bias=None,
+                             q_norm=None, k_norm=None, eps=1e-6, stream=None):
+    """The prelude with the KV append fused in: k, v go straight to their
+    page slot at position context_lens[b] - 1."""
+    _check_bf16(x=x, w_packed=w_packed, q_out=q_out, k_cache=k_cache, v_cache=v_cache, bias=bias, q_norm=q_norm,
+                k_norm=k_norm)
+    dims = prelude_dims(x.shape[0], x.shape[1], num_q_heads, num_kv_heads, head_dim,
+                        head_dim if rotary_dim is None else rotary_dim, interleaved, rope_theta, eps)
+    n, p = k_cache.shape[0], k_cache.shape[1]
+    _check(load().pda_attention_prelude_append(
+        x.data_ptr(), w_packed.data_ptr(), _ptr(bias), _ptr(q_norm), _ptr(k_norm), context_lens.data_ptr(),
+        q_out.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), p, n,
+        block_table.shape[1], ctypes.byref(dims), _stream_ptr(stream)))
+
+
+def prelude_workspace_reserve(dims: PreludeDims, stream=None) -> None:
+    _check(load().pda_prelude_workspace_reserve(ctypes.byref(dims), _stream_ptr(stream)))
 
 
 def plan(batch, hq, hkv, d, page_size, max_pages, num_cus=256) -> Tuple[int, int, int]:

@@ -17,6 +17,7 @@
 
 #include "pda.h"
 #include "pda_append.h"
+#include "pda_gemv.h"
 #include "pda_internal.h"
 
 namespace {
@@ -219,6 +220,87 @@ hipEvent_t prof_event() {
   hipEvent_t e = nullptr;
   if (hipEventCreate(&e) != hipSuccess) return nullptr;
   return e;
+}
+
+// ---------------------------------------------------------------- prelude
+bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
+
+int check_prelude(const pda_prelude_dims* dm) {
+  if (!dm) return fail(PDA_ERR_NULL, "dims is NULL");
+  const pda_prelude_dims& d = *dm;
+  if (d.batch < 0) return fail(PDA_ERR_SHAPE, "batch must be >= 0 (got %d)", d.batch);
+  if (d.batch > pda::kMaxGemvBatch)
+    return fail(PDA_ERR_UNSUPPORTED, "prelude batch %d exceeds %d", d.batch, pda::kMaxGemvBatch);
+  if (d.hidden <= 0 || d.num_q_heads <= 0 || d.num_kv_heads <= 0)
+    return fail(PDA_ERR_SHAPE, "hidden and head counts must be positive");
+  if (d.hidden % (pda::kGemvWaves * pda::kTileK) || d.hidden > 65536)
+    return fail(PDA_ERR_UNSUPPORTED, "hidden %d (supported: multiples of 256 up to 65536)", d.hidden);
+  if (d.num_q_heads % d.num_kv_heads)
+    return fail(PDA_ERR_SHAPE, "num_q_heads %d is not a multiple of num_kv_heads %d", d.num_q_heads,
+                d.num_kv_heads);
+  if (d.head_dim != 64 && d.head_dim != 128 && d.head_dim != 256)
+    return fail(PDA_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128, 256)", d.head_dim);
+  if (d.num_kv_heads > PDA_MAX_KV_HEADS || d.num_q_heads > 8 * PDA_MAX_KV_HEADS)
+    return fail(PDA_ERR_UNSUPPORTED, "too many heads (q %d, kv %d)", d.num_q_heads, d.num_kv_heads);
+  if (d.rotary_dim < 0 || d.rotary_dim > d.head_dim || (d.rotary_dim & 1))
+    return fail(PDA_ERR_SHAPE, "rotary_dim %d (0, or even up to head_dim %d)", d.rotary_dim, d.head_dim);
+  if (d.interleaved != 0 && d.interleaved != 1) return fail(PDA_ERR_SHAPE, "interleaved must be 0 or 1");
+  if (!std::isfinite(d.rope_theta) || !(d.rope_theta > 0.f))
+    return fail(PDA_ERR_SCALE, "rope_theta must be finite and > 0");
+  if (!std::isfinite(d.eps) || d.eps < 0.f) return fail(PDA_ERR_SCALE, "eps must be finite and >= 0");
+  return PDA_OK;
+}
+
+int64_t prelude_rows(const pda_prelude_dims& d) {
+  return static_cast<int64_t>(d.num_q_heads + 2 * d.num_kv_heads) * d.head_dim;
+}
+
+int64_t prelude_ws_bytes(const pda_prelude_dims& d) {
+  return align256(static_cast<int64_t>(d.batch) * prelude_rows(d) * 4);
+}
+
+// Shared by both prelude entry points once their own arguments are checked.
+int run_prelude(const void* x, const void* w_packed, const void* bias, const void* q_norm, const void* k_norm,
+                const int32_t* context_lens, void* q_out, pda::PreludeArgs ep, const pda_prelude_dims& d,
+                void* stream) {
+  if (!x || !w_packed || !context_lens || !q_out) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if ((q_norm == nullptr) != (k_norm == nullptr))
+    return fail(PDA_ERR_NULL, "q_norm and k_norm must both be given or both be NULL");
+  if (misaligned(x, 16) || misaligned(w_packed, 16) || misaligned(q_out, 16))
+    return fail(PDA_ERR_ALIGN, "x, w_packed and the outputs must be 16-byte aligned");
+  if (misaligned(bias, 2) || misaligned(q_norm, 2) || misaligned(k_norm, 2) || misaligned(context_lens, 4))
+    return fail(PDA_ERR_ALIGN, "bias / norm weights must be 2-byte and context_lens 4-byte aligned");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  int rc = workspace_for(dev, st, prelude_ws_bytes(d), &ws);
+  if (rc) return rc;
+  pda::GemvArgs g;
+  g.x = static_cast<const uint16_t*>(x);
+  g.wp = static_cast<const uint16_t*>(w_packed);
+  g.y = static_cast<float*>(ws);
+  g.batch = d.batch;
+  g.n = static_cast<int>(prelude_rows(d));
+  g.k = d.hidden;
+  if ((e = pda::launch_gemv(g, st)) != hipSuccess) return hip_fail(e, "GEMV kernel launch");
+  ep.y = g.y;
+  ep.bias = static_cast<const uint16_t*>(bias);
+  ep.q_norm = static_cast<const uint16_t*>(q_norm);
+  ep.k_norm = static_cast<const uint16_t*>(k_norm);
+  ep.lens = context_lens;
+  ep.q_out = static_cast<uint16_t*>(q_out);
+  ep.batch = d.batch;
+  ep.hq = d.num_q_heads;
+  ep.hkv = d.num_kv_heads;
+  ep.d = d.head_dim;
+  ep.rotary_dim = d.rotary_dim;
+  ep.interleaved = d.interleaved;
+  ep.theta = d.rope_theta;
+  ep.eps = d.eps;
+  if ((e = pda::launch_prelude_epilogue(ep, st)) != hipSuccess) return hip_fail(e, "prelude epilogue launch");
+  return PDA_OK;
 }
 
 }  // namespace
@@ -483,6 +565,80 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
     g_prof_recs.push_back(rec);
   }
   return PDA_OK;
+}
+
+int pda_pack_weights(const void* w, void* w_packed, int32_t rows, int32_t cols, void* stream) {
+  g_err.clear();
+  if (rows <= 0 || cols <= 0) return fail(PDA_ERR_SHAPE, "rows and cols must be positive");
+  if (rows % pda::kTileRows || cols % pda::kTileK)
+    return fail(PDA_ERR_SHAPE, "rows must be a multiple of 16 and cols of 32 (got %d x %d)", rows, cols);
+  if (static_cast<int64_t>(rows) * cols > (int64_t{1} << 34)) return fail(PDA_ERR_SHAPE, "matrix too large");
+  if (!w || !w_packed) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if (misaligned(w, 16) || misaligned(w_packed, 16)) return fail(PDA_ERR_ALIGN, "w and w_packed must be 16-byte aligned");
+  const uintptr_t a = reinterpret_cast<uintptr_t>(w), b = reinterpret_cast<uintptr_t>(w_packed);
+  const uintptr_t bytes = static_cast<uintptr_t>(rows) * cols * 2;
+  if (a < b + bytes && b < a + bytes) return fail(PDA_ERR_SHAPE, "w and w_packed overlap");
+  hipError_t e = pda::launch_pack(static_cast<const uint16_t*>(w), static_cast<uint16_t*>(w_packed), rows, cols,
+                                  static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
+  return PDA_OK;
+}
+
+int pda_attention_prelude(const void* x, const void* w_packed, const void* bias, const void* q_norm,
+                          const void* k_norm, const int32_t* context_lens, void* q_out, void* k_out,
+                          void* v_out, const pda_prelude_dims* dims, void* stream) {
+  g_err.clear();
+  int rc = check_prelude(dims);
+  if (rc) return rc;
+  if (dims->batch == 0) return PDA_OK;
+  if (!k_out || !v_out) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if (misaligned(k_out, 16) || misaligned(v_out, 16))
+    return fail(PDA_ERR_ALIGN, "x, w_packed and the outputs must be 16-byte aligned");
+  pda::PreludeArgs ep{};
+  ep.k_out = static_cast<uint16_t*>(k_out);
+  ep.v_out = static_cast<uint16_t*>(v_out);
+  return run_prelude(x, w_packed, bias, q_norm, k_norm, context_lens, q_out, ep, *dims, stream);
+}
+
+int pda_attention_prelude_append(const void* x, const void* w_packed, const void* bias, const void* q_norm,
+                                 const void* k_norm, const int32_t* context_lens, void* q_out, void* k_cache,
+                                 void* v_cache, const int32_t* block_table, int32_t page_size, int32_t num_pages,
+                                 int32_t max_pages_per_seq, const pda_prelude_dims* dims, void* stream) {
+  g_err.clear();
+  int rc = check_prelude(dims);
+  if (rc) return rc;
+  if (page_size <= 0 || max_pages_per_seq <= 0)
+    return fail(PDA_ERR_SHAPE, "page_size and max_pages_per_seq must be positive");
+  if (!is_pow2(page_size) || page_size > PDA_MAX_PAGE_SIZE)
+    return fail(PDA_ERR_UNSUPPORTED, "page_size %d (supported: powers of two up to %d)", page_size,
+                PDA_MAX_PAGE_SIZE);
+  if (static_cast<int64_t>(max_pages_per_seq) * page_size > (int64_t{1} << 30))
+    return fail(PDA_ERR_SHAPE, "max_pages_per_seq * page_size too large");
+  if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
+  if (dims->batch == 0) return PDA_OK;
+  if (!k_cache || !v_cache || !block_table) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if (misaligned(k_cache, 16) || misaligned(v_cache, 16) || misaligned(block_table, 4))
+    return fail(PDA_ERR_ALIGN, "caches must be 16-byte and block_table 4-byte aligned");
+  pda::PreludeArgs ep{};
+  ep.k_cache = static_cast<uint16_t*>(k_cache);
+  ep.v_cache = static_cast<uint16_t*>(v_cache);
+  ep.bt = block_table;
+  ep.page_shift = log2i(page_size);
+  ep.num_pages = num_pages;
+  ep.maxp = max_pages_per_seq;
+  return run_prelude(x, w_packed, bias, q_norm, k_norm, context_lens, q_out, ep, *dims, stream);
+}
+
+int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream) {
+  g_err.clear();
+  int rc = check_prelude(dims);
+  if (rc) return rc;
+  if (dims->batch == 0) return PDA_OK;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  void* ptr = nullptr;
+  return workspace_for(dev, static_cast<hipStream_t>(stream), prelude_ws_bytes(*dims), &ptr);
 }
 
 }  // extern "C"

@@ -1,0 +1,273 @@
+// Decode GEMV and the attention prelude for MI355X (gfx950, CDNA4, wave64).
+//
+// What is computed: the paper's kernel family (i), the attention prelude
+// (Method, "Principle-Driven LLM Kernel Generator"): the QKV projection of
+// the new token's hidden state, then per-head RMSNorm of q and k (when the
+// model has it) and the rotary position embedding of q and k.  Its template
+// GEMV (Method, "CUDA Code Generator") reads [N, K] weight rows with 128-bit
+// loads and reduces across lanes; on CDNA4 the same bandwidth-bound
+// product is laid out differently:
+//
+//  * Weights are packed once into the matrix cores' operand order: a tile of
+//    16 rows x 32 k is 1 KB, and lane l of a wave holds row l % 16, k
+//    8 (l / 16) .. +7 of it.  Every weight load of the GEMV is then one
+//    contiguous 1 KB wave access that feeds v_mfma_f32_16x16x32_bf16
+//    directly, with no LDS staging and no lane shuffles.
+//  * The batch (up to 64 sequences) forms the MFMA's B columns, in up to four
+//    16-column tiles; x rows past the batch read as zeros through the buffer
+//    descriptor's size.
+//  * One workgroup per 16-row tile, its 8 waves splitting K, so a 6144-row
+//    projection runs 384 workgroups and every wave streams one contiguous
+//    run of packed weights; the waves' partial sums meet in LDS.
+//  * The epilogue (bias, RMSNorm, rotation, bf16 rounding, and optionally the
+//    KV append into the page slot) runs per (sequence, head) on the fp32
+//    projection: a head's norm and its rotation pairs need all of its rows,
+//    which no single GEMV workgroup holds.
+#include "pda_gemv.h"
+
+namespace pda {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBufferDword3 = 0x00020000;  // raw 32-bit buffer format
+constexpr int kCachePolicyNT = 2;          // non-temporal: weights are read once
+
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
+  void* ub = reinterpret_cast<void*>((static_cast<uint64_t>(hi) << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, static_cast<int>(__builtin_amdgcn_readfirstlane(bytes)),
+                                           kBufferDword3);
+}
+
+// Packed layout: tile (t, kt) of rows 16t .. 16t+15 and k 32kt .. 32kt+31 is
+// stored at element (t * (k / 32) + kt) * 512; inside it, 16-byte chunk l
+// holds W[16t + l % 16][32kt + 8 (l / 16) .. +7].  One thread per chunk.
+__global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __restrict__ w,
+                                                            uint16_t* __restrict__ wp, int n, int k) {
+  const int64_t chunk = static_cast<int64_t>(blockIdx.x) * kPackThreads + threadIdx.x;
+  const int64_t chunks = static_cast<int64_t>(n) * k / 8;
+  if (chunk >= chunks) return;
+  const int kt_count = k / kTileK;
+  const int64_t tile = chunk / 64;
+  const int l = static_cast<int>(chunk % 64);
+  const int64_t t = tile / kt_count;
+  const int kt = static_cast<int>(tile % kt_count);
+  const int64_t row = t * kTileRows + (l & 15);
+  const int64_t col = static_cast<int64_t>(kt) * kTileK + 8 * (l >> 4);
+  *reinterpret_cast<u32x4*>(wp + chunk * 8) = *reinterpret_cast<const u32x4*>(w + row * k + col);
+}
+
+// One workgroup per 16-row tile t; wave wv takes k tiles [wv*per, (wv+1)*per).
+template <int kNBT>
+__global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __restrict__ x,
+                                                            const uint16_t* __restrict__ wp,
+                                                            float* __restrict__ y, int batch, int n, int k) {
+  __shared__ f32x4 part[kGemvWaves][kNBT][64];
+  const int t = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wv = uniform(threadIdx.x >> 6);
+  const int kt_count = k / kTileK;
+  const int per = kt_count / kGemvWaves;
+  const int kt0 = wv * per;
+
+  const uint16_t* wbase = wp + (static_cast<int64_t>(t) * kt_count + kt0) * (kTileRows * kTileK);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(wbase, static_cast<uint32_t>(per) * 1024u);
+  // x rows at or past the batch fall outside the descriptor and read as zeros
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(batch) * k * 2u);
+  const int r = lane & 15;
+  const int g4 = lane >> 4;
+  int xoff[kNBT];
+#pragma unroll
+  for (int bt = 0; bt < kNBT; ++bt) xoff[bt] = ((16 * bt + r) * k + kt0 * kTileK + 8 * g4) * 2;
+
+  f32x4 acc[kNBT];
+#pragma unroll
+  for (int bt = 0; bt < kNBT; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  constexpr int kChunk = 8;  // k tiles whose loads are in flight together
+  for (int j0 = 0; j0 < per; j0 += kChunk) {
+    u32x4 wa[kChunk];
+    u32x4 xb[kChunk][kNBT];
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+      // tiles past the wave's share read as zeros (outside the descriptor)
+      wa[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
+#pragma unroll
+      for (int bt = 0; bt < kNBT; ++bt) {
+        const bool in = j0 + j < per;
+        xb[j][bt] = in ? __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[bt] + (j0 + j) * kTileK * 2, 0, 0)
+                       : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+      for (int bt = 0; bt < kNBT; ++bt)
+        acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[j]),
+                                                          __builtin_bit_cast(bf16x8, xb[j][bt]), acc[bt], 0,
+                                                          0, 0);
+  }
+
+#pragma unroll
+  for (int bt = 0; bt < kNBT; ++bt) part[wv][bt][lane] = acc[bt];
+  __syncthreads();
+  // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
+  const int tid = threadIdx.x;
+  if (tid < 64 * kNBT) {
+    const int bt = tid >> 6;
+    const int l = tid & 63;
+    f32x4 s = part[0][bt][l];
+#pragma unroll
+    for (int w2 = 1; w2 < kGemvWaves; ++w2) s += part[w2][bt][l];
+    const int b = 16 * bt + (l & 15);
+    if (b < batch)
+      *reinterpret_cast<f32x4*>(y + static_cast<int64_t>(b) * n + t * kTileRows + 4 * (l >> 4)) = s;
+  }
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __builtin_bit_cast(float, static_cast<uint32_t>(h) << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// One wave per (sequence b, head h) of the projection: h < hq is a q head,
+// then hkv k heads, then hkv v heads.  Lane owns elements lane + 64 j.
+template <int D>
+__global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
+  constexpr int E = D / 64;
+  __shared__ float s[D];
+  const int heads = a.hq + 2 * a.hkv;
+  const int b = blockIdx.x / heads;
+  const int h = blockIdx.x - b * heads;
+  const int lane = threadIdx.x;
+  const int n = heads * D;
+  const bool is_q = h < a.hq;
+  const bool is_k = !is_q && h < a.hq + a.hkv;
+
+  float v[E];
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = a.y[static_cast<int64_t>(b) * n + h * D + e];
+    if (a.bias) v[j] += bf16_to_f32(a.bias[h * D + e]);
+  }
+  const uint16_t* nw = is_q ? a.q_norm : (is_k ? a.k_norm : nullptr);
+  if (nw) {
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < E; ++j) ss += v[j] * v[j];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+    const float inv = rsqrtf(ss / D + a.eps);
+#pragma unroll
+    for (int j = 0; j < E; ++j) v[j] = v[j] * inv * bf16_to_f32(nw[lane + 64 * j]);
+  }
+  const int L = a.lens[b];
+  const int pos = L > 0 ? L - 1 : 0;
+  if ((is_q || is_k) && a.rotary_dim > 0) {
+#pragma unroll
+    for (int j = 0; j < E; ++j) s[lane + 64 * j] = v[j];
+    __syncthreads();
+    const int r = a.rotary_dim;
+    const double log2_theta = log2(static_cast<double>(a.theta));
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      const int e = lane + 64 * j;
+      if (e >= r) continue;
+      int i, partner;
+      bool first;
+      if (a.interleaved) {
+        i = e >> 1;
+        partner = e ^ 1;
+        first = (e & 1) == 0;
+      } else {
+        first = e < r / 2;
+        i = first ? e : e - r / 2;
+        partner = first ? e + r / 2 : e - r / 2;
+      }
+      // the angle p * theta^(-2i/r) in fp64: positions reach 10^5 and more,
+      // where an fp32 angle would already be off by ~10^-2 rad
+      const double ang = static_cast<double>(pos) * exp2(-(2.0 * i / r) * log2_theta);
+      double sd, cd;
+      sincos(ang, &sd, &cd);
+      const float c = static_cast<float>(cd), sn = static_cast<float>(sd);
+      const float other = s[partner];
+      v[j] = first ? v[j] * c - other * sn : v[j] * c + other * sn;
+    }
+  }
+
+  // outputs: q to q_out; k and v to k_out / v_out and, with a cache, to the page slot
+  uint16_t* dst = nullptr;
+  uint16_t* cache = nullptr;
+  int64_t row = 0;
+  if (is_q) {
+    dst = a.q_out + (static_cast<int64_t>(b) * a.hq + h) * D;
+  } else {
+    const int g = is_k ? h - a.hq : h - a.hq - a.hkv;
+    uint16_t* out = is_k ? a.k_out : a.v_out;
+    if (out) dst = out + (static_cast<int64_t>(b) * a.hkv + g) * D;
+    cache = is_k ? a.k_cache : a.v_cache;
+    if (cache) {
+      const int max_ctx = a.maxp << a.page_shift;
+      const int Lc = L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
+      if (Lc == 0) {
+        cache = nullptr;  // no token in this slot: nothing to append
+      } else {
+        const int t = Lc - 1;
+        const unsigned raw = static_cast<unsigned>(a.bt[static_cast<int64_t>(b) * a.maxp + (t >> a.page_shift)]);
+        const int64_t page = raw < static_cast<unsigned>(a.num_pages) ? raw : a.num_pages - 1;
+        row = (((page << a.page_shift) + (t & ((1 << a.page_shift) - 1))) * a.hkv + g) * D;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const uint16_t o = f32_to_bf16(v[j]);
+    if (dst) dst[lane + 64 * j] = o;
+    if (cache) cache[row + lane + 64 * j] = o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_t st) {
+  const int64_t chunks = static_cast<int64_t>(n) * k / 8;
+  const dim3 grid(static_cast<unsigned>((chunks + kPackThreads - 1) / kPackThreads));
+  hipLaunchKernelGGL(pack_kernel, grid, dim3(kPackThreads), 0, st, w, wp, n, k);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
+  const dim3 grid(a.n / kTileRows);
+  const int nbt = (a.batch + 15) / 16;
+  switch (nbt) {
+    case 1: hipLaunchKernelGGL((gemv_kernel<1>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<2>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
+    case 3: hipLaunchKernelGGL((gemv_kernel<3>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
+    default: hipLaunchKernelGGL((gemv_kernel<4>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_prelude_epilogue(const PreludeArgs& a, hipStream_t st) {
+  const dim3 grid(a.batch * (a.hq + 2 * a.hkv));
+  if (a.d == 64)
+    hipLaunchKernelGGL((prelude_epilogue<64>), grid, dim3(64), 0, st, a);
+  else if (a.d == 128)
+    hipLaunchKernelGGL((prelude_epilogue<128>), grid, dim3(64), 0, st, a);
+  else
+    hipLaunchKernelGGL((prelude_epilogue<256>), grid, dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace pda

@@ -182,3 +182,64 @@ def test_workspace_covers_every_num_queries(lib):
     _, _, ws = B.plan(4, 32, 8, 128, 16, 512, num_cus=256)
     g, _, _ = B.plan(4, 32, 8, 128, 16, 512, num_cus=256)
     assert ws >= (g + 4) * 8 * 16 * (128 + 2) * 4
+
+
+# ------------------------------------------------------------------ prelude
+def dims(**kw):
+    d = dict(batch=2, hidden=512, hq=8, hkv=2, d=128, rotary_dim=128, interleaved=0, theta=1e4, eps=1e-6)
+    d.update(kw)
+    return B.PreludeDims(d["batch"], d["hidden"], d["hq"], d["hkv"], d["d"], d["rotary_dim"], d["interleaved"],
+                         d["theta"], d["eps"])
+
+
+def prelude_call(ptrs=None, **kw):
+    p = ptrs or [16] * 9
+    return B.load().pda_attention_prelude(*p, ctypes.byref(dims(**kw)), None)
+
+
+@pytest.mark.parametrize("kwargs,code,text", [
+    (dict(batch=-1), SHAPE, "batch"),
+    (dict(batch=65), UNSUPPORTED, "batch"),
+    (dict(hidden=300), UNSUPPORTED, "hidden"),
+    (dict(hidden=0), SHAPE, "positive"),
+    (dict(hkv=3), SHAPE, "multiple"),
+    (dict(d=96), UNSUPPORTED, "head_dim"),
+    (dict(rotary_dim=7), SHAPE, "rotary_dim"),
+    (dict(rotary_dim=130), SHAPE, "rotary_dim"),
+    (dict(interleaved=2), SHAPE, "interleaved"),
+    (dict(theta=0.0), SCALE, "rope_theta"),
+    (dict(theta=float("inf")), SCALE, "rope_theta"),
+    (dict(eps=-1.0), SCALE, "eps"),
+    (dict(ptrs=[0] + [16] * 8), NULL, "NULL"),
+    (dict(ptrs=[16, 16, 0, 16, 0, 16, 16, 16, 16]), NULL, "both"),   # q_norm without k_norm
+    (dict(ptrs=[16, 16, 0, 0, 0, 16, 16, 16, 24]), ALIGN, "16-byte"),
+    (dict(ptrs=[24, 16, 0, 0, 0, 16, 16, 16, 16]), ALIGN, "16-byte"),
+])
+def test_prelude_argument_errors(lib, kwargs, code, text):
+    rc = prelude_call(**kwargs)
+    assert rc == code, B.last_error()
+    assert text in B.last_error()
+
+
+def test_prelude_dims_null_and_empty_batch(lib):
+    assert B.load().pda_attention_prelude(*[16] * 9, None, None) == NULL
+    assert prelude_call(ptrs=[0] * 9, batch=0) == OK
+
+
+def test_prelude_append_checks_the_cache_arguments(lib):
+    f = B.load().pda_attention_prelude_append
+    d = dims()
+    assert f(*[16] * 10, 24, 64, 8, ctypes.byref(d), None) == UNSUPPORTED          # page size
+    assert f(*[16] * 10, 16, 0, 8, ctypes.byref(d), None) == SHAPE                 # num_pages
+    assert f(*[16] * 7, 0, 16, 16, 16, 64, 8, ctypes.byref(d), None) == NULL       # k_cache
+    assert f(*[16] * 7, 24, 16, 16, 16, 64, 8, ctypes.byref(d), None) == ALIGN
+
+
+@pytest.mark.parametrize("rows,cols,code", [(15, 64, SHAPE), (16, 48, SHAPE), (0, 64, SHAPE)])
+def test_pack_argument_errors(lib, rows, cols, code):
+    assert B.load().pda_pack_weights(16, 1 << 20, rows, cols, None) == code
+
+
+def test_pack_rejects_overlap_and_null(lib):
+    assert B.load().pda_pack_weights(4096, 4096 + 512, 16, 64, None) == SHAPE
+    assert B.load().pda_pack_weights(0, 4096, 16, 64, None) == NULL

@@ -365,7 +365,7 @@ class PreludeConfig:
     theta: float
     qk_norm: bool = False
     bias: bool = False
-    rotary_dim: int = 0          # 0 = head_dim
+    rotary_dim: Optional[int] = None   # None = head_dim, 0 = no rotation
     interleaved: bool = False
     description: str = ""
 
@@ -435,12 +435,13 @@ class PreludeWorkload:
 
 
 def build_prelude(batch, hidden, num_q_heads, num_kv_heads, head_dim, seed, *, lengths=None,
-                  theta=1.0e4, qk_norm=False, bias=False, rotary_dim=0, interleaved=False,
+                  theta=1.0e4, qk_norm=False, bias=False, rotary_dim=None, interleaved=False,
                   eps=1e-6, name="custom", rng=None) -> PreludeWorkload:
     """Seeded prelude inputs.  Draw order: lengths (by the caller), x, W,
     bias, q_norm, k_norm.  x ~ N(0, 1) (a normalised hidden state); W ~
     N(0, 1/hidden) so that q, k, v are O(1); bias ~ N(0, 0.1^2); norm
-    weights ~ 1 + N(0, 0.1^2)."""
+    weights ~ 1 + N(0, 0.1^2).  ``rotary_dim`` None means the whole head,
+    0 no rotation."""
     if rng is None:
         rng = np.random.Generator(np.random.PCG64(seed))
     n = (num_q_heads + 2 * num_kv_heads) * head_dim
@@ -456,7 +457,7 @@ def build_prelude(batch, hidden, num_q_heads, num_kv_heads, head_dim, seed, *, l
     return PreludeWorkload(x=x, w_qkv=w, bias=bvec, q_norm=qn, k_norm=kn,
                            context_lens=np.asarray(lengths, dtype=np.int32), num_q_heads=num_q_heads,
                            num_kv_heads=num_kv_heads, head_dim=head_dim, theta=np.float32(theta),
-                           eps=np.float32(eps), rotary_dim=int(rotary_dim or head_dim),
+                           eps=np.float32(eps), rotary_dim=head_dim if rotary_dim is None else int(rotary_dim),
                            interleaved=bool(interleaved), name=name)
 
 
