@@ -35,7 +35,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long70b",
-                    choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16"])
+                    choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16",
+                             "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
+                             "prelude_falcon3"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the oracle cpu_baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -129,6 +131,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.workload.startswith("prelude_"):
+        prelude_main(args)
         return
 
     import torch
@@ -299,10 +304,174 @@ def main():
     print(json.dumps(res), flush=True)
 
 
-def _kernel_sha():
+def prelude_main(args):
+    """The attention prelude (QKV GEMV + RoPE, optionally Q/K RMSNorm) of one
+    decode step.  Weights are packed once; the timed calls cycle over enough
+    copies of the layer's weights (>= 2 GB in all) that every call reads its
+    weights from HBM, not from the 256 MB last-level cache, as a model's
+    successive layers would."""
+    import torch
+    import workloads as W
+    from paper_2606_07665_amd import binding as pda
+
+    pda.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = W.make_prelude(args.workload)
+    dev = torch.device("cuda:0")
+
+    def bf(a):
+        if a is None:
+            return None
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    x, bias, qn, kn = bf(w.x), bf(w.bias), bf(w.q_norm), bf(w.k_norm)
+    lens = torch.from_numpy(w.context_lens).to(dev)
+    wp0 = pda.pack_weights(bf(w.w_qkv))
+    wbytes = 2 * w.rows * w.hidden
+    layers = max(1, -(-2_000_000_000 // wbytes))
+    wps = [wp0] + [wp0.clone() for _ in range(layers - 1)]
+    b, hq, hkv, d = w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim
+    q = torch.empty((b, hq, d), dtype=torch.bfloat16, device=dev)
+    k = torch.empty((b, hkv, d), dtype=torch.bfloat16, device=dev)
+    v = torch.empty_like(k)
+    stream = torch.cuda.current_stream()
+    kw = dict(num_q_heads=hq, num_kv_heads=hkv, head_dim=d, rope_theta=float(w.theta), rotary_dim=w.rotary_dim,
+              interleaved=w.interleaved, bias=bias, q_norm=qn, k_norm=kn, eps=float(w.eps))
+    it = [0]
+
+    def call():
+        pda.attention_prelude(x, wps[it[0] % layers], lens, q, k, v, **kw)
+        it[0] += 1
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+
+    pda.profile_enable(True)
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    gemv_ms, epi_ms, n = pda.profile_read_prelude()
+    pda.profile_enable(False)
+    gemv_ms /= max(n, 1)
+    epi_ms /= max(n, 1)
+
+    graph_us = None
+    if not args.no_graph:
+        s = torch.cuda.Stream()
+        pda.prelude_workspace_reserve(pda.prelude_dims(b, w.hidden, hq, hkv, d, w.rotary_dim, w.interleaved,
+                                                       w.theta, w.eps), stream=s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for i in range(20):
+                pda.attention_prelude(x, wps[i % layers], lens, q, k, v, **kw)
+        g.replay()
+        torch.cuda.synchronize()
+        reps = max(1, args.steps // 20)
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for _ in range(reps):
+            g.replay()
+        g1.record()
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) / (reps * 20) * 1e3
+
+    nbytes = w.algorithmic_bytes()
+    gemv_bytes = 2 * w.rows * w.hidden + 2 * b * w.hidden     # weights once, x in
+    value = nbytes / (ms_per_step * 1e-3) / 1e9
+    achieved = gemv_bytes / (gemv_ms * 1e-3) / 1e9
+    traffic = None
+    path = os.path.join(ROOT, "profiles", "traffic_prelude.json")
+    if os.path.exists(path):
+        try:
+            t = json.load(open(path))
+            if t.get("kernel_source_sha") == _kernel_sha(PRELUDE_SOURCES) and args.workload in t:
+                traffic = t[args.workload].get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    res = {
+        "metric": "attention prelude (QKV GEMV + RoPE) µs/call + achieved HBM GB/s (% of MI355X peak), 1 GPU",
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "us_per_call": round(ms_per_step * 1e3, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload, "batch": b, "hidden": w.hidden, "num_q_heads": hq, "num_kv_heads": hkv,
+            "head_dim": d, "rotary_dim": w.rotary_dim, "interleaved": w.interleaved,
+            "qk_norm": w.q_norm is not None, "bias": w.bias is not None, "weight_copies": layers,
+            "algorithmic_bytes": nbytes, "parallelism": "single GPU", "device": torch.cuda.get_device_name(0),
+        },
+        "kernels_ms": {"gemv": round(gemv_ms, 5), "epilogue": round(epi_ms, 5)},
+        "graph_us_per_call": None if graph_us is None else round(graph_us, 2),
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
+            "kernel": "gemv_kernel (packed-weight MFMA GEMV of the QKV projection)",
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = prelude_cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+def prelude_cpu_baseline(w, budget_s):
+    """The fp64 oracle prelude on the same workload, one thread, repeated
+    until the budget is used."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:  # pragma: no cover
+        limiter = None
+    calls = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.prelude(w.x, w.w_qkv, w.num_q_heads, w.num_kv_heads, w.head_dim, w.context_lens, w.theta,
+                       bias=w.bias, q_norm=w.q_norm, k_norm=w.k_norm, eps=w.eps, rotary_dim=w.rotary_dim,
+                       interleaved=w.interleaved)
+        calls += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    if limiter is not None and hasattr(limiter, "unregister"):
+        limiter.unregister()
+    return {
+        "value": round(w.algorithmic_bytes() * calls / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{calls} whole calls of the same workload, {dt:.1f} s single-threaded fp64 numpy; "
+                  f"host has {os.cpu_count()} logical cpus",
+        "us_per_call_equiv": round(dt / calls * 1e6, 1),
+    }
+
+
+ATTENTION_SOURCES = ("pda_kernels.hip", "pda_internal.h")
+PRELUDE_SOURCES = ("pda_gemv.hip", "pda_gemv.h")
+
+
+def _kernel_sha(files=ATTENTION_SOURCES):
     import hashlib
     h = hashlib.sha256()
-    for f in ("pda_kernels.hip", "pda_internal.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2606_07665_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -223,14 +223,17 @@ int pda_set_option(int32_t option, int32_t value);
 int32_t pda_get_option(int32_t option);
 
 /*
- * Kernel timing for measurement harnesses.  While enabled, every
- * paged_decode_attention call records HIP events on its stream around each
- * kernel it launches.  pda_profile_read synchronises those events, returns
+ * Kernel timing for measurement harnesses.  While enabled, every attention
+ * call (paged_decode_attention and its _ext / _append forms) and every
+ * prelude call records HIP events on its stream around each kernel it
+ * launches.  pda_profile_read synchronises those events, returns
  * the summed milliseconds of the split kernel and of the merge kernel and
  * the number of calls recorded since the last read, and clears the record.
  */
 int pda_profile_enable(int32_t on);
 int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls);
+/* The same for the prelude calls: summed GEMV and epilogue milliseconds. */
+int pda_profile_read_prelude(double* gemv_ms, double* epilogue_ms, int64_t* calls);
 
 /*
  * ---------------------------------------------------------------------------

@@ -76,6 +76,8 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.pda_profile_read.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(i64)]
     lib.pda_profile_read.restype = ctypes.c_int
+    lib.pda_profile_read_prelude.argtypes = lib.pda_profile_read.argtypes
+    lib.pda_profile_read_prelude.restype = ctypes.c_int
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -328,4 +330,11 @@ def profile_read() -> Tuple[float, float, int]:
     """(split kernel ms, merge kernel ms, calls) summed since the last read."""
     s, m, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
     _check(load().pda_profile_read(ctypes.byref(s), ctypes.byref(m), ctypes.byref(n)))
+    return s.value, m.value, n.value
+
+
+def profile_read_prelude() -> Tuple[float, float, int]:
+    """(GEMV kernel ms, epilogue kernel ms, prelude calls) summed since the last read."""
+    s, m, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+    _check(load().pda_profile_read_prelude(ctypes.byref(s), ctypes.byref(m), ctypes.byref(n)))
     return s.value, m.value, n.value

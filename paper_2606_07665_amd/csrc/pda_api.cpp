@@ -203,8 +203,11 @@ int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
 }
 
 // ---------------------------------------------------------------- profiling
+// Events around the two kernels of a call: kind 0 is attention (split,
+// merge), kind 1 the prelude (GEMV, epilogue).
 struct Rec {
   hipEvent_t a, b, c;
+  int kind;
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
@@ -220,6 +223,51 @@ hipEvent_t prof_event() {
   hipEvent_t e = nullptr;
   if (hipEventCreate(&e) != hipSuccess) return nullptr;
   return e;
+}
+
+// A record with three events when profiling is on, else one with none.
+Rec prof_begin(int kind) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  if (!g_prof_on) return Rec{nullptr, nullptr, nullptr, kind};
+  Rec r{prof_event(), prof_event(), prof_event(), kind};
+  if (!r.a || !r.b || !r.c) return Rec{nullptr, nullptr, nullptr, kind};
+  return r;
+}
+
+void prof_push(const Rec& r) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_prof_recs.push_back(r);
+}
+
+// Sum the two intervals of every record of `kind`, release them.
+int prof_read(int kind, double* first_ms, double* second_ms, int64_t* calls) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  double s = 0, m = 0;
+  int64_t n = 0;
+  int rc = PDA_OK;
+  std::vector<Rec> keep;
+  for (const Rec& r : g_prof_recs) {
+    if (r.kind != kind) {
+      keep.push_back(r);
+      continue;
+    }
+    float t1 = 0, t2 = 0;
+    hipError_t e = hipEventSynchronize(r.c);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t1, r.a, r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t2, r.b, r.c);
+    if (e != hipSuccess) rc = hip_fail(e, "reading profile events");
+    s += t1;
+    m += t2;
+    ++n;
+    g_prof_pool.push_back(r.a);
+    g_prof_pool.push_back(r.b);
+    g_prof_pool.push_back(r.c);
+  }
+  g_prof_recs.swap(keep);
+  *first_ms = s;
+  *second_ms = m;
+  *calls = n;
+  return rc;
 }
 
 // ---------------------------------------------------------------- prelude
@@ -255,8 +303,13 @@ int64_t prelude_rows(const pda_prelude_dims& d) {
   return static_cast<int64_t>(d.num_q_heads + 2 * d.num_kv_heads) * d.head_dim;
 }
 
-int64_t prelude_ws_bytes(const pda_prelude_dims& d) {
-  return align256(static_cast<int64_t>(d.batch) * prelude_rows(d) * 4);
+// The GEMV plan of a prelude on this device's compute units.
+pda::GemvPlan prelude_plan(const pda_prelude_dims& d, int cus) {
+  return pda::plan_gemv(d.batch, static_cast<int>(prelude_rows(d)), d.hidden, cus);
+}
+
+int64_t prelude_ws_bytes(const pda_prelude_dims& d, int cus) {
+  return align256(pda::gemv_partial_floats(prelude_plan(d, cus), d.batch, static_cast<int>(prelude_rows(d))) * 4);
 }
 
 // Shared by both prelude entry points once their own arguments are checked.
@@ -273,19 +326,27 @@ int run_prelude(const void* x, const void* w_packed, const void* bias, const voi
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  int rc = device_cus(dev, &cus);
+  if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
-  int rc = workspace_for(dev, st, prelude_ws_bytes(d), &ws);
-  if (rc) return rc;
+  if ((rc = workspace_for(dev, st, prelude_ws_bytes(d, cus), &ws))) return rc;
   pda::GemvArgs g;
   g.x = static_cast<const uint16_t*>(x);
   g.wp = static_cast<const uint16_t*>(w_packed);
-  g.y = static_cast<float*>(ws);
+  g.part = static_cast<float*>(ws);
   g.batch = d.batch;
   g.n = static_cast<int>(prelude_rows(d));
   g.k = d.hidden;
+  g.plan = prelude_plan(d, cus);
+  const Rec rec = prof_begin(1);
+  const bool prof = rec.a != nullptr;
+  if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if ((e = pda::launch_gemv(g, st)) != hipSuccess) return hip_fail(e, "GEMV kernel launch");
-  ep.y = g.y;
+  if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  ep.part = g.part;
+  ep.plan = g.plan;
   ep.bias = static_cast<const uint16_t*>(bias);
   ep.q_norm = static_cast<const uint16_t*>(q_norm);
   ep.k_norm = static_cast<const uint16_t*>(k_norm);
@@ -300,6 +361,10 @@ int run_prelude(const void* x, const void* w_packed, const void* bias, const voi
   ep.theta = d.rope_theta;
   ep.eps = d.eps;
   if ((e = pda::launch_prelude_epilogue(ep, st)) != hipSuccess) return hip_fail(e, "prelude epilogue launch");
+  if (prof) {
+    if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    prof_push(rec);
+  }
   return PDA_OK;
 }
 
@@ -397,26 +462,13 @@ int pda_profile_enable(int32_t on) {
 int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls) {
   g_err.clear();
   if (!split_ms || !merge_ms || !calls) return fail(PDA_ERR_NULL, "pda_profile_read: NULL output pointer");
-  std::lock_guard<std::mutex> lock(g_prof_mu);
-  double s = 0, m = 0;
-  int rc = PDA_OK;
-  for (const Rec& r : g_prof_recs) {
-    float t1 = 0, t2 = 0;
-    hipError_t e = hipEventSynchronize(r.c);
-    if (e == hipSuccess) e = hipEventElapsedTime(&t1, r.a, r.b);
-    if (e == hipSuccess) e = hipEventElapsedTime(&t2, r.b, r.c);
-    if (e != hipSuccess) rc = hip_fail(e, "reading profile events");
-    s += t1;
-    m += t2;
-    g_prof_pool.push_back(r.a);
-    g_prof_pool.push_back(r.b);
-    g_prof_pool.push_back(r.c);
-  }
-  *split_ms = s;
-  *merge_ms = m;
-  *calls = static_cast<int64_t>(g_prof_recs.size());
-  g_prof_recs.clear();
-  return rc;
+  return prof_read(0, split_ms, merge_ms, calls);
+}
+
+int pda_profile_read_prelude(double* gemv_ms, double* epilogue_ms, int64_t* calls) {
+  g_err.clear();
+  if (!gemv_ms || !epilogue_ms || !calls) return fail(PDA_ERR_NULL, "pda_profile_read_prelude: NULL output pointer");
+  return prof_read(1, gemv_ms, epilogue_ms, calls);
 }
 
 int pda_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
@@ -544,15 +596,8 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
   a.nq = num_queries;
   a.window = window;
 
-  Rec rec{nullptr, nullptr, nullptr};
-  bool prof = false;
-  {
-    std::lock_guard<std::mutex> lock(g_prof_mu);
-    if (g_prof_on) {
-      rec = Rec{prof_event(), prof_event(), prof_event()};
-      prof = rec.a && rec.b && rec.c;
-    }
-  }
+  const Rec rec = prof_begin(0);
+  const bool prof = rec.a != nullptr;
   if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if ((e = pda::launch_attn_kernel(a, st)) != hipSuccess) return hip_fail(e, "attention kernel launch");
   if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -561,8 +606,7 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
     return hip_fail(e, "merge kernel launch");
   if (prof) {
     if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    std::lock_guard<std::mutex> lock(g_prof_mu);
-    g_prof_recs.push_back(rec);
+    prof_push(rec);
   }
   return PDA_OK;
 }
@@ -637,8 +681,10 @@ int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  if ((rc = device_cus(dev, &cus))) return rc;
   void* ptr = nullptr;
-  return workspace_for(dev, static_cast<hipStream_t>(stream), prelude_ws_bytes(*dims), &ptr);
+  return workspace_for(dev, static_cast<hipStream_t>(stream), prelude_ws_bytes(*dims, cus), &ptr);
 }
 
 }  // extern "C"

@@ -5,23 +5,40 @@
 
 namespace pda {
 
-constexpr int kGemvWaves = 8;                   // waves per GEMV workgroup, splitting K
+constexpr int kGemvWaves = 4;                   // independent waves per GEMV workgroup
 constexpr int kGemvThreads = 64 * kGemvWaves;
+constexpr int kGemvBlocksPerCu = 3;
+constexpr int kGemvMinTiles = 4;                // fewest k tiles a wave is given
+constexpr int kGemvMaxSlots = 16;               // most waves sharing one 16-row tile
 constexpr int kTileRows = 16;                   // rows of W per MFMA tile
 constexpr int kTileK = 32;                      // k per MFMA tile
 constexpr int kMaxGemvBatch = 64;               // sequences: four 16-column tiles
 constexpr int kPackThreads = 256;
 
-// y[b, n] = sum_k x[b, k] W[n, k] over a packed W (see launch_pack), fp32 out.
+// y[b, n] = sum_k x[b, k] W[n, k] over a packed W (see launch_pack), as
+// fp32 partials: part[t][j][b][16] holds the contribution of the j-th wave
+// that touched 16-row tile t.  GemvPlan says how the waves split the work.
+struct GemvPlan {
+  int grid;     // workgroups of kGemvWaves waves
+  int slots;    // partial slots per row tile (an upper bound)
+  int64_t waves, units;
+  int kt_count;
+};
+
+GemvPlan plan_gemv(int batch, int n, int k, int num_cus);
+int64_t gemv_partial_floats(const GemvPlan& p, int batch, int n);
+
 struct GemvArgs {
   const uint16_t* x;   // bf16 [batch, k]
   const uint16_t* wp;  // packed bf16 [n, k]
-  float* y;            // fp32 [batch, n]
+  float* part;         // fp32 partials, gemv_partial_floats() of them
   int batch, n, k;
+  GemvPlan plan;
 };
 
 struct PreludeArgs {
-  const float* y;            // fp32 [batch, (hq + 2 hkv) * d]
+  const float* part;         // GEMV partials of y [batch, (hq + 2 hkv) * d]
+  GemvPlan plan;
   const uint16_t* bias;      // bf16 [(hq + 2 hkv) * d] or null
   const uint16_t* q_norm;    // bf16 [d] or null
   const uint16_t* k_norm;    // bf16 [d] or null

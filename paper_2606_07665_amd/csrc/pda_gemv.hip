@@ -16,13 +16,15 @@
 //  * The batch (up to 64 sequences) forms the MFMA's B columns, in up to four
 //    16-column tiles; x rows past the batch read as zeros through the buffer
 //    descriptor's size.
-//  * One workgroup per 16-row tile, its 8 waves splitting K, so a 6144-row
-//    projection runs 384 workgroups and every wave streams one contiguous
-//    run of packed weights; the waves' partial sums meet in LDS.
-//  * The epilogue (bias, RMSNorm, rotation, bf16 rounding, and optionally the
-//    KV append into the page slot) runs per (sequence, head) on the fp32
-//    projection: a head's norm and its rotation pairs need all of its rows,
-//    which no single GEMV workgroup holds.
+//  * Stream-K over (16-row tile, 32-k tile) units: every wave of a grid sized
+//    to the device streams the same number of packed weight tiles, whatever
+//    the shape, so no half-empty last round of workgroups; a wave leaves one
+//    fp32 partial per row tile it touched and the epilogue adds a tile's
+//    partials in wave order.
+//  * The epilogue (partial sums, bias, RMSNorm, rotation, bf16 rounding, and
+//    optionally the KV append into the page slot) runs per (sequence, head):
+//    a head's norm and its rotation pairs need all of its rows, which no
+//    single wave of the GEMV holds.
 #include "pda_gemv.h"
 
 namespace pda {
@@ -64,72 +66,96 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
   *reinterpret_cast<u32x4*>(wp + chunk * 8) = *reinterpret_cast<const u32x4*>(w + row * k + col);
 }
 
-// One workgroup per 16-row tile t; wave wv takes k tiles [wv*per, (wv+1)*per).
+// Stream-K GEMV: the flattened space of (16-row tile t, 32-k tile) units is
+// cut into equal contiguous ranges, one per wave, so every wave streams the
+// same number of packed weight tiles whatever the matrix shape.  A wave
+// writes one partial (16 rows x batch, fp32) per row tile its range touches,
+// into slot j = wave - first_wave(t) of that tile; the epilogue sums a tile's
+// slots in order (deterministic).
 template <int kNBT>
 __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __restrict__ x,
                                                             const uint16_t* __restrict__ wp,
-                                                            float* __restrict__ y, int batch, int n, int k) {
-  __shared__ f32x4 part[kGemvWaves][kNBT][64];
-  const int t = blockIdx.x;
+                                                            float* __restrict__ part, int batch, int n, int k,
+                                                            int slots) {
   const int lane = threadIdx.x & 63;
-  const int wv = uniform(threadIdx.x >> 6);
+  const int64_t waves = static_cast<int64_t>(gridDim.x) * (kGemvThreads / 64);
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * (kGemvThreads / 64) + uniform(threadIdx.x >> 6);
   const int kt_count = k / kTileK;
-  const int per = kt_count / kGemvWaves;
-  const int kt0 = wv * per;
+  const int64_t units = static_cast<int64_t>(n / kTileRows) * kt_count;
+  int64_t u = w * units / waves;
+  const int64_t u_end = (w + 1) * units / waves;
+  if (u >= u_end) return;
 
-  const uint16_t* wbase = wp + (static_cast<int64_t>(t) * kt_count + kt0) * (kTileRows * kTileK);
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(wbase, static_cast<uint32_t>(per) * 1024u);
   // x rows at or past the batch fall outside the descriptor and read as zeros
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(batch) * k * 2u);
   const int r = lane & 15;
   const int g4 = lane >> 4;
-  int xoff[kNBT];
+  int xrow[kNBT];
 #pragma unroll
-  for (int bt = 0; bt < kNBT; ++bt) xoff[bt] = ((16 * bt + r) * k + kt0 * kTileK + 8 * g4) * 2;
+  for (int bt = 0; bt < kNBT; ++bt) xrow[bt] = ((16 * bt + r) * k + 8 * g4) * 2;
 
-  f32x4 acc[kNBT];
-#pragma unroll
-  for (int bt = 0; bt < kNBT; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  while (u < u_end) {
+    const int t = static_cast<int>(u / kt_count);
+    const int kt0 = static_cast<int>(u - static_cast<int64_t>(t) * kt_count);
+    const int64_t seg_end = u_end < static_cast<int64_t>(t + 1) * kt_count ? u_end
+                                                                           : static_cast<int64_t>(t + 1) * kt_count;
+    const int per = static_cast<int>(seg_end - u);
+    const uint16_t* wbase = wp + (static_cast<int64_t>(t) * kt_count + kt0) * (kTileRows * kTileK);
+    // tiles past the segment read as zeros (outside the weight descriptor)
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(wbase, static_cast<uint32_t>(per) * 1024u);
 
-  constexpr int kChunk = 8;  // k tiles whose loads are in flight together
-  for (int j0 = 0; j0 < per; j0 += kChunk) {
-    u32x4 wa[kChunk];
-    u32x4 xb[kChunk][kNBT];
+    f32x4 acc[kNBT];
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j) {
-      // tiles past the wave's share read as zeros (outside the descriptor)
-      wa[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
+    for (int bt = 0; bt < kNBT; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    constexpr int kChunk = kNBT == 1 ? 8 : 4;  // k tiles whose loads are in flight together
+    for (int j0 = 0; j0 < per; j0 += kChunk) {
+      u32x4 wa[kChunk];
+      u32x4 xb[kChunk][kNBT];
 #pragma unroll
-      for (int bt = 0; bt < kNBT; ++bt) {
+      for (int j = 0; j < kChunk; ++j) {
+        wa[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
         const bool in = j0 + j < per;
-        xb[j][bt] = in ? __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[bt] + (j0 + j) * kTileK * 2, 0, 0)
-                       : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int bt = 0; bt < kNBT; ++bt)
+          xb[j][bt] = in ? __builtin_amdgcn_raw_buffer_load_b128(rx, xrow[bt] + (kt0 + j0 + j) * kTileK * 2, 0, 0)
+                         : u32x4{0u, 0u, 0u, 0u};
       }
+#pragma unroll
+      for (int j = 0; j < kChunk; ++j)
+#pragma unroll
+        for (int bt = 0; bt < kNBT; ++bt)
+          acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[j]),
+                                                            __builtin_bit_cast(bf16x8, xb[j][bt]), acc[bt], 0,
+                                                            0, 0);
     }
+    // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
+    const int64_t first = (static_cast<int64_t>(t) * kt_count * waves + waves - 1) / units;  // first wave of t
+    float* slot = part + ((static_cast<int64_t>(t) * slots + (w - first)) * batch) * kTileRows;
 #pragma unroll
-    for (int j = 0; j < kChunk; ++j)
-#pragma unroll
-      for (int bt = 0; bt < kNBT; ++bt)
-        acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[j]),
-                                                          __builtin_bit_cast(bf16x8, xb[j][bt]), acc[bt], 0,
-                                                          0, 0);
+    for (int bt = 0; bt < kNBT; ++bt) {
+      const int b = 16 * bt + r;
+      if (b < batch) *reinterpret_cast<f32x4*>(slot + b * kTileRows + 4 * g4) = acc[bt];
+    }
+    u = seg_end;
   }
+}
 
+// y[b][row]: the sum, in wave order, of the partials of row's tile.
+__device__ __forceinline__ float gemv_result(const float* __restrict__ part, const GemvPlan& p, int batch, int b,
+                                             int row) {
+  const int t = row >> 4;
+  const int64_t x0 = static_cast<int64_t>(t) * p.kt_count;
+  const int64_t first = ((x0 + 1) * p.waves - 1) / p.units;
+  const int64_t last = ((x0 + p.kt_count) * p.waves - 1) / p.units;
+  const int cnt = static_cast<int>(last - first + 1);  // at most kGemvMaxSlots (plan_gemv)
+  const float* q = part + (static_cast<int64_t>(t) * p.slots * batch + b) * kTileRows + (row & 15);
+  float v[kGemvMaxSlots];
 #pragma unroll
-  for (int bt = 0; bt < kNBT; ++bt) part[wv][bt][lane] = acc[bt];
-  __syncthreads();
-  // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
-  const int tid = threadIdx.x;
-  if (tid < 64 * kNBT) {
-    const int bt = tid >> 6;
-    const int l = tid & 63;
-    f32x4 s = part[0][bt][l];
+  for (int j = 0; j < kGemvMaxSlots; ++j) v[j] = j < cnt ? q[static_cast<int64_t>(j) * batch * kTileRows] : 0.f;
+  float s = 0.f;
 #pragma unroll
-    for (int w2 = 1; w2 < kGemvWaves; ++w2) s += part[w2][bt][l];
-    const int b = 16 * bt + (l & 15);
-    if (b < batch)
-      *reinterpret_cast<f32x4*>(y + static_cast<int64_t>(b) * n + t * kTileRows + 4 * (l >> 4)) = s;
-  }
+  for (int j = 0; j < kGemvMaxSlots; ++j) s += v[j];
+  return s;
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
@@ -150,7 +176,6 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
   const int b = blockIdx.x / heads;
   const int h = blockIdx.x - b * heads;
   const int lane = threadIdx.x;
-  const int n = heads * D;
   const bool is_q = h < a.hq;
   const bool is_k = !is_q && h < a.hq + a.hkv;
 
@@ -158,7 +183,7 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
 #pragma unroll
   for (int j = 0; j < E; ++j) {
     const int e = lane + 64 * j;
-    v[j] = a.y[static_cast<int64_t>(b) * n + h * D + e];
+    v[j] = gemv_result(a.part, a.plan, a.batch, b, h * D + e);
     if (a.bias) v[j] += bf16_to_f32(a.bias[h * D + e]);
   }
   const uint16_t* nw = is_q ? a.q_norm : (is_k ? a.k_norm : nullptr);
@@ -247,14 +272,39 @@ hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_
   return hipGetLastError();
 }
 
+GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
+  (void)batch;
+  GemvPlan p;
+  p.kt_count = k / kTileK;
+  p.units = static_cast<int64_t>(n / kTileRows) * p.kt_count;
+  int64_t grid = static_cast<int64_t>(num_cus) * kGemvBlocksPerCu;
+  const int64_t most = (p.units + static_cast<int64_t>(kGemvWaves) * kGemvMinTiles - 1) /
+                       (static_cast<int64_t>(kGemvWaves) * kGemvMinTiles);
+  if (grid > most) grid = most;
+  // at most kGemvMaxSlots waves per row tile: waves <= (kGemvMaxSlots - 1) * tiles
+  const int64_t cap = static_cast<int64_t>(kGemvMaxSlots - 1) * (n / kTileRows) / kGemvWaves;
+  if (grid > cap) grid = cap;
+  if (grid < 1) grid = 1;
+  p.grid = static_cast<int>(grid);
+  p.waves = grid * kGemvWaves;
+  // waves touching one row tile: its kt_count units span at most this many ranges
+  p.slots = static_cast<int>((static_cast<int64_t>(p.kt_count) * p.waves + p.units - 1) / p.units + 1);
+  return p;
+}
+
+int64_t gemv_partial_floats(const GemvPlan& p, int batch, int n) {
+  return static_cast<int64_t>(n / kTileRows) * p.slots * batch * kTileRows;
+}
+
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
-  const dim3 grid(a.n / kTileRows);
+  const dim3 grid(a.plan.grid);
   const int nbt = (a.batch + 15) / 16;
+  const int sl = a.plan.slots;
   switch (nbt) {
-    case 1: hipLaunchKernelGGL((gemv_kernel<1>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<2>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
-    case 3: hipLaunchKernelGGL((gemv_kernel<3>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
-    default: hipLaunchKernelGGL((gemv_kernel<4>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.y, a.batch, a.n, a.k); break;
+    case 1: hipLaunchKernelGGL((gemv_kernel<1>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<2>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
+    case 3: hipLaunchKernelGGL((gemv_kernel<3>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
+    default: hipLaunchKernelGGL((gemv_kernel<4>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
   }
   return hipGetLastError();
 }
