@@ -36,6 +36,10 @@ v (Method, "Principle-Driven LLM Kernel Generator", kernel family (i): QKV
 projection plus rotary position embedding, optionally with a per-head
 RMSNorm of q and k).
 
+:func:`o_proj_residual_norm` is the step after attention (kernel family (v)
+of the same section: the output projection fused with the residual add and
+the RMSNorm that follows it).
+
 :func:`attend_masked` is the same definition with a key range per query:
 several query tokens per sequence (the decode steps that the paper's engine
 mixes with chunked prefill, each seeing only keys up to its own position)
@@ -57,7 +61,7 @@ import numpy as np
 
 __all__ = ["bf16_to_f64", "attend", "attend_pairs", "weights", "split_merge",
            "brute_force_tiny", "kv_append", "attend_masked", "visible_range",
-           "prelude", "rms_norm", "rope"]
+           "prelude", "rms_norm", "rope", "o_proj_residual_norm"]
 
 
 def bf16_to_f64(bits) -> np.ndarray:
@@ -384,3 +388,17 @@ def prelude(x, w_qkv, num_q_heads, num_kv_heads, head_dim, context_lens, theta, 
     q = rope(q, pos, theta, rd, interleaved)
     k = rope(k, pos, theta, rd, interleaved)
     return q, k, v.copy()
+
+
+def o_proj_residual_norm(attn, w_o, residual, norm_w, eps):
+    """Output projection + residual add + RMSNorm of one decode step, in fp64
+    (kernel family (v) of Method, "Principle-Driven LLM Kernel Generator").
+
+    attn: bf16 bits [B, K] (the attention output, heads concatenated);
+    w_o: bf16 bits [H, K]; residual: bf16 bits [B, H]; norm_w: bf16 bits [H].
+    z = W_o attn + residual is the new residual stream; h = RMSNorm(z) * w
+    over the H features is the next sublayer's input (z not rounded first).
+    Returns (z, h), float64 [B, H] each.
+    """
+    z = bf16_to_f64(attn) @ bf16_to_f64(w_o).T + bf16_to_f64(residual)
+    return z, rms_norm(z, norm_w, eps)

@@ -255,3 +255,47 @@ def test_each_prelude_mutant_is_caught(name, monkeypatch):
         except (AssertionError, ValueError, IndexError):
             failed.append(getattr(f, "__name__", str(f)))
     assert failed, f"mutant '{name}' passed every pin"
+
+
+# ------------------------------------------------------------------ o_proj
+import test_oracle_oproj as opins  # noqa: E402
+
+_oproj = oracle.o_proj_residual_norm
+
+
+def oproj_no_residual(attn, w_o, residual, norm_w, eps):
+    z = oracle.bf16_to_f64(attn) @ oracle.bf16_to_f64(w_o).T
+    return z, oracle.rms_norm(z, norm_w, eps)
+
+
+def oproj_norm_before_residual(attn, w_o, residual, norm_w, eps):
+    y = oracle.bf16_to_f64(attn) @ oracle.bf16_to_f64(w_o).T
+    z = y + oracle.bf16_to_f64(residual)
+    return z, oracle.rms_norm(y, norm_w, eps) + 0 * z
+
+
+def oproj_transposed(attn, w_o, residual, norm_w, eps):
+    a = oracle.bf16_to_f64(attn)
+    wt = oracle.bf16_to_f64(w_o)
+    z = (a @ wt.reshape(wt.shape[1], wt.shape[0])).reshape(len(a), -1)[:, :wt.shape[0]] + oracle.bf16_to_f64(residual)
+    return z, oracle.rms_norm(z, norm_w, eps)
+
+
+OPROJ_PINS = [opins.test_integer_projection_plus_residual_is_exact,
+              opins.test_norm_output_has_unit_rms_and_ignores_scale,
+              *[functools.partial(opins.test_matches_torch_linear_and_rms_norm, e) for e in (1e-6, 1e-5, 0.5)]]
+OPROJ_MUTANTS = {"residual dropped": oproj_no_residual, "norm of the projection alone": oproj_norm_before_residual,
+                 "weights read transposed": oproj_transposed}
+
+
+@pytest.mark.parametrize("name", list(OPROJ_MUTANTS))
+def test_each_oproj_mutant_is_caught(name, monkeypatch):
+    monkeypatch.setattr(oracle, "o_proj_residual_norm", OPROJ_MUTANTS[name])
+    failed = []
+    for f in OPROJ_PINS:
+        try:
+            with np.errstate(all="ignore"):
+                f()
+        except (AssertionError, ValueError, IndexError):
+            failed.append(getattr(f, "__name__", str(f)))
+    assert failed, f"mutant '{name}' passed every pin"

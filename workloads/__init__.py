@@ -471,3 +471,73 @@ def make_prelude(name: str, seed: Optional[int] = None) -> PreludeWorkload:
     return build_prelude(cfg.batch, cfg.hidden, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.seed,
                          lengths=lens, theta=cfg.theta, qk_norm=cfg.qk_norm, bias=cfg.bias,
                          rotary_dim=cfg.rotary_dim, interleaved=cfg.interleaved, name=name, rng=rng)
+
+
+
+# ------------------------------------------------------------------ o_proj
+@dataclasses.dataclass(frozen=True)
+class OProjConfig:
+    """One synthetic output-projection workload (o_proj + residual + RMSNorm)."""
+
+    name: str
+    batch: int
+    in_features: int   # Hq * D
+    hidden: int
+    seed: int
+    description: str = ""
+
+
+OPROJ_CONFIGS: Dict[str, OProjConfig] = {
+    "oproj_qwen3_4b": OProjConfig("oproj_qwen3_4b", 1, 4096, 2560, 20,
+                                  "Qwen3-4B-shaped o_proj, batch 1, 32 x 128 -> 2560"),
+    "oproj_llama8b": OProjConfig("oproj_llama8b", 64, 4096, 4096, 21,
+                                 "Llama-3-8B-shaped o_proj, batch 64, 4096 -> 4096"),
+    "oproj_70b": OProjConfig("oproj_70b", 4, 8192, 8192, 22, "70B-shaped o_proj, batch 4, 8192 -> 8192"),
+}
+
+
+@dataclasses.dataclass
+class OProjWorkload:
+    """Inputs of one o_proj + residual + RMSNorm call (host bf16 bits)."""
+
+    attn: np.ndarray      # [B, K]
+    w_o: np.ndarray       # [H, K]
+    residual: np.ndarray  # [B, H]
+    norm_w: np.ndarray    # [H]
+    eps: np.float32
+    name: str = "custom"
+
+    @property
+    def batch(self) -> int:
+        return self.attn.shape[0]
+
+    @property
+    def in_features(self) -> int:
+        return self.attn.shape[1]
+
+    @property
+    def hidden(self) -> int:
+        return self.w_o.shape[0]
+
+    def algorithmic_bytes(self) -> int:
+        """Weights once, attention output and residual in, residual and
+        normed outputs out, the norm weights."""
+        b, k, h = self.batch, self.in_features, self.hidden
+        return int(2 * h * k + 2 * b * k + 2 * b * h * 3 + 2 * h)
+
+
+def build_oproj(batch, in_features, hidden, seed, *, eps=1e-5, name="custom", rng=None) -> OProjWorkload:
+    """Seeded o_proj inputs.  Draw order: attn, W_o, residual, norm weights.
+    attn ~ N(0, 1); W_o ~ N(0, 1/K); residual ~ N(0, 1); weights ~ 1 + N(0, 0.1^2)."""
+    if rng is None:
+        rng = np.random.Generator(np.random.PCG64(seed))
+    attn = _normal_bf16(rng, (batch, in_features), 1.0)
+    w = _normal_bf16(rng, (hidden, in_features), 1.0 / math.sqrt(in_features))
+    res = _normal_bf16(rng, (batch, hidden), 1.0)
+    nw = f32_to_bf16_bits(bf16_bits_to_f32(_normal_bf16(rng, (hidden,), 0.1)) + np.float32(1.0))
+    return OProjWorkload(attn=attn, w_o=w, residual=res, norm_w=nw, eps=np.float32(eps), name=name)
+
+
+def make_oproj(name: str, seed: Optional[int] = None) -> OProjWorkload:
+    cfg = OPROJ_CONFIGS[name]
+    return build_oproj(cfg.batch, cfg.in_features, cfg.hidden, cfg.seed if seed is None else seed, name=name)
