@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--workload", default="long70b",
                     choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16",
                              "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
-                             "prelude_falcon3"])
+                             "prelude_falcon3", "oproj_qwen3_4b", "oproj_llama8b", "oproj_70b"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the oracle cpu_baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -134,6 +134,9 @@ def main():
         return
     if args.workload.startswith("prelude_"):
         prelude_main(args)
+        return
+    if args.workload.startswith("oproj_"):
+        oproj_main(args)
         return
 
     import torch
@@ -430,6 +433,118 @@ def prelude_main(args):
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = prelude_cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(res), flush=True)
+
+
+def oproj_main(args):
+    """The output projection + residual add + RMSNorm of one decode step, on
+    cold weights (the calls cycle over >= 2 GB of weight copies)."""
+    import torch
+    import workloads as W
+    from paper_2606_07665_amd import binding as pda
+
+    pda.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = W.make_oproj(args.workload)
+    dev = torch.device("cuda:0")
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    attn, res, nw = bf(w.attn), bf(w.residual), bf(w.norm_w)
+    wp0 = pda.pack_weights(bf(w.w_o))
+    wbytes = 2 * w.hidden * w.in_features
+    layers = max(1, -(-2_000_000_000 // wbytes))
+    wps = [wp0] + [wp0.clone() for _ in range(layers - 1)]
+    z = torch.empty_like(res)
+    h = torch.empty_like(res)
+    stream = torch.cuda.current_stream()
+    it = [0]
+
+    def call(i=None):
+        j = it[0] if i is None else i
+        pda.o_proj_residual_norm(attn, wps[j % layers], res, nw, z, h, eps=float(w.eps))
+        it[0] += 1
+
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    pda.profile_enable(True)
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    gemv_ms, epi_ms, n = pda.profile_read_o_proj()
+    pda.profile_enable(False)
+    gemv_ms /= max(n, 1)
+    epi_ms /= max(n, 1)
+    graph_us = None
+    if not args.no_graph:
+        s = torch.cuda.Stream()
+        pda.o_proj_workspace_reserve(w.batch, w.in_features, w.hidden, stream=s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for i in range(20):
+                call(i)
+        g.replay()
+        torch.cuda.synchronize()
+        reps = max(1, args.steps // 20)
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for _ in range(reps):
+            g.replay()
+        g1.record()
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) / (reps * 20) * 1e3
+    nbytes = w.algorithmic_bytes()
+    gemv_bytes = wbytes + 2 * w.batch * w.in_features
+    achieved = gemv_bytes / (gemv_ms * 1e-3) / 1e9
+    res_line = {
+        "metric": "o_proj GEMV + residual + RMSNorm µs/call + achieved HBM GB/s (% of MI355X peak), 1 GPU",
+        "value": round(nbytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "us_per_call": round(ms_per_step * 1e3, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "batch": w.batch, "in_features": w.in_features, "hidden": w.hidden,
+                   "weight_copies": layers, "algorithmic_bytes": nbytes, "parallelism": "single GPU",
+                   "device": torch.cuda.get_device_name(0)},
+        "kernels_ms": {"gemv": round(gemv_ms, 5), "epilogue": round(epi_ms, 5)},
+        "graph_us_per_call": None if graph_us is None else round(graph_us, 2),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "kernel": "gemv_kernel (packed-weight MFMA GEMV of the output projection)"},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0, calls = time.perf_counter(), 0
+            while True:
+                oracle.o_proj_residual_norm(w.attn, w.w_o, w.residual, w.norm_w, w.eps)
+                calls += 1
+                if time.perf_counter() - t0 >= args.cpu_seconds:
+                    break
+            dt = time.perf_counter() - t0
+        res_line["cpu_baseline"] = {"value": round(nbytes * calls / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+                                    "kind": "oracle",
+                                    "sample": f"{calls} whole calls of the same workload, {dt:.1f} s fp64 numpy"}
+    print(json.dumps(res_line), flush=True)
 
 
 def prelude_cpu_baseline(w, budget_s):

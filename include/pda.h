@@ -232,8 +232,9 @@ int32_t pda_get_option(int32_t option);
  */
 int pda_profile_enable(int32_t on);
 int pda_profile_read(double* split_ms, double* merge_ms, int64_t* calls);
-/* The same for the prelude calls: summed GEMV and epilogue milliseconds. */
+/* The same for the prelude and o_proj calls: summed GEMV and epilogue ms. */
 int pda_profile_read_prelude(double* gemv_ms, double* epilogue_ms, int64_t* calls);
+int pda_profile_read_o_proj(double* gemv_ms, double* epilogue_ms, int64_t* calls);
 
 /*
  * ---------------------------------------------------------------------------
@@ -255,7 +256,7 @@ int pda_profile_read_prelude(double* gemv_ms, double* epilogue_ms, int64_t* call
  */
 typedef struct {
   int32_t batch;         /* sequences, 0 .. 64                                  */
-  int32_t hidden;        /* H: a positive multiple of 256, at most 65536        */
+  int32_t hidden;        /* H: a positive multiple of 32, at most 65536         */
   int32_t num_q_heads;   /* Hq, a multiple of num_kv_heads                      */
   int32_t num_kv_heads;  /* Hkv                                                 */
   int32_t head_dim;      /* D: 64, 128 or 256                                   */
@@ -310,6 +311,33 @@ int pda_attention_prelude_append(const void* x, const void* w_packed, const void
 
 /* Grow the (current device, stream) workspace for a prelude of these dims. */
 int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * pda_o_proj_residual_norm -- the step after attention, the paper's kernel
+ * family (v) (Method, "Principle-Driven LLM Kernel Generator": the output
+ * projection fused with the residual add and the RMSNorm that follows):
+ *
+ *   z = W_o a + residual          (the new residual stream)
+ *   h = z / sqrt(mean(z^2) + eps) * norm_w   (over the hidden features)
+ *
+ *   attn          bf16 [batch, in_features] (the heads' outputs concatenated),
+ *                 16-byte aligned.
+ *   w_packed      W_o bf16 [hidden, in_features], packed by pda_pack_weights.
+ *   residual      bf16 [batch, hidden]; norm_w bf16 [hidden].
+ *   residual_out  bf16 [batch, hidden]: z rounded once (may be residual itself,
+ *                 updated in place); normed_out bf16 [batch, hidden]: h, from
+ *                 the unrounded z; must not be residual_out.
+ *   batch 0..64; in_features a multiple of 32 up to 65536; hidden a multiple
+ *   of 16 up to 32768; eps finite and >= 0.
+ * Uses the (device, stream) workspace (pda_o_proj_workspace_reserve before
+ * graph capture).  Asynchronous.  Errors as for pda_attention_prelude.
+ * ---------------------------------------------------------------------------
+ */
+int pda_o_proj_residual_norm(const void* attn, const void* w_packed, const void* residual, const void* norm_w,
+                             void* residual_out, void* normed_out, int32_t batch, int32_t in_features,
+                             int32_t hidden, float eps, void* stream);
+int pda_o_proj_workspace_reserve(int32_t batch, int32_t in_features, int32_t hidden, void* stream);
 
 #ifdef __cplusplus
 }

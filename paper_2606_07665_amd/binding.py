@@ -52,6 +52,10 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.pda_attention_prelude_append.restype = ctypes.c_int
     lib.pda_prelude_workspace_reserve.argtypes = [dims_p, vp]
     lib.pda_prelude_workspace_reserve.restype = ctypes.c_int
+    lib.pda_o_proj_residual_norm.argtypes = [vp] * 6 + [i32, i32, i32, f32, vp]
+    lib.pda_o_proj_residual_norm.restype = ctypes.c_int
+    lib.pda_o_proj_workspace_reserve.argtypes = [i32, i32, i32, vp]
+    lib.pda_o_proj_workspace_reserve.restype = ctypes.c_int
     lib.pda_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
     lib.pda_kv_append.restype = ctypes.c_int
     lib.paged_decode_attention_append.argtypes = [vp] * 8 + [i32] * 7 + [f32, vp]
@@ -78,6 +82,8 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.pda_profile_read.restype = ctypes.c_int
     lib.pda_profile_read_prelude.argtypes = lib.pda_profile_read.argtypes
     lib.pda_profile_read_prelude.restype = ctypes.c_int
+    lib.pda_profile_read_o_proj.argtypes = lib.pda_profile_read.argtypes
+    lib.pda_profile_read_o_proj.restype = ctypes.c_int
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -337,4 +343,32 @@ def profile_read_prelude() -> Tuple[float, float, int]:
     """(GEMV kernel ms, epilogue kernel ms, prelude calls) summed since the last read."""
     s, m, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
     _check(load().pda_profile_read_prelude(ctypes.byref(s), ctypes.byref(m), ctypes.byref(n)))
+    return s.value, m.value, n.value
+
+
+
+def o_proj_residual_norm(attn, w_packed, residual, norm_w, residual_out, normed_out, eps=1e-5, stream=None):
+    """z = W_o attn + residual -> residual_out (bf16); RMSNorm(z) * norm_w ->
+    normed_out.  attn [B, K], w_packed [H, K] from :func:`pack_weights`,
+    residual / outputs [B, H], norm_w [H]; residual_out may be residual."""
+    _check_bf16(attn=attn, w_packed=w_packed, residual=residual, norm_w=norm_w, residual_out=residual_out,
+                normed_out=normed_out)
+    b, k = attn.shape
+    h = w_packed.shape[0]
+    if w_packed.shape[1] != k or residual.shape != (b, h) or residual_out.shape != (b, h) or \
+            normed_out.shape != (b, h) or norm_w.shape != (h,):
+        raise ValueError("inconsistent o_proj shapes")
+    _check(load().pda_o_proj_residual_norm(attn.data_ptr(), w_packed.data_ptr(), residual.data_ptr(),
+                                           norm_w.data_ptr(), residual_out.data_ptr(), normed_out.data_ptr(), b, k,
+                                           h, ctypes.c_float(float(eps)), _stream_ptr(stream)))
+
+
+def o_proj_workspace_reserve(batch, in_features, hidden, stream=None) -> None:
+    _check(load().pda_o_proj_workspace_reserve(batch, in_features, hidden, _stream_ptr(stream)))
+
+
+def profile_read_o_proj() -> Tuple[float, float, int]:
+    """(GEMV kernel ms, epilogue kernel ms, o_proj calls) summed since the last read."""
+    s, m, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+    _check(load().pda_profile_read_o_proj(ctypes.byref(s), ctypes.byref(m), ctypes.byref(n)))
     return s.value, m.value, n.value

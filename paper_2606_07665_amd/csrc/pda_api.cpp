@@ -204,7 +204,7 @@ int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
 
 // ---------------------------------------------------------------- profiling
 // Events around the two kernels of a call: kind 0 is attention (split,
-// merge), kind 1 the prelude (GEMV, epilogue).
+// merge), kind 1 the prelude (GEMV, epilogue), kind 2 o_proj (GEMV, epilogue).
 struct Rec {
   hipEvent_t a, b, c;
   int kind;
@@ -281,8 +281,8 @@ int check_prelude(const pda_prelude_dims* dm) {
     return fail(PDA_ERR_UNSUPPORTED, "prelude batch %d exceeds %d", d.batch, pda::kMaxGemvBatch);
   if (d.hidden <= 0 || d.num_q_heads <= 0 || d.num_kv_heads <= 0)
     return fail(PDA_ERR_SHAPE, "hidden and head counts must be positive");
-  if (d.hidden % (pda::kGemvWaves * pda::kTileK) || d.hidden > 65536)
-    return fail(PDA_ERR_UNSUPPORTED, "hidden %d (supported: multiples of 256 up to 65536)", d.hidden);
+  if (d.hidden % pda::kTileK || d.hidden > 65536)
+    return fail(PDA_ERR_UNSUPPORTED, "hidden %d (supported: multiples of 32 up to 65536)", d.hidden);
   if (d.num_q_heads % d.num_kv_heads)
     return fail(PDA_ERR_SHAPE, "num_q_heads %d is not a multiple of num_kv_heads %d", d.num_q_heads,
                 d.num_kv_heads);
@@ -310,6 +310,16 @@ pda::GemvPlan prelude_plan(const pda_prelude_dims& d, int cus) {
 
 int64_t prelude_ws_bytes(const pda_prelude_dims& d, int cus) {
   return align256(pda::gemv_partial_floats(prelude_plan(d, cus), d.batch, static_cast<int>(prelude_rows(d))) * 4);
+}
+
+// o_proj workspace: GEMV partials, then z [batch, hidden] and the chunk sums.
+int64_t oproj_z_offset(const pda::GemvPlan& plan, int batch, int hidden) {
+  return align256(pda::gemv_partial_floats(plan, batch, hidden) * 4);
+}
+
+int64_t oproj_ws_bytes(const pda::GemvPlan& plan, int batch, int hidden) {
+  return oproj_z_offset(plan, batch, hidden) +
+         align256((static_cast<int64_t>(batch) * hidden + static_cast<int64_t>(batch) * pda::oproj_chunks(hidden)) * 4);
 }
 
 // Shared by both prelude entry points once their own arguments are checked.
@@ -671,6 +681,93 @@ int pda_attention_prelude_append(const void* x, const void* w_packed, const void
   ep.num_pages = num_pages;
   ep.maxp = max_pages_per_seq;
   return run_prelude(x, w_packed, bias, q_norm, k_norm, context_lens, q_out, ep, *dims, stream);
+}
+
+int pda_o_proj_residual_norm(const void* attn, const void* w_packed, const void* residual, const void* norm_w,
+                             void* residual_out, void* normed_out, int32_t batch, int32_t in_features,
+                             int32_t hidden, float eps, void* stream) {
+  g_err.clear();
+  if (batch < 0) return fail(PDA_ERR_SHAPE, "batch must be >= 0 (got %d)", batch);
+  if (batch > pda::kMaxGemvBatch) return fail(PDA_ERR_UNSUPPORTED, "batch %d exceeds %d", batch, pda::kMaxGemvBatch);
+  if (in_features <= 0 || hidden <= 0) return fail(PDA_ERR_SHAPE, "in_features and hidden must be positive");
+  if (in_features % pda::kTileK || in_features > 65536)
+    return fail(PDA_ERR_UNSUPPORTED, "in_features %d (supported: multiples of 32 up to 65536)", in_features);
+  if (hidden % pda::kTileRows || hidden > pda::kMaxOProjHidden)
+    return fail(PDA_ERR_UNSUPPORTED, "hidden %d (supported: multiples of 16 up to %d)", hidden,
+                pda::kMaxOProjHidden);
+  if (!std::isfinite(eps) || eps < 0.f) return fail(PDA_ERR_SCALE, "eps must be finite and >= 0");
+  if (batch == 0) return PDA_OK;
+  if (!attn || !w_packed || !residual || !norm_w || !residual_out || !normed_out)
+    return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if (misaligned(attn, 16) || misaligned(w_packed, 16))
+    return fail(PDA_ERR_ALIGN, "attn and w_packed must be 16-byte aligned");
+  if (misaligned(residual, 2) || misaligned(norm_w, 2) || misaligned(residual_out, 2) || misaligned(normed_out, 2))
+    return fail(PDA_ERR_ALIGN, "bf16 arrays must be 2-byte aligned");
+  if (normed_out == residual_out) return fail(PDA_ERR_SHAPE, "normed_out must not be residual_out");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  int rc = device_cus(dev, &cus);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const pda::GemvPlan plan = pda::plan_gemv(batch, hidden, in_features, cus);
+  void* ws = nullptr;
+  if ((rc = workspace_for(dev, st, oproj_ws_bytes(plan, batch, hidden), &ws))) return rc;
+  pda::GemvArgs g;
+  g.x = static_cast<const uint16_t*>(attn);
+  g.wp = static_cast<const uint16_t*>(w_packed);
+  g.part = static_cast<float*>(ws);
+  g.batch = batch;
+  g.n = hidden;
+  g.k = in_features;
+  g.plan = plan;
+  const Rec rec = prof_begin(2);
+  const bool prof = rec.a != nullptr;
+  if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = pda::launch_gemv(g, st)) != hipSuccess) return hip_fail(e, "GEMV kernel launch");
+  if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  pda::OProjArgs o;
+  o.part = g.part;
+  o.plan = plan;
+  o.residual = static_cast<const uint16_t*>(residual);
+  o.norm_w = static_cast<const uint16_t*>(norm_w);
+  o.residual_out = static_cast<uint16_t*>(residual_out);
+  o.normed_out = static_cast<uint16_t*>(normed_out);
+  o.z = reinterpret_cast<float*>(static_cast<char*>(ws) + oproj_z_offset(plan, batch, hidden));
+  o.chunk_ss = o.z + static_cast<int64_t>(batch) * hidden;
+  o.batch = batch;
+  o.hidden = hidden;
+  o.eps = eps;
+  if ((e = pda::launch_oproj_epilogue(o, st)) != hipSuccess) return hip_fail(e, "o_proj epilogue launch");
+  if (prof) {
+    if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    prof_push(rec);
+  }
+  return PDA_OK;
+}
+
+int pda_o_proj_workspace_reserve(int32_t batch, int32_t in_features, int32_t hidden, void* stream) {
+  g_err.clear();
+  if (batch < 0 || batch > pda::kMaxGemvBatch || in_features <= 0 || in_features % pda::kTileK ||
+      hidden <= 0 || hidden % pda::kTileRows || hidden > pda::kMaxOProjHidden)
+    return fail(PDA_ERR_SHAPE, "o_proj shape out of range");
+  if (batch == 0) return PDA_OK;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  int rc = device_cus(dev, &cus);
+  if (rc) return rc;
+  const pda::GemvPlan plan = pda::plan_gemv(batch, hidden, in_features, cus);
+  void* ptr = nullptr;
+  return workspace_for(dev, static_cast<hipStream_t>(stream), oproj_ws_bytes(plan, batch, hidden), &ptr);
+}
+
+int pda_profile_read_o_proj(double* gemv_ms, double* epilogue_ms, int64_t* calls) {
+  g_err.clear();
+  if (!gemv_ms || !epilogue_ms || !calls) return fail(PDA_ERR_NULL, "pda_profile_read_o_proj: NULL output pointer");
+  return prof_read(2, gemv_ms, epilogue_ms, calls);
 }
 
 int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream) {

@@ -54,7 +54,29 @@ struct PreludeArgs {
   float theta, eps;
 };
 
+// o_proj epilogue, two passes over (sequence, chunk of kOProjChunk features):
+// z = y + residual and the chunk's sum of z^2, then h = RMSNorm(z) * w once
+// every chunk's sum is known.
+constexpr int kOProjChunk = 256;                // features per workgroup (one per thread)
+constexpr int kMaxOProjHidden = 32768;
+
+struct OProjArgs {
+  const float* part;          // GEMV partials of y [batch, hidden]
+  GemvPlan plan;
+  const uint16_t* residual;   // bf16 [batch, hidden]
+  const uint16_t* norm_w;     // bf16 [hidden]
+  uint16_t* residual_out;     // bf16 [batch, hidden] (may be residual itself)
+  uint16_t* normed_out;       // bf16 [batch, hidden]
+  float* z;                   // fp32 [batch, hidden] scratch
+  float* chunk_ss;            // fp32 [batch, chunks] scratch
+  int batch, hidden;
+  float eps;
+};
+
+__host__ __device__ inline int oproj_chunks(int hidden) { return (hidden + kOProjChunk - 1) / kOProjChunk; }
+
 hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_t st);
+hipError_t launch_oproj_epilogue(const OProjArgs& a, hipStream_t st);
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st);
 hipError_t launch_prelude_epilogue(const PreludeArgs& a, hipStream_t st);
 

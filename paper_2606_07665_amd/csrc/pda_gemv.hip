@@ -1,4 +1,5 @@
-// Decode GEMV and the attention prelude for MI355X (gfx950, CDNA4, wave64).
+// Decode GEMV, the attention prelude and the output projection for MI355X
+// (gfx950, CDNA4, wave64).
 //
 // What is computed: the paper's kernel family (i), the attention prelude
 // (Method, "Principle-Driven LLM Kernel Generator"): the QKV projection of
@@ -25,6 +26,11 @@
 //    optionally the KV append into the page slot) runs per (sequence, head):
 //    a head's norm and its rotation pairs need all of its rows, which no
 //    single wave of the GEMV holds.
+//
+// The output projection after attention (kernel family (v): o_proj GEMV +
+// residual add + the RMSNorm that follows) runs on the same GEMV; its
+// epilogue works in two passes over (sequence, chunk of features), since the
+// norm spans all hidden features of a sequence.
 #include "pda_gemv.h"
 
 namespace pda {
@@ -263,7 +269,62 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
   }
 }
 
+// Pass 1, one workgroup per (sequence b, chunk c of features), one feature
+// per thread: z = y + residual (fp32 to scratch, bf16 to residual_out) and
+// the chunk's sum of z^2 (fixed reduction order).  residual_out may be the
+// residual buffer: each feature is read and written by the same thread.
+__global__ __launch_bounds__(kOProjChunk) void oproj_residual_kernel(OProjArgs a) {
+  __shared__ float wsum[kOProjChunk / 64];
+  const int chunks = oproj_chunks(a.hidden);
+  const int b = blockIdx.x / chunks;
+  const int c = blockIdx.x - b * chunks;
+  const int n = c * kOProjChunk + threadIdx.x;
+  const int64_t at = static_cast<int64_t>(b) * a.hidden + n;
+  float z = 0.f;
+  if (n < a.hidden) {
+    z = gemv_result(a.part, a.plan, a.batch, b, n) + bf16_to_f32(a.residual[at]);
+    a.z[at] = z;
+    a.residual_out[at] = f32_to_bf16(z);
+  }
+  float ss = z * z;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < kOProjChunk / 64; ++i) t += wsum[i];
+    a.chunk_ss[static_cast<int64_t>(b) * chunks + c] = t;
+  }
+}
+
+// Pass 2, same grid: the sequence's total (chunk sums in chunk order) and
+// h = z / sqrt(mean + eps) * w.
+__global__ __launch_bounds__(kOProjChunk) void oproj_norm_kernel(OProjArgs a) {
+  const int chunks = oproj_chunks(a.hidden);
+  const int b = blockIdx.x / chunks;
+  const int c = blockIdx.x - b * chunks;
+  const int n = c * kOProjChunk + threadIdx.x;
+  if (n >= a.hidden) return;
+  const float* ss = a.chunk_ss + static_cast<int64_t>(b) * chunks;
+  float tot = 0.f;
+  for (int i = 0; i < chunks; ++i) tot += ss[i];
+  const float inv = rsqrtf(tot / a.hidden + a.eps);
+  const int64_t at = static_cast<int64_t>(b) * a.hidden + n;
+  a.normed_out[at] = f32_to_bf16(a.z[at] * inv * bf16_to_f32(a.norm_w[n]));
+}
+
 }  // namespace
+
+hipError_t launch_oproj_epilogue(const OProjArgs& a, hipStream_t st) {
+  const dim3 grid(a.batch * oproj_chunks(a.hidden));
+  hipLaunchKernelGGL(oproj_residual_kernel, grid, dim3(kOProjChunk), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(oproj_norm_kernel, grid, dim3(kOProjChunk), 0, st, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_t st) {
   const int64_t chunks = static_cast<int64_t>(n) * k / 8;

@@ -243,3 +243,32 @@ def test_pack_argument_errors(lib, rows, cols, code):
 def test_pack_rejects_overlap_and_null(lib):
     assert B.load().pda_pack_weights(4096, 4096 + 512, 16, 64, None) == SHAPE
     assert B.load().pda_pack_weights(0, 4096, 16, 64, None) == NULL
+
+
+# ------------------------------------------------------------------ o_proj
+def oproj_call(ptrs=None, batch=2, k=256, h=512, eps=1e-5):
+    p = ptrs or [16] * 6
+    return B.load().pda_o_proj_residual_norm(*p, batch, k, h, ctypes.c_float(eps), None)
+
+
+@pytest.mark.parametrize("kwargs,code,text", [
+    (dict(batch=-1), SHAPE, "batch"),
+    (dict(batch=65), UNSUPPORTED, "batch"),
+    (dict(k=0), SHAPE, "positive"),
+    (dict(k=100), UNSUPPORTED, "in_features"),
+    (dict(h=24), UNSUPPORTED, "hidden"),
+    (dict(h=32768 + 16), UNSUPPORTED, "hidden"),
+    (dict(eps=float("nan")), SCALE, "eps"),
+    (dict(ptrs=[16, 16, 0, 16, 16, 32]), NULL, "NULL"),
+    (dict(ptrs=[24, 16, 16, 16, 16, 32]), ALIGN, "16-byte"),
+    (dict(ptrs=[16, 16, 16, 16, 17, 32]), ALIGN, "2-byte"),
+    (dict(ptrs=[16, 16, 16, 16, 32, 32]), SHAPE, "normed_out"),
+])
+def test_oproj_argument_errors(lib, kwargs, code, text):
+    rc = oproj_call(**kwargs)
+    assert rc == code, B.last_error()
+    assert text in B.last_error()
+
+
+def test_oproj_empty_batch_is_a_noop(lib):
+    assert oproj_call(ptrs=[0] * 6, batch=0) == OK
