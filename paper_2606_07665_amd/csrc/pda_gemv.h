@@ -16,11 +16,14 @@ constexpr int kMaxGemvBatch = 64;               // sequences: four 16-column til
 constexpr int kPackThreads = 256;
 
 // y[b, n] = sum_k x[b, k] W[n, k] over a packed W (see launch_pack), as
-// fp32 partials: part[t][j][b][16] holds the contribution of the j-th wave
-// that touched 16-row tile t.  GemvPlan says how the waves split the work.
+// fp32 partials: a work unit is one 32-k tile of a group of `group`
+// consecutive 16-row tiles; part[g][j][i][b][16] holds the contribution of
+// the j-th wave that touched row group g, for its tile i.  GemvPlan says how
+// the waves split the work.
 struct GemvPlan {
   int grid;     // workgroups of kGemvWaves waves
-  int slots;    // partial slots per row tile (an upper bound)
+  int slots;    // partial slots per row group (an upper bound)
+  int group;    // 16-row tiles per work unit (x fragments are reused across them)
   int64_t waves, units;
   int kt_count;
 };

@@ -72,13 +72,16 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
   *reinterpret_cast<u32x4*>(wp + chunk * 8) = *reinterpret_cast<const u32x4*>(w + row * k + col);
 }
 
-// Stream-K GEMV: the flattened space of (16-row tile t, 32-k tile) units is
+// Stream-K GEMV: the flattened space of (row group g, 32-k tile) units is
 // cut into equal contiguous ranges, one per wave, so every wave streams the
-// same number of packed weight tiles whatever the matrix shape.  A wave
-// writes one partial (16 rows x batch, fp32) per row tile its range touches,
-// into slot j = wave - first_wave(t) of that tile; the epilogue sums a tile's
-// slots in order (deterministic).
-template <int kNBT>
+// same number of packed weight tiles whatever the matrix shape.  A row group
+// is kR consecutive 16-row tiles: each x fragment a wave loads feeds kR
+// MFMAs, which keeps x reads (L2) at or below the weight reads (HBM) when the
+// batch spans several 16-column tiles.  A wave writes one partial (kR tiles
+// x batch, fp32) per row group its range touches, into slot
+// j = wave - first_wave(g) of that group; the epilogue sums a group's slots
+// in order (deterministic).
+template <int kNBT, int kR>
 __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __restrict__ x,
                                                             const uint16_t* __restrict__ wp,
                                                             float* __restrict__ part, int batch, int n, int k,
@@ -87,7 +90,7 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __re
   const int64_t waves = static_cast<int64_t>(gridDim.x) * (kGemvThreads / 64);
   const int64_t w = static_cast<int64_t>(blockIdx.x) * (kGemvThreads / 64) + uniform(threadIdx.x >> 6);
   const int kt_count = k / kTileK;
-  const int64_t units = static_cast<int64_t>(n / kTileRows) * kt_count;
+  const int64_t units = static_cast<int64_t>(n / (kTileRows * kR)) * kt_count;
   int64_t u = w * units / waves;
   const int64_t u_end = (w + 1) * units / waves;
   if (u >= u_end) return;
@@ -99,27 +102,37 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __re
   int xrow[kNBT];
 #pragma unroll
   for (int bt = 0; bt < kNBT; ++bt) xrow[bt] = ((16 * bt + r) * k + 8 * g4) * 2;
+  const uint32_t tile_stride = static_cast<uint32_t>(kt_count) * 1024u;  // bytes between row tiles
 
   while (u < u_end) {
-    const int t = static_cast<int>(u / kt_count);
-    const int kt0 = static_cast<int>(u - static_cast<int64_t>(t) * kt_count);
-    const int64_t seg_end = u_end < static_cast<int64_t>(t + 1) * kt_count ? u_end
-                                                                           : static_cast<int64_t>(t + 1) * kt_count;
+    const int g = static_cast<int>(u / kt_count);
+    const int kt0 = static_cast<int>(u - static_cast<int64_t>(g) * kt_count);
+    const int64_t seg_end = u_end < static_cast<int64_t>(g + 1) * kt_count ? u_end
+                                                                           : static_cast<int64_t>(g + 1) * kt_count;
     const int per = static_cast<int>(seg_end - u);
-    const uint16_t* wbase = wp + (static_cast<int64_t>(t) * kt_count + kt0) * (kTileRows * kTileK);
-    // tiles past the segment read as zeros (outside the weight descriptor)
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(wbase, static_cast<uint32_t>(per) * 1024u);
-
-    f32x4 acc[kNBT];
+    // the group's tiles at k tile kt0 onwards; tile i of the group is tile_stride further on
+    const uint16_t* wbase = wp + (static_cast<int64_t>(g) * kR * kt_count + kt0) * (kTileRows * kTileK);
+    __amdgpu_buffer_rsrc_t rw[kR];
 #pragma unroll
-    for (int bt = 0; bt < kNBT; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    constexpr int kChunk = kNBT == 1 ? 8 : 4;  // k tiles whose loads are in flight together
+    for (int i = 0; i < kR; ++i)  // k tiles past the segment read as zeros (outside the descriptor)
+      rw[i] = make_rsrc(wbase + static_cast<int64_t>(i) * kt_count * (kTileRows * kTileK),
+                        static_cast<uint32_t>(per) * 1024u);
+    (void)tile_stride;
+
+    f32x4 acc[kR][kNBT];
+#pragma unroll
+    for (int i = 0; i < kR; ++i)
+#pragma unroll
+      for (int bt = 0; bt < kNBT; ++bt) acc[i][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    constexpr int kChunk = kNBT * kR >= 4 ? 2 : (kNBT == 1 ? 8 : 4);  // k tiles in flight together
     for (int j0 = 0; j0 < per; j0 += kChunk) {
-      u32x4 wa[kChunk];
+      u32x4 wa[kChunk][kR];
       u32x4 xb[kChunk][kNBT];
 #pragma unroll
       for (int j = 0; j < kChunk; ++j) {
-        wa[j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
+#pragma unroll
+        for (int i = 0; i < kR; ++i)
+          wa[j][i] = __builtin_amdgcn_raw_buffer_load_b128(rw[i], (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
         const bool in = j0 + j < per;
 #pragma unroll
         for (int bt = 0; bt < kNBT; ++bt)
@@ -129,35 +142,43 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __re
 #pragma unroll
       for (int j = 0; j < kChunk; ++j)
 #pragma unroll
-        for (int bt = 0; bt < kNBT; ++bt)
-          acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[j]),
-                                                            __builtin_bit_cast(bf16x8, xb[j][bt]), acc[bt], 0,
-                                                            0, 0);
+        for (int i = 0; i < kR; ++i)
+#pragma unroll
+          for (int bt = 0; bt < kNBT; ++bt)
+            acc[i][bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[j][i]),
+                                                                 __builtin_bit_cast(bf16x8, xb[j][bt]), acc[i][bt],
+                                                                 0, 0, 0);
     }
     // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
-    const int64_t first = (static_cast<int64_t>(t) * kt_count * waves + waves - 1) / units;  // first wave of t
-    float* slot = part + ((static_cast<int64_t>(t) * slots + (w - first)) * batch) * kTileRows;
+    const int64_t first = (static_cast<int64_t>(g) * kt_count * waves + waves - 1) / units;  // first wave of g
+    float* slot = part + (static_cast<int64_t>(g) * slots + (w - first)) * kR * batch * kTileRows;
 #pragma unroll
-    for (int bt = 0; bt < kNBT; ++bt) {
-      const int b = 16 * bt + r;
-      if (b < batch) *reinterpret_cast<f32x4*>(slot + b * kTileRows + 4 * g4) = acc[bt];
-    }
+    for (int i = 0; i < kR; ++i)
+#pragma unroll
+      for (int bt = 0; bt < kNBT; ++bt) {
+        const int b = 16 * bt + r;
+        if (b < batch) *reinterpret_cast<f32x4*>(slot + (i * batch + b) * kTileRows + 4 * g4) = acc[i][bt];
+      }
     u = seg_end;
   }
 }
 
-// y[b][row]: the sum, in wave order, of the partials of row's tile.
+// y[b][row]: the sum, in wave order, of the partials of row's group.
 __device__ __forceinline__ float gemv_result(const float* __restrict__ part, const GemvPlan& p, int batch, int b,
                                              int row) {
   const int t = row >> 4;
-  const int64_t x0 = static_cast<int64_t>(t) * p.kt_count;
+  const int g = t / p.group;
+  const int i = t - g * p.group;
+  const int64_t x0 = static_cast<int64_t>(g) * p.kt_count;
   const int64_t first = ((x0 + 1) * p.waves - 1) / p.units;
   const int64_t last = ((x0 + p.kt_count) * p.waves - 1) / p.units;
   const int cnt = static_cast<int>(last - first + 1);  // at most kGemvMaxSlots (plan_gemv)
-  const float* q = part + (static_cast<int64_t>(t) * p.slots * batch + b) * kTileRows + (row & 15);
+  const int64_t slot_floats = static_cast<int64_t>(p.group) * batch * kTileRows;
+  const float* q = part + static_cast<int64_t>(g) * p.slots * slot_floats + (static_cast<int64_t>(i) * batch + b) * kTileRows +
+                   (row & 15);
   float v[kGemvMaxSlots];
 #pragma unroll
-  for (int j = 0; j < kGemvMaxSlots; ++j) v[j] = j < cnt ? q[static_cast<int64_t>(j) * batch * kTileRows] : 0.f;
+  for (int j = 0; j < kGemvMaxSlots; ++j) v[j] = j < cnt ? q[j * slot_floats] : 0.f;
   float s = 0.f;
 #pragma unroll
   for (int j = 0; j < kGemvMaxSlots; ++j) s += v[j];
@@ -334,16 +355,18 @@ hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_
 }
 
 GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
-  (void)batch;
   GemvPlan p;
+  const int nbt = (batch + 15) / 16;
+  const int tiles = n / kTileRows;
+  p.group = (nbt > 1 && tiles % nbt == 0) ? nbt : 1;
   p.kt_count = k / kTileK;
-  p.units = static_cast<int64_t>(n / kTileRows) * p.kt_count;
+  p.units = static_cast<int64_t>(tiles / p.group) * p.kt_count;
   int64_t grid = static_cast<int64_t>(num_cus) * kGemvBlocksPerCu;
   const int64_t most = (p.units + static_cast<int64_t>(kGemvWaves) * kGemvMinTiles - 1) /
                        (static_cast<int64_t>(kGemvWaves) * kGemvMinTiles);
   if (grid > most) grid = most;
-  // at most kGemvMaxSlots waves per row tile: waves <= (kGemvMaxSlots - 1) * tiles
-  const int64_t cap = static_cast<int64_t>(kGemvMaxSlots - 1) * (n / kTileRows) / kGemvWaves;
+  // at most kGemvMaxSlots waves per row group: waves <= (kGemvMaxSlots - 1) * groups
+  const int64_t cap = static_cast<int64_t>(kGemvMaxSlots - 1) * (tiles / p.group) / kGemvWaves;
   if (grid > cap) grid = cap;
   if (grid < 1) grid = 1;
   p.grid = static_cast<int>(grid);
@@ -354,19 +377,23 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
 }
 
 int64_t gemv_partial_floats(const GemvPlan& p, int batch, int n) {
-  return static_cast<int64_t>(n / kTileRows) * p.slots * batch * kTileRows;
+  return static_cast<int64_t>(n / kTileRows) * p.slots * batch * kTileRows;  // groups * group tiles = n / 16
 }
 
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
   const dim3 grid(a.plan.grid);
   const int nbt = (a.batch + 15) / 16;
   const int sl = a.plan.slots;
+  const bool grouped = a.plan.group > 1;
+#define PDA_GEMV(NBT, R) \
+  hipLaunchKernelGGL((gemv_kernel<NBT, R>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl)
   switch (nbt) {
-    case 1: hipLaunchKernelGGL((gemv_kernel<1>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<2>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
-    case 3: hipLaunchKernelGGL((gemv_kernel<3>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
-    default: hipLaunchKernelGGL((gemv_kernel<4>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl); break;
+    case 1: PDA_GEMV(1, 1); break;
+    case 2: if (grouped) PDA_GEMV(2, 2); else PDA_GEMV(2, 1); break;
+    case 3: if (grouped) PDA_GEMV(3, 3); else PDA_GEMV(3, 1); break;
+    default: if (grouped) PDA_GEMV(4, 4); else PDA_GEMV(4, 1); break;
   }
+#undef PDA_GEMV
   return hipGetLastError();
 }
 
