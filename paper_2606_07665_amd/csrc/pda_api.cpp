@@ -368,7 +368,7 @@ int run_prelude(const void* x, const void* w_packed, const void* bias, const voi
   ep.d = d.head_dim;
   ep.rotary_dim = d.rotary_dim;
   ep.interleaved = d.interleaved;
-  ep.theta = d.rope_theta;
+  ep.log2_theta = std::log2(static_cast<double>(d.rope_theta));
   ep.eps = d.eps;
   if ((e = pda::launch_prelude_epilogue(ep, st)) != hipSuccess) return hip_fail(e, "prelude epilogue launch");
   if (prof) {

@@ -54,7 +54,8 @@ struct PreludeArgs {
   const int32_t* bt;         // [batch, maxp]
   int page_shift, num_pages, maxp;
   int batch, hq, hkv, d, rotary_dim, interleaved;
-  float theta, eps;
+  double log2_theta;  // log2 of the rotary base, computed in fp64 on the host
+  float eps;
 };
 
 // o_proj epilogue, two passes over (sequence, chunk of kOProjChunk features):

@@ -231,7 +231,7 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
     for (int j = 0; j < E; ++j) s[lane + 64 * j] = v[j];
     __syncthreads();
     const int r = a.rotary_dim;
-    const double log2_theta = log2(static_cast<double>(a.theta));
+    constexpr double kInvTwoPi = 0.15915494309189535;
 #pragma unroll
     for (int j = 0; j < E; ++j) {
       const int e = lane + 64 * j;
@@ -247,12 +247,14 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
         i = first ? e : e - r / 2;
         partner = first ? e + r / 2 : e - r / 2;
       }
-      // the angle p * theta^(-2i/r) in fp64: positions reach 10^5 and more,
-      // where an fp32 angle would already be off by ~10^-2 rad
-      const double ang = static_cast<double>(pos) * exp2(-(2.0 * i / r) * log2_theta);
-      double sd, cd;
-      sincos(ang, &sd, &cd);
-      const float c = static_cast<float>(cd), sn = static_cast<float>(sd);
+      // the angle p * theta^(-2i/r), in turns, in fp64 (positions reach 10^5
+      // and more, where an fp32 angle would already be off by ~10^-2 rad);
+      // its fraction in [-1/2, 1/2] goes to the hardware sine and cosine,
+      // which take turns
+      const double turns = static_cast<double>(pos) * exp2(-(2.0 * i / r) * a.log2_theta) * kInvTwoPi;
+      const float frac = static_cast<float>(turns - __builtin_rint(turns));
+      const float sn = __builtin_amdgcn_sinf(frac);
+      const float c = __builtin_amdgcn_cosf(frac);
       const float other = s[partner];
       v[j] = first ? v[j] * c - other * sn : v[j] * c + other * sn;
     }
