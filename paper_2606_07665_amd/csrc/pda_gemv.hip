@@ -124,31 +124,45 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __re
     for (int i = 0; i < kR; ++i)
 #pragma unroll
       for (int bt = 0; bt < kNBT; ++bt) acc[i][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    constexpr int kChunk = kNBT * kR >= 4 ? 2 : (kNBT == 1 ? 8 : 4);  // k tiles in flight together
-    for (int j0 = 0; j0 < per; j0 += kChunk) {
-      u32x4 wa[kChunk][kR];
-      u32x4 xb[kChunk][kNBT];
+    // k tiles in chunks, the next chunk's loads in flight while the current
+    // chunk's MFMAs run
+    constexpr int kChunk = kNBT * kR >= 4 ? 2 : (kNBT == 1 ? 8 : 4);
+    u32x4 wa[2][kChunk][kR];
+    u32x4 xb[2][kChunk][kNBT];
+    auto load = [&](int buf, int j0) {
 #pragma unroll
       for (int j = 0; j < kChunk; ++j) {
 #pragma unroll
         for (int i = 0; i < kR; ++i)
-          wa[j][i] = __builtin_amdgcn_raw_buffer_load_b128(rw[i], (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
+          wa[buf][j][i] = __builtin_amdgcn_raw_buffer_load_b128(rw[i], (j0 + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
         const bool in = j0 + j < per;
 #pragma unroll
         for (int bt = 0; bt < kNBT; ++bt)
-          xb[j][bt] = in ? __builtin_amdgcn_raw_buffer_load_b128(rx, xrow[bt] + (kt0 + j0 + j) * kTileK * 2, 0, 0)
-                         : u32x4{0u, 0u, 0u, 0u};
+          xb[buf][j][bt] = in ? __builtin_amdgcn_raw_buffer_load_b128(rx, xrow[bt] + (kt0 + j0 + j) * kTileK * 2, 0, 0)
+                              : u32x4{0u, 0u, 0u, 0u};
       }
+    };
+    auto mma = [&](int buf) {
 #pragma unroll
       for (int j = 0; j < kChunk; ++j)
 #pragma unroll
         for (int i = 0; i < kR; ++i)
 #pragma unroll
           for (int bt = 0; bt < kNBT; ++bt)
-            acc[i][bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[j][i]),
-                                                                 __builtin_bit_cast(bf16x8, xb[j][bt]), acc[i][bt],
-                                                                 0, 0, 0);
+            acc[i][bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[buf][j][i]),
+                                                                 __builtin_bit_cast(bf16x8, xb[buf][j][bt]),
+                                                                 acc[i][bt], 0, 0, 0);
+    };
+    const int chunks = (per + kChunk - 1) / kChunk;
+    load(0, 0);
+    int c = 0;
+    for (; c + 2 <= chunks; c += 2) {
+      load(1, (c + 1) * kChunk);
+      mma(0);
+      if (c + 2 < chunks) load(0, (c + 2) * kChunk);
+      mma(1);
     }
+    if (c < chunks) mma(0);
     // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
     const int64_t first = (static_cast<int64_t>(g) * kt_count * waves + waves - 1) / units;  // first wave of g
     float* slot = part + (static_cast<int64_t>(g) * slots + (w - first)) * kR * batch * kTileRows;
