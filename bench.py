@@ -393,14 +393,7 @@ def prelude_main(args):
     value = nbytes / (ms_per_step * 1e-3) / 1e9
     achieved = gemv_bytes / (gemv_ms * 1e-3) / 1e9
     traffic = None
-    path = os.path.join(ROOT, "profiles", "traffic_prelude.json")
-    if os.path.exists(path):
-        try:
-            t = json.load(open(path))
-            if t.get("kernel_source_sha") == _kernel_sha(PRELUDE_SOURCES) and args.workload in t:
-                traffic = t[args.workload].get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = _gemv_traffic(args.workload)
     res = {
         "metric": "attention prelude (QKV GEMV + RoPE) µs/call + achieved HBM GB/s (% of MI355X peak), 1 GPU",
         "value": round(value, 1),
@@ -526,7 +519,7 @@ def oproj_main(args):
         "kernels_ms": {"gemv": round(gemv_ms, 5), "epilogue": round(epi_ms, 5)},
         "graph_us_per_call": None if graph_us is None else round(graph_us, 2),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": _gemv_traffic(args.workload),
                      "kernel": "gemv_kernel (packed-weight MFMA GEMV of the output projection)"},
     }
     if not args.no_cpu_baseline:
@@ -580,7 +573,20 @@ def prelude_cpu_baseline(w, budget_s):
 
 
 ATTENTION_SOURCES = ("pda_kernels.hip", "pda_internal.h")
-PRELUDE_SOURCES = ("pda_gemv.hip", "pda_gemv.h")
+GEMV_SOURCES = ("pda_gemv.hip", "pda_gemv.h")
+
+
+def _gemv_traffic(workload):
+    """Calibrated HBM bytes per GEMV launch from profiles/traffic_gemv.json,
+    or None when the GEMV source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic_gemv.json")
+    try:
+        t = json.load(open(path))
+        if t.get("kernel_source_sha") == _kernel_sha(GEMV_SOURCES) and workload in t:
+            return t[workload].get("bytes_per_launch")
+    except Exception:
+        pass
+    return None
 
 
 def _kernel_sha(files=ATTENTION_SOURCES):
