@@ -256,14 +256,7 @@ def main():
     nbytes = w.algorithmic_bytes()
     value = nbytes / (ms_per_step * 1e-3) / 1e9
     achieved = nbytes / (split_ms * 1e-3) / 1e9
-    traffic = None
-    if os.path.exists(args.traffic):
-        try:
-            t = json.load(open(args.traffic)).get(args.workload)
-            if t and t.get("kernel_source_sha") == _kernel_sha():
-                traffic = t.get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = _attention_traffic(args.traffic, args.workload)
     gpu_name = torch.cuda.get_device_name(0)
     res = {
         "metric": METRIC,
@@ -574,6 +567,20 @@ def prelude_cpu_baseline(w, budget_s):
 
 ATTENTION_SOURCES = ("pda_kernels.hip", "pda_internal.h")
 GEMV_SOURCES = ("pda_gemv.hip", "pda_gemv.h")
+
+
+def _attention_traffic(path, workload):
+    """Calibrated HBM bytes per attention-kernel launch from a traffic file
+    (profiles/traffic.json), or None when the attention source changed since
+    the counters were taken or the workload was not profiled."""
+    try:
+        doc = json.load(open(path))
+        t = doc.get(workload)
+        if t and doc.get("kernel_source_sha") == _kernel_sha(ATTENTION_SOURCES):
+            return t.get("bytes_per_launch")
+    except Exception:
+        pass
+    return None
 
 
 def _gemv_traffic(workload):
