@@ -5,11 +5,11 @@
 
 namespace pda {
 
-constexpr int kGemvWaves = 4;                   // independent waves per GEMV workgroup
+constexpr int kGemvWaves = 4;                   // waves per GEMV workgroup, splitting each segment's k tiles
 constexpr int kGemvThreads = 64 * kGemvWaves;
 constexpr int kGemvBlocksPerCu = 3;
-constexpr int kGemvMinTiles = 4;                // fewest k tiles a wave is given
-constexpr int kGemvMaxSlots = 16;               // most waves sharing one 16-row tile
+constexpr int kGemvMinTiles = 4;                // fewest k tiles per wave (on average)
+constexpr int kGemvMaxSlots = 16;               // most workgroups sharing one row group
 constexpr int kTileRows = 16;                   // rows of W per MFMA tile
 constexpr int kTileK = 32;                      // k per MFMA tile
 constexpr int kMaxGemvBatch = 64;               // sequences: four 16-column tiles
@@ -18,13 +18,13 @@ constexpr int kPackThreads = 256;
 // y[b, n] = sum_k x[b, k] W[n, k] over a packed W (see launch_pack), as
 // fp32 partials: a work unit is one 32-k tile of a group of `group`
 // consecutive 16-row tiles; part[g][j][i][b][16] holds the contribution of
-// the j-th wave that touched row group g, for its tile i.  GemvPlan says how
+// the j-th workgroup that touched row group g, for its tile i.  GemvPlan says how
 // the waves split the work.
 struct GemvPlan {
   int grid;     // workgroups of kGemvWaves waves
   int slots;    // partial slots per row group (an upper bound)
   int group;    // 16-row tiles per work unit (x fragments are reused across them)
-  int64_t waves, units;
+  int64_t blocks, units;
   int kt_count;
 };
 

@@ -73,27 +73,30 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
 }
 
 // Stream-K GEMV: the flattened space of (row group g, 32-k tile) units is
-// cut into equal contiguous ranges, one per wave, so every wave streams the
-// same number of packed weight tiles whatever the matrix shape.  A row group
-// is kR consecutive 16-row tiles: each x fragment a wave loads feeds kR
-// MFMAs, which keeps x reads (L2) at or below the weight reads (HBM) when the
-// batch spans several 16-column tiles.  A wave writes one partial (kR tiles
-// x batch, fp32) per row group its range touches, into slot
-// j = wave - first_wave(g) of that group; the epilogue sums a group's slots
-// in order (deterministic).
+// cut into equal contiguous ranges, one per workgroup, so every workgroup
+// streams the same number of packed weight tiles whatever the matrix shape.
+// A row group is kR consecutive 16-row tiles: each x fragment a wave loads
+// feeds kR MFMAs, which keeps x reads (L2) at or below the weight reads
+// (HBM) when the batch spans several 16-column tiles.  Inside a workgroup
+// the 4 waves split each group segment's k tiles into contiguous quarters
+// and add their accumulators in LDS; the workgroup then writes one partial
+// (kR tiles x batch, fp32) per row group its range touches, into slot
+// j = workgroup - first_workgroup(g) of that group, and the epilogue sums a
+// group's slots in order (deterministic).
 template <int kNBT, int kR>
 __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __restrict__ x,
                                                             const uint16_t* __restrict__ wp,
                                                             float* __restrict__ part, int batch, int n, int k,
                                                             int slots) {
+  __shared__ f32x4 red[kGemvWaves][kR * kNBT][64];
   const int lane = threadIdx.x & 63;
-  const int64_t waves = static_cast<int64_t>(gridDim.x) * (kGemvThreads / 64);
-  const int64_t w = static_cast<int64_t>(blockIdx.x) * (kGemvThreads / 64) + uniform(threadIdx.x >> 6);
+  const int wv = uniform(threadIdx.x >> 6);
+  const int64_t blocks = gridDim.x;
+  const int64_t blk = blockIdx.x;
   const int kt_count = k / kTileK;
   const int64_t units = static_cast<int64_t>(n / (kTileRows * kR)) * kt_count;
-  int64_t u = w * units / waves;
-  const int64_t u_end = (w + 1) * units / waves;
-  if (u >= u_end) return;
+  int64_t u = blk * units / blocks;
+  const int64_t u_end = (blk + 1) * units / blocks;
 
   // x rows at or past the batch fall outside the descriptor and read as zeros
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(batch) * k * 2u);
@@ -102,22 +105,22 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __re
   int xrow[kNBT];
 #pragma unroll
   for (int bt = 0; bt < kNBT; ++bt) xrow[bt] = ((16 * bt + r) * k + 8 * g4) * 2;
-  const uint32_t tile_stride = static_cast<uint32_t>(kt_count) * 1024u;  // bytes between row tiles
 
   while (u < u_end) {
     const int g = static_cast<int>(u / kt_count);
-    const int kt0 = static_cast<int>(u - static_cast<int64_t>(g) * kt_count);
     const int64_t seg_end = u_end < static_cast<int64_t>(g + 1) * kt_count ? u_end
                                                                            : static_cast<int64_t>(g + 1) * kt_count;
-    const int per = static_cast<int>(seg_end - u);
-    // the group's tiles at k tile kt0 onwards; tile i of the group is tile_stride further on
+    const int seg = static_cast<int>(seg_end - u);
+    // this wave's quarter of the segment: k tiles [kt0, kt0 + per)
+    const int lo = wv * seg / kGemvWaves;
+    const int per = (wv + 1) * seg / kGemvWaves - lo;
+    const int kt0 = static_cast<int>(u - static_cast<int64_t>(g) * kt_count) + lo;
     const uint16_t* wbase = wp + (static_cast<int64_t>(g) * kR * kt_count + kt0) * (kTileRows * kTileK);
     __amdgpu_buffer_rsrc_t rw[kR];
 #pragma unroll
-    for (int i = 0; i < kR; ++i)  // k tiles past the segment read as zeros (outside the descriptor)
+    for (int i = 0; i < kR; ++i)  // k tiles past the quarter read as zeros (outside the descriptor)
       rw[i] = make_rsrc(wbase + static_cast<int64_t>(i) * kt_count * (kTileRows * kTileK),
                         static_cast<uint32_t>(per) * 1024u);
-    (void)tile_stride;
 
     f32x4 acc[kR][kNBT];
 #pragma unroll
@@ -154,25 +157,38 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __re
                                                                  acc[i][bt], 0, 0, 0);
     };
     const int chunks = (per + kChunk - 1) / kChunk;
-    load(0, 0);
-    int c = 0;
-    for (; c + 2 <= chunks; c += 2) {
-      load(1, (c + 1) * kChunk);
-      mma(0);
-      if (c + 2 < chunks) load(0, (c + 2) * kChunk);
-      mma(1);
+    if (chunks > 0) {
+      load(0, 0);
+      int c = 0;
+      for (; c + 2 <= chunks; c += 2) {
+        load(1, (c + 1) * kChunk);
+        mma(0);
+        if (c + 2 < chunks) load(0, (c + 2) * kChunk);
+        mma(1);
+      }
+      if (c < chunks) mma(0);
     }
-    if (c < chunks) mma(0);
-    // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
-    const int64_t first = (static_cast<int64_t>(g) * kt_count * waves + waves - 1) / units;  // first wave of g
-    float* slot = part + (static_cast<int64_t>(g) * slots + (w - first)) * kR * batch * kTileRows;
+
+    // the 4 waves' accumulators meet in LDS; wave wv adds and stores the
+    // (tile, column tile) pairs wv, wv + 4, ...
 #pragma unroll
     for (int i = 0; i < kR; ++i)
 #pragma unroll
-      for (int bt = 0; bt < kNBT; ++bt) {
-        const int b = 16 * bt + r;
-        if (b < batch) *reinterpret_cast<f32x4*>(slot + (i * batch + b) * kTileRows + 4 * g4) = acc[i][bt];
-      }
+      for (int bt = 0; bt < kNBT; ++bt) red[wv][i * kNBT + bt][lane] = acc[i][bt];
+    __syncthreads();
+    // C layout: lane holds rows 4 (l / 16) + i, column l % 16 of its tile
+    const int64_t first = (static_cast<int64_t>(g) * kt_count * blocks + blocks - 1) / units;  // first block of g
+    float* slot = part + (static_cast<int64_t>(g) * slots + (blk - first)) * kR * batch * kTileRows;
+    for (int p = wv; p < kR * kNBT; p += kGemvWaves) {
+      const int i = p / kNBT;
+      const int bt = p - i * kNBT;
+      f32x4 sum = red[0][p][lane];
+#pragma unroll
+      for (int w2 = 1; w2 < kGemvWaves; ++w2) sum += red[w2][p][lane];
+      const int b = 16 * bt + r;
+      if (b < batch) *reinterpret_cast<f32x4*>(slot + (i * batch + b) * kTileRows + 4 * g4) = sum;
+    }
+    __syncthreads();  // red is rewritten by the next segment
     u = seg_end;
   }
 }
@@ -184,8 +200,8 @@ __device__ __forceinline__ float gemv_result(const float* __restrict__ part, con
   const int g = t / p.group;
   const int i = t - g * p.group;
   const int64_t x0 = static_cast<int64_t>(g) * p.kt_count;
-  const int64_t first = ((x0 + 1) * p.waves - 1) / p.units;
-  const int64_t last = ((x0 + p.kt_count) * p.waves - 1) / p.units;
+  const int64_t first = ((x0 + 1) * p.blocks - 1) / p.units;
+  const int64_t last = ((x0 + p.kt_count) * p.blocks - 1) / p.units;
   const int cnt = static_cast<int>(last - first + 1);  // at most kGemvMaxSlots (plan_gemv)
   const int64_t slot_floats = static_cast<int64_t>(p.group) * batch * kTileRows;
   const float* q = part + static_cast<int64_t>(g) * p.slots * slot_floats + (static_cast<int64_t>(i) * batch + b) * kTileRows +
@@ -381,14 +397,14 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
   const int64_t most = (p.units + static_cast<int64_t>(kGemvWaves) * kGemvMinTiles - 1) /
                        (static_cast<int64_t>(kGemvWaves) * kGemvMinTiles);
   if (grid > most) grid = most;
-  // at most kGemvMaxSlots waves per row group: waves <= (kGemvMaxSlots - 1) * groups
-  const int64_t cap = static_cast<int64_t>(kGemvMaxSlots - 1) * (tiles / p.group) / kGemvWaves;
+  // at most kGemvMaxSlots workgroups per row group: blocks <= (kGemvMaxSlots - 1) * groups
+  const int64_t cap = static_cast<int64_t>(kGemvMaxSlots - 1) * (tiles / p.group);
   if (grid > cap) grid = cap;
   if (grid < 1) grid = 1;
   p.grid = static_cast<int>(grid);
-  p.waves = grid * kGemvWaves;
-  // waves touching one row tile: its kt_count units span at most this many ranges
-  p.slots = static_cast<int>((static_cast<int64_t>(p.kt_count) * p.waves + p.units - 1) / p.units + 1);
+  p.blocks = grid;
+  // workgroups touching one row group: its kt_count units span at most this many ranges
+  p.slots = static_cast<int>((static_cast<int64_t>(p.kt_count) * p.blocks + p.units - 1) / p.units + 1);
   return p;
 }
 
