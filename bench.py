@@ -37,7 +37,8 @@ def parse():
     ap.add_argument("--workload", default="long70b",
                     choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16",
                              "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
-                             "prelude_falcon3", "oproj_qwen3_4b", "oproj_llama8b", "oproj_70b"])
+                             "prelude_falcon3", "oproj_qwen3_4b", "oproj_llama8b", "oproj_70b",
+                             "layer70b", "layer8b"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the oracle cpu_baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -137,6 +138,9 @@ def main():
         return
     if args.workload.startswith("oproj_"):
         oproj_main(args)
+        return
+    if args.workload.startswith("layer"):
+        layer_main(args)
         return
 
     import torch
@@ -530,6 +534,126 @@ def oproj_main(args):
         res_line["cpu_baseline"] = {"value": round(nbytes * calls / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
                                     "kind": "oracle",
                                     "sample": f"{calls} whole calls of the same workload, {dt:.1f} s fp64 numpy"}
+    print(json.dumps(res_line), flush=True)
+
+
+LAYERS = {
+    # attention workload, prelude workload, o_proj workload of one decode step
+    "layer70b": ("long70b", "prelude_70b", "oproj_70b"),
+    "layer8b": ("batched", "prelude_llama8b", "oproj_llama8b"),
+}
+
+
+def layer_main(args):
+    """One decode step of one transformer layer's attention block, as the
+    paper's runtime replays it: the prelude (QKV projection, RoPE) writing k
+    and v into the paged cache, paged decode attention over the advanced
+    lengths, and the output projection with residual add and RMSNorm.  The
+    lengths already count the new token.  Timed eagerly and as one captured
+    graph per step; weights are cold (several layer copies)."""
+    import torch
+    import workloads as W
+    from paper_2606_07665_amd import binding as pda
+
+    pda.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    att_name, pre_name, op_name = LAYERS[args.workload]
+    aw = W.make(att_name, poison=False)
+    pw = W.make_prelude(pre_name)
+    ow = W.make_oproj(op_name)
+    assert pw.batch == aw.batch == ow.batch and pw.num_q_heads == aw.num_q_heads
+    dev = torch.device("cuda:0")
+
+    def bf(a):
+        if a is None:
+            return None
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    k, v = bf(aw.k_cache), bf(aw.v_cache)
+    bt = torch.from_numpy(aw.block_table).to(dev)
+    lens = torch.from_numpy(aw.context_lens).to(dev)
+    x = bf(pw.x)
+    wq0, wo0 = pda.pack_weights(bf(pw.w_qkv)), pda.pack_weights(bf(ow.w_o))
+    layer_bytes = 2 * pw.rows * pw.hidden + 2 * ow.hidden * ow.in_features
+    copies = max(1, -(-1_000_000_000 // layer_bytes))
+    wqs = [wq0] + [wq0.clone() for _ in range(copies - 1)]
+    wos = [wo0] + [wo0.clone() for _ in range(copies - 1)]
+    b, hq, d = aw.batch, aw.num_q_heads, aw.head_dim
+    q = torch.empty((b, hq, d), dtype=torch.bfloat16, device=dev)
+    att = torch.empty_like(q)
+    res = bf(ow.residual)
+    nw = bf(ow.norm_w)
+    z = torch.empty_like(res)
+    h = torch.empty_like(res)
+    pkw = dict(num_q_heads=hq, num_kv_heads=aw.num_kv_heads, head_dim=d, rope_theta=float(pw.theta),
+               rotary_dim=pw.rotary_dim, interleaved=pw.interleaved, bias=bf(pw.bias), q_norm=bf(pw.q_norm),
+               k_norm=bf(pw.k_norm), eps=float(pw.eps))
+    scale = float(aw.scale)
+
+    def step(i):
+        pda.attention_prelude_append(x, wqs[i % copies], lens, q, k, v, bt, **pkw)
+        pda.paged_decode_attention(q, k, v, bt, lens, att, scale)
+        pda.o_proj_residual_norm(att.reshape(b, hq * d), wos[i % copies], res, nw, z, h, eps=float(ow.eps))
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+
+    graph_us = None
+    if not args.no_graph:
+        s = torch.cuda.Stream()
+        pda.workspace_reserve(b, hq, aw.num_kv_heads, d, aw.page_size, aw.max_pages, stream=s)
+        pda.prelude_workspace_reserve(pda.prelude_dims(b, pw.hidden, hq, aw.num_kv_heads, d, pw.rotary_dim,
+                                                       pw.interleaved, pw.theta, pw.eps), stream=s)
+        pda.o_proj_workspace_reserve(b, ow.in_features, ow.hidden, stream=s)
+        graphs = []
+        for i in range(copies):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s):
+                step(i)
+            graphs.append(g)
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize()
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record()
+        for i in range(args.steps):
+            graphs[i % copies].replay()
+        g1.record()
+        torch.cuda.synchronize()
+        graph_us = g0.elapsed_time(g1) / args.steps * 1e3
+
+    nbytes = aw.algorithmic_bytes() + pw.algorithmic_bytes() + ow.algorithmic_bytes()
+    res_line = {
+        "metric": "one layer's attention block per decode step (prelude + paged attention + o_proj) µs/step "
+                  "+ achieved HBM GB/s, 1 GPU",
+        "value": round(nbytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "us_per_call": round(ms_per_step * 1e3, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "attention": att_name, "prelude": pre_name, "o_proj": op_name,
+                   "weight_copies": copies, "algorithmic_bytes": nbytes, "parallelism": "single GPU",
+                   "device": torch.cuda.get_device_name(0)},
+        "graph_us_per_step": None if graph_us is None else round(graph_us, 2),
+    }
     print(json.dumps(res_line), flush=True)
 
 
