@@ -190,6 +190,10 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
  * pda_workspace_reserve -- grow the workspace of (current device, stream) so
  * that a later call with this shape (any num_queries and window) allocates
  * nothing (e.g. before graph capture).  Synchronous; may call hipMalloc.
+ * A graph captured on a stream keeps using the workspace it was captured
+ * with: reserve the largest shape before capturing, and neither grow that
+ * stream's workspace (a larger eager call on the same stream) nor release it
+ * (pda_release_workspaces) while the graph may still be replayed.
  */
 int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t head_dim, int32_t page_size, int32_t max_pages_per_seq,

@@ -393,7 +393,12 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
   p.group = (nbt > 1 && tiles % nbt == 0) ? nbt : 1;
   p.kt_count = k / kTileK;
   p.units = static_cast<int64_t>(tiles / p.group) * p.kt_count;
-  int64_t grid = static_cast<int64_t>(num_cus) * kGemvBlocksPerCu;
+  // workgroups resident per CU: the LDS of the cross-wave reduction
+  // (4 waves x group x column tiles x 1 KB) limits the 4 x 4 case to two
+  const int lds = kGemvWaves * p.group * nbt * 1024;
+  int per_cu = (160 * 1024) / lds;
+  per_cu = per_cu < kGemvBlocksPerCu ? per_cu : kGemvBlocksPerCu;
+  int64_t grid = static_cast<int64_t>(num_cus) * per_cu;
   const int64_t most = (p.units + static_cast<int64_t>(kGemvWaves) * kGemvMinTiles - 1) /
                        (static_cast<int64_t>(kGemvWaves) * kGemvMinTiles);
   if (grid > most) grid = most;
