@@ -159,6 +159,19 @@ int pda_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_c
                   int32_t num_pages, int32_t max_pages_per_seq, void* stream);
 
 /*
+ * pda_kv_append_n -- the same for num_tokens (1 .. 1024) new tokens per
+ * sequence, as a step of several query tokens needs (paged_decode_attention_ext):
+ * k_new, v_new bf16 [batch, num_tokens, num_kv_heads, head_dim]; the lengths
+ * count all of them and token j of sequence b lands at position
+ * L_b - num_tokens + j; positions below 0 (L_b < num_tokens) write nothing.
+ * pda_kv_append is this call with num_tokens = 1.
+ */
+int pda_kv_append_n(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                    const int32_t* block_table, const int32_t* context_lens, int32_t batch, int32_t num_tokens,
+                    int32_t num_kv_heads, int32_t head_dim, int32_t page_size, int32_t num_pages,
+                    int32_t max_pages_per_seq, void* stream);
+
+/*
  * paged_decode_attention_append -- pda_kv_append followed by
  * paged_decode_attention on the same stream: append the step's key/value,
  * then attend with the length that counts them.  Arguments as for the two

@@ -252,19 +252,29 @@ def kv_append(k_cache, v_cache, k_new, v_new, block_table, context_lens):
     and value (``k_new[b]``, ``v_new[b]``: [Hkv, D] bf16 bits) land at
     position L_b - 1: page ``block_table[b, (L_b - 1) // P]``, slot
     ``(L_b - 1) % P``, every kv head.  Sequences with L_b = 0 write nothing.
+
+    With several new tokens per sequence (``k_new``: [B, T, Hkv, D]), the
+    lengths count all of them and token j lands at position L_b - T + j;
+    positions below 0 (L_b < T) write nothing.
     Returns new (k_cache, v_cache) arrays; the inputs are not modified.
     """
     k = np.array(k_cache, copy=True)
     v = np.array(v_cache, copy=True)
     page_size = k.shape[1]
+    kn = np.asarray(k_new)
+    vn = np.asarray(v_new)
+    if kn.ndim == 3:
+        kn, vn = kn[:, None], vn[:, None]
+    tokens = kn.shape[1]
     for b in range(len(context_lens)):
         length = int(context_lens[b])
-        if length == 0:
-            continue
-        t = length - 1
-        page = int(block_table[b][t // page_size])
-        k[page, t % page_size] = k_new[b]
-        v[page, t % page_size] = v_new[b]
+        for j in range(tokens):
+            t = length - tokens + j
+            if t < 0:
+                continue
+            page = int(block_table[b][t // page_size])
+            k[page, t % page_size] = kn[b, j]
+            v[page, t % page_size] = vn[b, j]
     return k, v
 
 

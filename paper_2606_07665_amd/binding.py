@@ -57,6 +57,8 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.pda_o_proj_workspace_reserve.argtypes = [i32, i32, i32, vp]
     lib.pda_o_proj_workspace_reserve.restype = ctypes.c_int
     lib.pda_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
+    lib.pda_kv_append_n.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp]
+    lib.pda_kv_append_n.restype = ctypes.c_int
     lib.pda_kv_append.restype = ctypes.c_int
     lib.paged_decode_attention_append.argtypes = [vp] * 8 + [i32] * 7 + [f32, vp]
     lib.paged_decode_attention_append.restype = ctypes.c_int
@@ -216,6 +218,21 @@ def kv_append(k_new, v_new, k_cache, v_cache, block_table, context_lens, stream=
     _check(load().pda_kv_append(k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                 block_table.data_ptr(), context_lens.data_ptr(), b, hkv, d, p, n,
                                 block_table.shape[1], _stream_ptr(stream)))
+
+
+def kv_append_n(k_new, v_new, k_cache, v_cache, block_table, context_lens, stream=None):
+    """Scatter T new tokens per sequence ([B, T, Hkv, D] bf16) to positions
+    context_lens[b] - T + j (the lengths count all of them)."""
+    import torch
+    _check_cache_args(k_cache, v_cache, block_table, context_lens,
+                      (("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)))
+    n, p, hkv, d = k_cache.shape
+    b = block_table.shape[0]
+    if k_new.dim() != 4 or k_new.shape[0] != b or k_new.shape[2:] != (hkv, d) or v_new.shape != k_new.shape:
+        raise ValueError("k_new/v_new must be [B, T, Hkv, D]")
+    _check(load().pda_kv_append_n(k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                  block_table.data_ptr(), context_lens.data_ptr(), b, k_new.shape[1], hkv, d, p,
+                                  n, block_table.shape[1], _stream_ptr(stream)))
 
 
 def paged_decode_attention_append(q, k_new, v_new, k_cache, v_cache, block_table, context_lens, out, scale,

@@ -485,9 +485,19 @@ int pda_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_c
                   const int32_t* block_table, const int32_t* context_lens, int32_t batch, int32_t num_kv_heads,
                   int32_t head_dim, int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
                   void* stream) {
+  return pda_kv_append_n(k_new, v_new, k_cache, v_cache, block_table, context_lens, batch, 1, num_kv_heads,
+                         head_dim, page_size, num_pages, max_pages_per_seq, stream);
+}
+
+int pda_kv_append_n(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                    const int32_t* block_table, const int32_t* context_lens, int32_t batch, int32_t num_tokens,
+                    int32_t num_kv_heads, int32_t head_dim, int32_t page_size, int32_t num_pages,
+                    int32_t max_pages_per_seq, void* stream) {
   g_err.clear();
   int rc = check_shape(batch, num_kv_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
+  if (num_tokens < 1 || num_tokens > 1024)
+    return fail(PDA_ERR_SHAPE, "num_tokens must be in [1, 1024] (got %d)", num_tokens);
   if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
   if (batch == 0) return PDA_OK;
   if (!k_new || !v_new || !k_cache || !v_cache || !block_table || !context_lens)
@@ -505,6 +515,7 @@ int pda_kv_append(const void* k_new, const void* v_new, void* k_cache, void* v_c
   a.bt = block_table;
   a.lens = context_lens;
   a.batch = batch;
+  a.tokens = num_tokens;
   a.hkv = num_kv_heads;
   a.head_dim = head_dim;
   a.page_shift = log2i(page_size);

@@ -272,3 +272,10 @@ def test_oproj_argument_errors(lib, kwargs, code, text):
 
 def test_oproj_empty_batch_is_a_noop(lib):
     assert oproj_call(ptrs=[0] * 6, batch=0) == OK
+
+
+def test_kv_append_n_token_count_errors(lib):
+    f = B.load().pda_kv_append_n
+    assert f(*[16] * 6, 2, 0, 8, 128, 16, 64, 8, None) == SHAPE and "num_tokens" in B.last_error()
+    assert f(*[16] * 6, 2, 1025, 8, 128, 16, 64, 8, None) == SHAPE
+    assert f(*[0] * 6, 0, 4, 8, 128, 16, 64, 8, None) == OK

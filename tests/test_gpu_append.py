@@ -176,3 +176,41 @@ def test_decode_loop_in_a_graph(lib):
         assert np.array_equal(dev["lens"].cpu().numpy(), lens)
         check(out.float().cpu().numpy().astype(np.float64), ref, f"graph step {step}")
     assert np.array_equal(bits(dev["k"]), hk) and np.array_equal(bits(dev["v"]), hv)
+
+
+@pytest.mark.parametrize("tokens,p,lens", [(4, 16, [1, 3, 4, 5, 33, 700, 0]), (3, 1, [2, 9, 40]),
+                                           (16, 1024, [15, 16, 1025, 3000]), (2, 32, [31, 32, 33, 64])])
+def test_kv_append_n_bitwise(lib, tokens, p, lens):
+    import torch
+    w = W.build(lens, 8, 2, 128, p, seed=sum(lens) + tokens, pool="holes:0.2")
+    rng = np.random.default_rng(tokens)
+    shape = (w.batch, tokens, 2, 128)
+    kn = W.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    vn = W.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    dev = to_gpu(w)
+    lib.kv_append_n(bf_dev(kn), bf_dev(vn), dev["k"], dev["v"], dev["bt"], dev["lens"])
+    torch.cuda.synchronize()
+    rk, rv = oracle.kv_append(w.k_cache, w.v_cache, kn, vn, w.block_table, w.context_lens)
+    assert np.array_equal(bits(dev["k"]), rk) and np.array_equal(bits(dev["v"]), rv)
+
+
+def test_multi_token_step_append_then_attend(lib):
+    """A step of four new tokens per sequence (e.g. draft tokens): append
+    their k, v, then attend with four causal queries."""
+    import torch
+    tq = 4
+    lens = [4, 37, 300, 2049]
+    w = W.build(lens, 32, 8, 128, 16, seed=60, num_queries=tq)
+    rng = np.random.default_rng(61)
+    shape = (w.batch, tq, 8, 128)
+    kn = W.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    vn = W.f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32))
+    dev = to_gpu(w)
+    lib.kv_append_n(bf_dev(kn), bf_dev(vn), dev["k"], dev["v"], dev["bt"], dev["lens"])
+    out = torch.empty(tuple(w.q.shape), dtype=torch.bfloat16, device="cuda")
+    lib.paged_decode_attention_ext(dev["q"], dev["k"], dev["v"], dev["bt"], dev["lens"], out, float(w.scale))
+    torch.cuda.synchronize()
+    rk, rv = oracle.kv_append(w.k_cache, w.v_cache, kn, vn, w.block_table, w.context_lens)
+    assert np.array_equal(bits(dev["k"]), rk) and np.array_equal(bits(dev["v"]), rv)
+    ref = oracle.attend_masked(w.q, rk, rv, w.block_table, w.context_lens, w.scale)[0]
+    check(out.float().cpu().numpy().astype(np.float64), ref, "4-token step")

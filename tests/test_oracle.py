@@ -333,3 +333,22 @@ def test_queries_before_the_first_token_are_zero():
                 assert np.array_equal(out[b, j], np.zeros_like(out[b, j])) and np.isneginf(lse[b, j]).all()
             else:
                 assert np.isfinite(lse[b, j]).all()
+
+
+def test_kv_append_of_several_tokens_equals_one_at_a_time():
+    w = small([3, 40, 17, 2], hq=8, hkv=2, d=64, seed=33)
+    rng = np.random.default_rng(1)
+    T = 3
+    kn = rng.integers(0, 1 << 15, size=(4, T, 2, 64)).astype(np.uint16)
+    vn = rng.integers(0, 1 << 15, size=(4, T, 2, 64)).astype(np.uint16)
+    k1, v1 = oracle.kv_append(w.k_cache, w.v_cache, kn, vn, w.block_table, w.context_lens)
+    k2, v2 = w.k_cache, w.v_cache
+    for j in range(T):
+        lens = (w.context_lens - T + 1 + j).astype(np.int32)
+        live = lens > 0
+        kj, vj = kn[:, j].copy(), vn[:, j].copy()
+        k2, v2 = oracle.kv_append(k2, v2, kj, vj, w.block_table, np.where(live, lens, 0))
+    assert np.array_equal(k1, k2) and np.array_equal(v1, v2)
+    # the sequence of length 2 takes only its last two tokens (positions 0 and 1)
+    page = w.block_table[3, 0]
+    assert np.array_equal(k1[page, 0], kn[3, 1]) and np.array_equal(k1[page, 1], kn[3, 2])
