@@ -215,6 +215,12 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
 /* Free every workspace the library holds (synchronises their streams). */
 int pda_release_workspaces(void);
 
+/*
+ * Threads: calls may come from several host threads; error messages are
+ * per thread.  The workspace belongs to a (device, stream) pair, so calls on
+ * one stream must not be issued from two host threads at the same time.
+ */
+
 /* Thread-local message of the last failing call on this thread ("" if none). */
 const char* pda_last_error(void);
 

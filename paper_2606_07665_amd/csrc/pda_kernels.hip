@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "pda_internal.h"
 
 namespace pda {
@@ -632,12 +634,17 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
 template <int D, bool kLanePages>
 static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   const size_t lds = attn_lds_bytes(D, a.batch, a.waves);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
+  // the dynamic-LDS limit is raised once per device (bit = device ordinal)
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
+  if (!bit || !(attr_set.load() & bit)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    attr_set.fetch_or(bit);
   }
   hipLaunchKernelGGL((attn_kernel<D, kLanePages>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
                      a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.batch, a.hq, a.hkv, a.group,
