@@ -221,6 +221,20 @@ int pda_release_workspaces(void);
  * one stream must not be issued from two host threads at the same time.
  */
 
+/*
+ * pda_validate_paging -- debugging aid: synchronise `stream`, copy
+ * context_lens [batch] and block_table [batch, max_pages_per_seq] (device
+ * pointers) to the host and check 0 <= L_b <= max_pages_per_seq * page_size
+ * and 0 <= block_table[b][j] < num_pages for every page a sequence uses.
+ * Returns PDA_OK, or PDA_ERR_SHAPE naming the first bad entry.  The kernels
+ * never trust these device contents (out-of-range values are clamped, so a
+ * bad table gives wrong numbers but no fault); with PDA_DEBUG_VALIDATE=1 in
+ * the environment, every attention and append call runs this check first
+ * (synchronising; skipped while the stream is being captured).
+ */
+int pda_validate_paging(const int32_t* block_table, const int32_t* context_lens, int32_t batch,
+                        int32_t max_pages_per_seq, int32_t page_size, int32_t num_pages, void* stream);
+
 /* Thread-local message of the last failing call on this thread ("" if none). */
 const char* pda_last_error(void);
 

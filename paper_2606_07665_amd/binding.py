@@ -59,6 +59,8 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.pda_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, vp]
     lib.pda_kv_append_n.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp]
     lib.pda_kv_append_n.restype = ctypes.c_int
+    lib.pda_validate_paging.argtypes = [vp, vp, i32, i32, i32, i32, vp]
+    lib.pda_validate_paging.restype = ctypes.c_int
     lib.pda_kv_append.restype = ctypes.c_int
     lib.paged_decode_attention_append.argtypes = [vp] * 8 + [i32] * 7 + [f32, vp]
     lib.paged_decode_attention_append.restype = ctypes.c_int
@@ -389,3 +391,11 @@ def profile_read_o_proj() -> Tuple[float, float, int]:
     s, m, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
     _check(load().pda_profile_read_o_proj(ctypes.byref(s), ctypes.byref(m), ctypes.byref(n)))
     return s.value, m.value, n.value
+
+
+
+def validate_paging(block_table, context_lens, num_pages, page_size, stream=None) -> None:
+    """Check the device page table and lengths on the host (synchronises);
+    raises PdaError naming the first bad entry."""
+    _check(load().pda_validate_paging(block_table.data_ptr(), context_lens.data_ptr(), block_table.shape[0],
+                                      block_table.shape[1], page_size, num_pages, _stream_ptr(stream)))

@@ -270,6 +270,47 @@ int prof_read(int kind, double* first_ms, double* second_ms, int64_t* calls) {
   return rc;
 }
 
+// ---------------------------------------------------------------- validation
+// Host-side check of the device page tables and lengths (debugging aid):
+// synchronises the stream and copies both to the host.
+int validate_paging(const int32_t* block_table, const int32_t* context_lens, int32_t batch, int32_t maxp,
+                    int32_t page_size, int32_t num_pages, hipStream_t st) {
+  std::vector<int32_t> lens(batch), bt(static_cast<size_t>(batch) * maxp);
+  hipError_t e = hipMemcpyAsync(lens.data(), context_lens, lens.size() * 4, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(bt.data(), block_table, bt.size() * 4, hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "reading block_table / context_lens for validation");
+  const int64_t max_ctx = static_cast<int64_t>(maxp) * page_size;
+  for (int32_t b = 0; b < batch; ++b) {
+    if (lens[b] < 0 || lens[b] > max_ctx)
+      return fail(PDA_ERR_SHAPE, "context_lens[%d] = %d outside [0, %lld]", b, lens[b],
+                  static_cast<long long>(max_ctx));
+    const int32_t pages = (lens[b] + page_size - 1) / page_size;
+    for (int32_t j = 0; j < pages; ++j) {
+      const int32_t id = bt[static_cast<size_t>(b) * maxp + j];
+      if (id < 0 || id >= num_pages)
+        return fail(PDA_ERR_SHAPE, "block_table[%d][%d] = %d outside [0, %d)", b, j, id, num_pages);
+    }
+  }
+  return PDA_OK;
+}
+
+// PDA_DEBUG_VALIDATE=1: check the paging inputs before every attention or
+// append call (skipped while the stream is being captured).
+bool debug_validate() {
+  static const bool on = env_int("PDA_DEBUG_VALIDATE", 0, 0, 1) == 1;
+  return on;
+}
+
+int maybe_validate(const int32_t* block_table, const int32_t* context_lens, int32_t batch, int32_t maxp,
+                   int32_t page_size, int32_t num_pages, hipStream_t st) {
+  if (!debug_validate()) return PDA_OK;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cap) != hipSuccess || cap != hipStreamCaptureStatusNone) return PDA_OK;
+  return validate_paging(block_table, context_lens, batch, maxp, page_size, num_pages, st);
+}
+
 // ---------------------------------------------------------------- prelude
 bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
 
@@ -507,6 +548,9 @@ int pda_kv_append_n(const void* k_new, const void* v_new, void* k_cache, void* v
     return fail(PDA_ERR_ALIGN, "k_new, v_new, k_cache and v_cache must be 16-byte aligned");
   if (misaligned(block_table, 4) || misaligned(context_lens, 4))
     return fail(PDA_ERR_ALIGN, "block_table and context_lens must be 4-byte aligned");
+  if ((rc = maybe_validate(block_table, context_lens, batch, max_pages_per_seq, page_size, num_pages,
+                           static_cast<hipStream_t>(stream))))
+    return rc;
   pda::AppendArgs a;
   a.k_new = static_cast<const uint16_t*>(k_new);
   a.v_new = static_cast<const uint16_t*>(v_new);
@@ -579,6 +623,9 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
     return fail(PDA_ERR_ALIGN, "q, k_cache, v_cache and out must be 16-byte aligned");
   if (misaligned(block_table, 4) || misaligned(context_lens, 4))
     return fail(PDA_ERR_ALIGN, "block_table and context_lens must be 4-byte aligned");
+  if ((rc = maybe_validate(block_table, context_lens, batch, max_pages_per_seq, page_size, num_pages,
+                           static_cast<hipStream_t>(stream))))
+    return rc;
 
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -779,6 +826,19 @@ int pda_profile_read_o_proj(double* gemv_ms, double* epilogue_ms, int64_t* calls
   g_err.clear();
   if (!gemv_ms || !epilogue_ms || !calls) return fail(PDA_ERR_NULL, "pda_profile_read_o_proj: NULL output pointer");
   return prof_read(2, gemv_ms, epilogue_ms, calls);
+}
+
+int pda_validate_paging(const int32_t* block_table, const int32_t* context_lens, int32_t batch,
+                        int32_t max_pages_per_seq, int32_t page_size, int32_t num_pages, void* stream) {
+  g_err.clear();
+  if (batch < 0 || max_pages_per_seq <= 0 || page_size <= 0 || num_pages <= 0)
+    return fail(PDA_ERR_SHAPE, "batch, max_pages_per_seq, page_size and num_pages out of range");
+  if (batch == 0) return PDA_OK;
+  if (!block_table || !context_lens) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  if (static_cast<int64_t>(batch) * max_pages_per_seq > (int64_t{1} << 31))
+    return fail(PDA_ERR_SHAPE, "block_table too large to validate");
+  return validate_paging(block_table, context_lens, batch, max_pages_per_seq, page_size, num_pages,
+                         static_cast<hipStream_t>(stream));
 }
 
 int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream) {

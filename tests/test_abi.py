@@ -279,3 +279,11 @@ def test_kv_append_n_token_count_errors(lib):
     assert f(*[16] * 6, 2, 0, 8, 128, 16, 64, 8, None) == SHAPE and "num_tokens" in B.last_error()
     assert f(*[16] * 6, 2, 1025, 8, 128, 16, 64, 8, None) == SHAPE
     assert f(*[0] * 6, 0, 4, 8, 128, 16, 64, 8, None) == OK
+
+
+def test_validate_paging_argument_errors(lib):
+    f = B.load().pda_validate_paging
+    assert f(16, 16, -1, 8, 16, 64, None) == SHAPE
+    assert f(16, 16, 2, 0, 16, 64, None) == SHAPE
+    assert f(0, 16, 2, 8, 16, 64, None) == NULL
+    assert f(0, 0, 0, 8, 16, 64, None) == OK
