@@ -36,9 +36,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long70b",
                     choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16",
-                             "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
+                             "falcon3", "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
                              "prelude_falcon3", "oproj_qwen3_4b", "oproj_llama8b", "oproj_70b",
-                             "layer70b", "layer8b"])
+                             "oproj_falcon3", "layer70b", "layer8b", "layer_falcon3"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of each oracle cpu_baseline sample (all cores, then one thread)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -636,6 +636,7 @@ LAYERS = {
     # attention workload, prelude workload, o_proj workload of one decode step
     "layer70b": ("long70b", "prelude_70b", "oproj_70b"),
     "layer8b": ("batched", "prelude_llama8b", "oproj_llama8b"),
+    "layer_falcon3": ("falcon3", "prelude_falcon3", "oproj_falcon3"),
 }
 
 

@@ -64,6 +64,9 @@ enum pda_status {
 
 /* Supported set of this version. */
 #define PDA_MAX_BATCH 8192
+#define PDA_MAX_BATCH_D256 4096  /* attention at head_dim 256: the kernel's
+                                    per-sequence table shares LDS with its
+                                    34 KB-per-wave K/V tiles                */
 #define PDA_MAX_GROUP 16      /* num_q_heads / num_kv_heads                */
 #define PDA_MAX_PAGE_SIZE 1024
 #define PDA_MAX_KV_HEADS 1024
@@ -82,9 +85,9 @@ enum pda_status {
  *                be captured in a HIP graph).
  *   out          bf16 [batch, num_q_heads, head_dim], contiguous, 16-B
  *                aligned; fully written on success.  Must not alias inputs.
- *   head_dim     64 or 128.   page_size: a power of two in [1, 1024].
+ *   head_dim     64, 128 or 256.   page_size: a power of two in [1, 1024].
  *   num_q_heads  a multiple of num_kv_heads, with group <= 16.
- *   batch        0 .. 8192 (0 is a no-op).
+ *   batch        0 .. 8192 (0 is a no-op); at head_dim 256, 0 .. 4096.
  *   scale        finite fp32 multiplier of the scores (usually 1/sqrt(D)).
  *   stream       hipStream_t to launch on; NULL means the null stream.
  *

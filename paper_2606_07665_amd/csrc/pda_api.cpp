@@ -85,7 +85,7 @@ int check_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, in
     return fail(PDA_ERR_UNSUPPORTED, "num_kv_heads %d exceeds %d", hkv, PDA_MAX_KV_HEADS);
   if (hq / hkv > PDA_MAX_GROUP)
     return fail(PDA_ERR_UNSUPPORTED, "query group %d exceeds %d", hq / hkv, PDA_MAX_GROUP);
-  if (d != 64 && d != 128) return fail(PDA_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", d);
+  if (d != 64 && d != 128 && d != 256) return fail(PDA_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128, 256)", d);
   if (p <= 0 || maxp <= 0) return fail(PDA_ERR_SHAPE, "page_size and max_pages_per_seq must be positive");
   if (!is_pow2(p) || p > PDA_MAX_PAGE_SIZE)
     return fail(PDA_ERR_UNSUPPORTED, "page_size %d (supported: powers of two up to %d)", p, PDA_MAX_PAGE_SIZE);
@@ -95,6 +95,15 @@ int check_shape(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, in
   const int64_t steps = static_cast<int64_t>(batch) * ((max_ctx + pda::kStep - 1) / pda::kStep);
   if (steps >= (int64_t{1} << 31))
     return fail(PDA_ERR_UNSUPPORTED, "batch * max context exceeds 2^36 tokens");
+  return PDA_OK;
+}
+
+// Attention-only limits on top of check_shape.
+int check_attention(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp) {
+  int rc = check_shape(batch, hq, hkv, d, p, maxp);
+  if (rc) return rc;
+  if (d == 256 && batch > PDA_MAX_BATCH_D256)
+    return fail(PDA_ERR_UNSUPPORTED, "batch %d exceeds %d at head_dim 256", batch, PDA_MAX_BATCH_D256);
   return PDA_OK;
 }
 
@@ -108,16 +117,16 @@ struct Plan {
 
 int64_t align256(int64_t x) { return (x + 255) & ~int64_t{255}; }
 
-// Largest divisor of hkv that is at most kMaxWaves: the kv heads a workgroup
+// Largest divisor of hkv that is at most max_waves: the kv heads a workgroup
 // reads together from every page.
-int heads_per_group(int hkv) {
-  for (int d = pda::kMaxWaves; d > 1; --d)
+int heads_per_group(int hkv, int max_waves) {
+  for (int d = max_waves; d > 1; --d)
     if (hkv % d == 0) return d;
   return 1;
 }
 
-// Workgroups: one wave per kv head of a group, times step phases up to 8
-// waves; as many workgroups as fill the device (blocks_per_cu per CU), but
+// Workgroups: one wave per kv head of a group, times step phases up to
+// max_waves(d) waves (8; 4 at D = 256); as many workgroups as fill the device (blocks_per_cu per CU), but
 // none with fewer than min_steps 32-token steps per wave at the largest
 // context the page table allows.  Partial slots: one per (workgroup,
 // sequence piece), at most grid + batch * kv-head groups, each holding `cols`
@@ -125,8 +134,9 @@ int heads_per_group(int hkv) {
 Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus,
                int cols) {
   Plan pl;
-  pl.hgs = heads_per_group(hkv);
-  const int phases = pl.hgs >= pda::kMaxWaves ? 1 : pda::kMaxWaves / pl.hgs;
+  const int max_waves = pda::max_waves(d);
+  pl.hgs = heads_per_group(hkv, max_waves);
+  const int phases = max_waves / pl.hgs;
   pl.waves = pl.hgs * phases;
   const int64_t ngroups = hkv / pl.hgs;
   const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
@@ -432,7 +442,7 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
              int32_t* waves, int64_t* workspace_bytes) {
   g_err.clear();
   if (!grid_blocks || !waves || !workspace_bytes) return fail(PDA_ERR_NULL, "pda_plan: NULL output pointer");
-  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (num_cus <= 0) return fail(PDA_ERR_SHAPE, "num_cus must be positive");
   Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus,
@@ -446,7 +456,7 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
 int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                           int32_t page_size, int32_t max_pages_per_seq, void* stream) {
   g_err.clear();
-  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (batch == 0) return PDA_OK;
   int dev = 0;
@@ -577,7 +587,7 @@ int paged_decode_attention_append(const void* q, const void* k_new, const void* 
                                   int32_t max_pages_per_seq, float scale, void* stream) {
   g_err.clear();
   // validate the attention arguments first so that nothing is written on error
-  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
   if (batch > 0 && (!q || !out)) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
@@ -606,7 +616,7 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
                                int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
                                int32_t num_queries, int32_t window, float scale, void* stream) {
   g_err.clear();
-  int rc = check_shape(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
   if (num_queries < 1) return fail(PDA_ERR_SHAPE, "num_queries must be >= 1 (got %d)", num_queries);
@@ -634,6 +644,8 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
   if ((rc = device_cus(dev, &cus))) return rc;
   const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
                             num_queries * (num_q_heads / num_kv_heads));
+  if (pda::attn_lds_bytes(head_dim, batch, pl.waves) > static_cast<size_t>(pda::kMaxLdsBytes))
+    return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has", batch);
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
   if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;

@@ -64,6 +64,9 @@ hipError_t launch_append_kernel(const AppendArgs& a, hipStream_t st) {
   if (a.head_dim == 128)
     hipLaunchKernelGGL((append_kernel<128>), grid, dim3(kAppendThreads), 0, st, a.k_new, a.v_new, a.k, a.v,
                        a.bt, a.lens, a.batch, a.tokens, a.hkv, a.page_shift, a.num_pages, a.maxp);
+  else if (a.head_dim == 256)
+    hipLaunchKernelGGL((append_kernel<256>), grid, dim3(kAppendThreads), 0, st, a.k_new, a.v_new, a.k, a.v,
+                       a.bt, a.lens, a.batch, a.tokens, a.hkv, a.page_shift, a.num_pages, a.maxp);
   else
     hipLaunchKernelGGL((append_kernel<64>), grid, dim3(kAppendThreads), 0, st, a.k_new, a.v_new, a.k, a.v,
                        a.bt, a.lens, a.batch, a.tokens, a.hkv, a.page_shift, a.num_pages, a.maxp);

@@ -17,11 +17,12 @@
 //  * The batch (up to 64 sequences) forms the MFMA's B columns, in up to four
 //    16-column tiles; x rows past the batch read as zeros through the buffer
 //    descriptor's size.
-//  * Stream-K over (16-row tile, 32-k tile) units: every wave of a grid sized
-//    to the device streams the same number of packed weight tiles, whatever
-//    the shape, so no half-empty last round of workgroups; a wave leaves one
-//    fp32 partial per row tile it touched and the epilogue adds a tile's
-//    partials in wave order.
+//  * Stream-K over (row group, 32-k tile) units: every workgroup of a grid
+//    sized to the device streams the same number of packed weight tiles,
+//    whatever the shape, so no half-empty last round of workgroups.  The
+//    waves of a workgroup split its k tiles and add their accumulators in
+//    LDS; the workgroup leaves one fp32 partial per row group it touched and
+//    the epilogue adds a group's partials in workgroup order.
 //  * The epilogue (partial sums, bias, RMSNorm, rotation, bf16 rounding, and
 //    optionally the KV append into the page slot) runs per (sequence, head):
 //    a head's norm and its rotation pairs need all of its rows, which no

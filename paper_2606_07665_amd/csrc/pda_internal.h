@@ -10,6 +10,10 @@ namespace pda {
 constexpr int kStep = 32;                 // tokens per pipeline step of a wave
 constexpr int kMaxWaves = 8;              // waves per attention workgroup (at most)
 constexpr int kMaxBlockThreads = 64 * kMaxWaves;
+// Waves per attention workgroup at most for a head size: a wave of D = 256
+// holds 32 KB of K/V per step in registers, twice the D = 128 figure, so its
+// workgroup has one wave per SIMD (up to 512 registers each) instead of two.
+__host__ __device__ constexpr int max_waves(int head_dim) { return head_dim == 256 ? 4 : kMaxWaves; }
 constexpr int kMergeThreads = 256;
 constexpr int kMaxLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 constexpr int kMaxCols = 16;              // MFMA columns: query tokens x heads of a kv head
@@ -25,7 +29,7 @@ struct LaunchArgs {
   float* ws_ml;       // [slots, hgs, nq * group, 2] partial (max in log2 units, sum)
   int32_t* ws_pref;   // [batch + 1] steps prefix, written by the attention kernel
   int batch, hq, hkv, group, head_dim, page_shift, num_pages, maxp;
-  int hgs;            // kv heads per workgroup (a divisor of hkv, at most 8)
+  int hgs;            // kv heads per workgroup (a divisor of hkv, at most max_waves(head_dim))
   int waves;          // waves per workgroup: hgs x step phases
   int grid;           // workgroups of the attention kernel
   int min_steps;      // fewest 32-token steps per wave

@@ -61,12 +61,18 @@ struct Shape {
   static constexpr int kChunks = D / 8;         // 16-byte chunks per key/value row
   static constexpr int kRowsPerLoad = 64 / kChunks;      // rows per wave load
   static constexpr int kLoads = kStep / kRowsPerLoad;    // loads per step (K and V each)
-  // One LDS tile per wave, used for K and then V of each step.  K rows have
+  // One LDS tile per wave for the K and V rows of a step.  K rows have
   // stride 2D+16 bytes (the A-operand read, lane = row, starts rows 4 banks
   // apart); V rows stride 2D+32 (the transposed reads start rows 8 banks apart).
   static constexpr int kKRowBytes = 2 * D + 16;
   static constexpr int kVRowBytes = 2 * D + 32;
-  static constexpr int kTileBytes = kStep * kVRowBytes;
+  // D = 256 keeps one register buffer of K/V per wave (a step is 32 KB): a
+  // step's K and V rows go to separate regions of the tile as soon as they
+  // arrive, and the next step's loads reuse the registers.  Smaller heads
+  // keep two register buffers and pass K, then V, through one region.
+  static constexpr bool kOneBuffer = D == 256;
+  static constexpr int kVOffset = kOneBuffer ? kStep * kKRowBytes : 0;  // V region of the tile
+  static constexpr int kTileBytes = kVOffset + kStep * kVRowBytes;
   static constexpr int kAccBytes = 64 * kDT * 16;  // one wave's accumulator in LDS
   static_assert(kAccBytes <= kTileBytes, "accumulator exchange reuses the tile");
 };
@@ -146,7 +152,7 @@ __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t pa
 }
 
 template <int D, bool kLanePages>
-__global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
+__global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
     const int32_t* __restrict__ lens, uint16_t* __restrict__ out,
@@ -358,14 +364,27 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
 
-    auto compute = [&](int s, const u32x4 (&kr)[S::kLoads], const u32x4 (&vv)[S::kLoads]) {
-      const int t0 = s * kStep;
-      const bool edge = t0 + kStep > hi_min || t0 < lo_max;  // some key of the step is masked
-      // K rows -> tile; rows past the end arrived as zeros
+    // K and V rows of a step -> the tile; rows past the end arrived as zeros
+    // (never NaN * 0 in the P.V product)
+    auto stage_k = [&](const u32x4 (&kr)[S::kLoads]) {
 #pragma unroll
       for (int i = 0; i < S::kLoads; ++i)
         *reinterpret_cast<u32x4*>(tile + (S::kRowsPerLoad * i + vr) * S::kKRowBytes + 16 * vq) = kr[i];
-      lds_order();
+    };
+    auto stage_v = [&](const u32x4 (&vv)[S::kLoads]) {
+#pragma unroll
+      for (int i = 0; i < S::kLoads; ++i)
+        *reinterpret_cast<u32x4*>(tile + S::kVOffset + (S::kRowsPerLoad * i + vr) * S::kVRowBytes + 16 * vq) =
+            vv[i];
+    };
+
+    auto compute = [&](int s, const u32x4 (&kr)[S::kLoads], const u32x4 (&vv)[S::kLoads]) {
+      const int t0 = s * kStep;
+      const bool edge = t0 + kStep > hi_min || t0 < lo_max;  // some key of the step is masked
+      if constexpr (!S::kOneBuffer) {
+        stage_k(kr);
+        lds_order();
+      }
       // S^T = K Q^T: rows = keys 16T + 4*g4 + i, column = head c; the A operand
       // is key row c, d = 32*kk + 8*g4 .. +7
       f32x4 sacc[2];
@@ -380,11 +399,10 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
                                                              sacc[T], 0, 0, 0);
         }
       }
-      lds_order();
-      // V rows -> the same tile (rows past the end arrived as zeros: never NaN * 0)
-#pragma unroll
-      for (int i = 0; i < S::kLoads; ++i)
-        *reinterpret_cast<u32x4*>(tile + (S::kRowsPerLoad * i + vr) * S::kVRowBytes + 16 * vq) = vv[i];
+      if constexpr (!S::kOneBuffer) {
+        lds_order();
+        stage_v(vv);  // over the K rows just read
+      }
       // online softmax in log2 units
       float sv[2][4];
       float mx = -__builtin_inff();
@@ -425,7 +443,7 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
       for (int dt = 0; dt < S::kDT; ++dt) acc[dt] *= alpha;
       lds_order();
       // O^T += V^T P^T ; V^T operand via transposed LDS reads
-      const unsigned char* r0 = tile + (4 * g4 + (c >> 2)) * S::kVRowBytes + 8 * (c & 3);
+      const unsigned char* r0 = tile + S::kVOffset + (4 * g4 + (c >> 2)) * S::kVRowBytes + 8 * (c & 3);
       const unsigned char* r1 = r0 + 16 * S::kVRowBytes;
 #pragma unroll
       for (int dt = 0; dt < S::kDT; ++dt) {
@@ -440,7 +458,28 @@ __global__ __launch_bounds__(kMaxBlockThreads, 1) void attn_kernel(
     };
 
     // ---- this wave's steps
-    if (nsteps > 0) {
+    if constexpr (S::kOneBuffer) {
+      if (nsteps > 0) {
+        u32x4 kA[S::kLoads], vA[S::kLoads];
+        int pa0, pb0, pa1, pb1;
+        load_pids(0, pa0, pb0);
+        load_pids(1, pa1, pb1);
+        issue(0, pa0, pb0, kA, vA);
+        for (int k = 0; k < nsteps; ++k) {
+          load_pids(k + 2, pa0, pb0);
+          __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
+          stage_k(kA);
+          stage_v(vA);
+          lds_order();
+          // past the last step the big-page path issues zero-size loads
+          // (no traffic); the small-page path would read, so it stops
+          if (!kLanePages || k + 1 < nsteps) issue(k + 1, pa1, pb1, kA, vA);
+          compute(step_of(k), kA, vA);
+          pa1 = pa0;
+          pb1 = pb0;
+        }
+      }
+    } else if (nsteps > 0) {
       u32x4 kA[S::kLoads], vA[S::kLoads], kB[S::kLoads], vB[S::kLoads];
       int pa0, pb0, pa1, pb1;
       load_pids(0, pa0, pb0);
@@ -654,7 +693,9 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
 
 hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
   const bool lane_pages = a.page_shift < 4;
+  if (a.waves > max_waves(a.head_dim)) return hipErrorInvalidValue;
   if (a.head_dim == 128) return lane_pages ? launch_attn<128, true>(a, st) : launch_attn<128, false>(a, st);
+  if (a.head_dim == 256) return lane_pages ? launch_attn<256, true>(a, st) : launch_attn<256, false>(a, st);
   return lane_pages ? launch_attn<64, true>(a, st) : launch_attn<64, false>(a, st);
 }
 
@@ -675,11 +716,14 @@ hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
   const int64_t seqs = static_cast<int64_t>(a.batch) * (a.hkv / a.hgs);
   const bool many = a.grid >= 8 * seqs;
   if (a.head_dim == 128) return many ? launch_merge<128, 8>(a, st) : launch_merge<128, 1>(a, st);
+  if (a.head_dim == 256) return many ? launch_merge<256, 4>(a, st) : launch_merge<256, 1>(a, st);
   return many ? launch_merge<64, 8>(a, st) : launch_merge<64, 1>(a, st);
 }
 
 size_t attn_lds_bytes(int head_dim, int batch, int waves) {
-  const int base = head_dim == 128 ? pref_offset<128>(waves) : pref_offset<64>(waves);
+  const int base = head_dim == 256   ? pref_offset<256>(waves)
+                   : head_dim == 128 ? pref_offset<128>(waves)
+                                     : pref_offset<64>(waves);
   return static_cast<size_t>(base) + static_cast<size_t>(batch + 1) * sizeof(int32_t);
 }
 

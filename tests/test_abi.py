@@ -42,6 +42,8 @@ def call(ptr=16, batch=2, hq=32, hkv=8, d=128, p=16, n=64, maxp=8, scale=0.088, 
     (dict(p=0), SHAPE, "positive"),
     (dict(maxp=0), SHAPE, "positive"),
     (dict(batch=8193), UNSUPPORTED, "batch"),
+    (dict(batch=4097, d=256), UNSUPPORTED, "head_dim 256"),
+    (dict(d=512), UNSUPPORTED, "head_dim"),
     (dict(n=0), SHAPE, "num_pages"),
     (dict(scale=float("inf")), SCALE, "finite"),
     (dict(scale=float("nan")), SCALE, "finite"),
@@ -75,6 +77,15 @@ def test_planner_fills_the_device_and_sizes_the_workspace(lib):
     assert w % 6 == 0
     g, w, _ = B.plan(2, 16, 16, 128, 16, 100, num_cus=256)
     assert w == 8 * g
+    # head_dim 256: at most 4 waves per workgroup (one per SIMD), 4 kv heads
+    # of a group read together, phases making up 4 waves when Hkv is smaller
+    g, w, _ = B.plan(16, 12, 4, 256, 16, 2048, num_cus=256)
+    assert g == 256 and w == 4 * g
+    g, w, _ = B.plan(16, 16, 8, 256, 16, 2048, num_cus=256)
+    assert w == 4 * g
+    g, w, _ = B.plan(16, 8, 1, 256, 16, 2048, num_cus=256)
+    assert w == 4 * g
+    assert B.plan(4096, 12, 4, 256, 16, 4, num_cus=256)[0] >= 1
     with pytest.raises(B.PdaError):
         B.plan(1, 8, 3, 64, 16, 16)
     with pytest.raises(B.PdaError):

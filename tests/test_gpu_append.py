@@ -47,6 +47,8 @@ CASES = [
     (64, 4, 4, 1, [1, 7, 8], "holes:0.2"),
     (128, 8, 8, 1024, [1023, 1024, 1025, 3000], "holes:0.1"),
     (64, 16, 2, 128, [129, 128, 4000], "perm:200"),
+    (256, 12, 4, 16, [1, 15, 16, 17, 0, 900], "holes:0.2"),
+    (256, 8, 2, 2, [1, 2, 3, 65], "exact"),
 ]
 
 

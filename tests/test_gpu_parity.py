@@ -49,6 +49,13 @@ SMALL = [
     (128, 64, 8, 16, [5000, 3]),
     (64, 32, 2, 128, [1, 129, 4000]),
     (128, 8, 8, 1024, [1023, 1025, 3000]),
+    # head_dim 256 (one register buffer, 4-wave workgroups)
+    (256, 12, 4, 16, [1, 2, 31, 32, 33, 100, 1000]),
+    (256, 8, 1, 32, [16, 31, 32, 33, 95, 2000]),
+    (256, 16, 8, 16, [77, 513, 3000]),
+    (256, 4, 2, 8, [1, 7, 8, 9, 300]),
+    (256, 32, 2, 1, [1, 2, 40]),
+    (256, 8, 4, 64, [0, 63, 64, 65, 1000]),
 ]
 
 
@@ -68,6 +75,14 @@ def test_many_short_sequences_max_batch(lib):
     check(run(lib, w), ref(w), "B=8192")
 
 
+def test_head_dim_256_max_batch(lib):
+    rng = np.random.default_rng(8)
+    lens = rng.integers(0, 70, size=4096).tolist()
+    w = W.build(lens, 12, 4, 256, 16, seed=6, pool="holes:0.1")
+    log("case D=256 batch 4096, L in [0, 70)")
+    check(run(lib, w), ref(w), "D=256 B=4096")
+
+
 def _pad_head_dim(w, d):
     """Zero-pad q, K and V from head_dim 2 to d: the scores and the first two
     output features are unchanged, the padded features are 0."""
@@ -80,7 +95,7 @@ def _pad_head_dim(w, d):
     return dataclasses.replace(w, q=pad(w.q), k_cache=pad(w.k_cache), v_cache=pad(w.v_cache))
 
 
-@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("d", [64, 128, 256])
 @pytest.mark.parametrize("name,w,expected", golden_cases(), ids=lambda x: x if isinstance(x, str) else "")
 def test_golden_closed_forms(lib, name, w, expected, d):
     got = run(lib, _pad_head_dim(w, d))

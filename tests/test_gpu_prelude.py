@@ -133,20 +133,21 @@ def test_prelude_append_writes_exactly_its_outputs_into_the_slots(lib):
     assert np.array_equal(bits(dev["k"]), rk) and np.array_equal(bits(dev["v"]), rv)
 
 
-def test_decode_step_prelude_append_then_attention(lib):
-    """One decode step of a 32:8-head layer: the prelude appends k, v into
-    the cache and attention reads them back; checked against the oracle's
-    prelude, append and attention on the same bf16 values."""
+@pytest.mark.parametrize("hq,hkv,d,hidden", [(32, 8, 128, 1024), (12, 4, 256, 768)], ids=["32:8-D128", "12:4-D256"])
+def test_decode_step_prelude_append_then_attention(lib, hq, hkv, d, hidden):
+    """One decode step of a layer: the prelude appends k, v into the cache
+    and attention reads them back; checked against the oracle's prelude,
+    append and attention on the same bf16 values."""
     import torch
     lens = [40, 1, 300, 4096]
-    pw = W.build_prelude(4, 1024, 32, 8, 128, seed=41, lengths=lens, theta=5.0e5)
-    aw = W.build(lens, 32, 8, 128, 16, seed=42)
+    pw = W.build_prelude(4, hidden, hq, hkv, d, seed=41, lengths=lens, theta=5.0e5)
+    aw = W.build(lens, hq, hkv, d, 16, seed=42)
     dev = to_gpu(aw)
-    q = torch.empty((4, 32, 128), dtype=torch.bfloat16, device="cuda")
+    q = torch.empty((4, hq, d), dtype=torch.bfloat16, device="cuda")
     out = torch.empty_like(q)
     wp = lib.pack_weights(dev_bf16(pw.w_qkv))
     lib.attention_prelude_append(dev_bf16(pw.x), wp, dev["lens"], q, dev["k"], dev["v"], dev["bt"],
-                                 num_q_heads=32, num_kv_heads=8, head_dim=128, rope_theta=float(pw.theta))
+                                 num_q_heads=hq, num_kv_heads=hkv, head_dim=d, rope_theta=float(pw.theta))
     lib.paged_decode_attention(q, dev["k"], dev["v"], dev["bt"], dev["lens"], out, float(aw.scale))
     torch.cuda.synchronize()
     rq, rk, rv = ref_prelude(pw)

@@ -67,6 +67,9 @@ CASES = [
     (128, 8, 8, 1024, [1023, 1025, 3000], 1, 1500),
     (128, 12, 4, 16, [0, 1, 2, 3, 4], 4, 0),                     # L < Tq: leading zero rows
     (64, 4, 2, 64, [129, 4000, 64], 8, 2000),
+    (256, 12, 4, 16, [1, 2, 31, 32, 33, 100, 1000], 4, 0),     # head_dim 256
+    (256, 8, 2, 16, [5, 33, 66, 1027, 3000], 2, 100),
+    (256, 4, 4, 4, [5, 64, 65, 300], 3, 37),
 ]
 
 
@@ -168,3 +171,7 @@ def test_multiq_workload_sampled(lib):
 
 def test_gqa16_workload_sampled(lib):
     _sampled_variant(lib, "gqa16", [0, 31])
+
+
+def test_falcon3_workload_sampled(lib):
+    _sampled_variant(lib, "falcon3", [0, 7, 15])

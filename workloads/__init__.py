@@ -137,9 +137,13 @@ CONFIGS: Dict[str, Config] = {
         "gqa16", 32, 32, 2, 128, 16, 7, "fixed:32768", "exact",
         description="GLM-4-shaped 32:2 heads (G=16), batch 32, D=128, "
                     "L=32768, P=16"),
+    "falcon3": Config(
+        "falcon3", 16, 12, 4, 256, 16, 8, "uniform:16:32768", "exact",
+        description="Falcon3-7B-shaped layer with head_dim 256, batch 16, 12:4 heads "
+                    "(G=3), L~U[16,32768], P=16"),
 }
 CONFIG_ORDER = ["tiny", "llama8b", "batched", "long70b", "ragged"]
-VARIANT_ORDER = ["window", "multiq", "gqa16"]
+VARIANT_ORDER = ["window", "multiq", "gqa16", "falcon3"]
 
 
 def window_start(length: int, num_queries: int, window: int) -> int:
@@ -493,6 +497,8 @@ OPROJ_CONFIGS: Dict[str, OProjConfig] = {
     "oproj_llama8b": OProjConfig("oproj_llama8b", 64, 4096, 4096, 21,
                                  "Llama-3-8B-shaped o_proj, batch 64, 4096 -> 4096"),
     "oproj_70b": OProjConfig("oproj_70b", 4, 8192, 8192, 22, "70B-shaped o_proj, batch 4, 8192 -> 8192"),
+    "oproj_falcon3": OProjConfig("oproj_falcon3", 16, 3072, 3072, 23,
+                                 "Falcon3-7B-shaped o_proj, batch 16, 12 x 256 -> 3072"),
 }
 
 
