@@ -8,6 +8,18 @@ namespace pda {
 constexpr int kGemvWaves = 4;                   // waves per GEMV workgroup, splitting each segment's k tiles
 constexpr int kGemvThreads = 64 * kGemvWaves;
 constexpr int kGemvBlocksPerCu = 3;
+// Workgroups of gemv_kernel<nbt, r> resident per CU (one wave of each per
+// SIMD), set by the kernel's registers: the three- and four-column-tile
+// kernels with deep chunks or row groups would take more than 256 registers
+// a wave unless held to two waves per SIMD (their launch bounds); the others
+// need at most 168, so three fit.
+__host__ __device__ constexpr int gemv_blocks_per_cu(int nbt, int r) {
+  return (nbt == 3 || nbt * r >= 9) ? 2 : kGemvBlocksPerCu;
+}
+// Waves per SIMD the launch bounds ask for: only the heavy kernels need it.
+__host__ __device__ constexpr int gemv_min_waves_per_simd(int nbt, int r) {
+  return gemv_blocks_per_cu(nbt, r) == 2 ? 2 : 1;
+}
 constexpr int kGemvMinTiles = 4;                // fewest k tiles per wave (on average)
 constexpr int kGemvMaxSlots = 16;               // most workgroups sharing one row group
 constexpr int kTileRows = 16;                   // rows of W per MFMA tile

@@ -85,10 +85,9 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
 // j = workgroup - first_workgroup(g) of that group, and the epilogue sums a
 // group's slots in order (deterministic).
 template <int kNBT, int kR>
-__global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const uint16_t* __restrict__ x,
-                                                            const uint16_t* __restrict__ wp,
-                                                            float* __restrict__ part, int batch, int n, int k,
-                                                            int slots) {
+__global__ __launch_bounds__(kGemvThreads, gemv_min_waves_per_simd(kNBT, kR)) void gemv_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wp, float* __restrict__ part, int batch, int n,
+    int k, int slots) {
   __shared__ f32x4 red[kGemvWaves][kR * kNBT][64];
   const int lane = threadIdx.x & 63;
   const int wv = uniform(threadIdx.x >> 6);
@@ -394,11 +393,14 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
   p.group = (nbt > 1 && tiles % nbt == 0) ? nbt : 1;
   p.kt_count = k / kTileK;
   p.units = static_cast<int64_t>(tiles / p.group) * p.kt_count;
-  // workgroups resident per CU: the LDS of the cross-wave reduction
-  // (4 waves x group x column tiles x 1 KB) limits the 4 x 4 case to two
+  // workgroups resident per CU: the kernel's registers (its launch bounds)
+  // and the LDS of the cross-wave reduction (4 waves x group x column tiles
+  // x 1 KB) both limit it; a grid larger than what is resident would run in
+  // two rounds
   const int lds = kGemvWaves * p.group * nbt * 1024;
   int per_cu = (160 * 1024) / lds;
-  per_cu = per_cu < kGemvBlocksPerCu ? per_cu : kGemvBlocksPerCu;
+  const int regs = gemv_blocks_per_cu(nbt, p.group);
+  per_cu = per_cu < regs ? per_cu : regs;
   int64_t grid = static_cast<int64_t>(num_cus) * per_cu;
   const int64_t most = (p.units + static_cast<int64_t>(kGemvWaves) * kGemvMinTiles - 1) /
                        (static_cast<int64_t>(kGemvWaves) * kGemvMinTiles);
