@@ -486,14 +486,24 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       load_pids(1, pa1, pb1);
       issue(0, pa0, pb0, kA, vA);
       int k = 0;
+      // The waves of a workgroup meet at a barrier once per step, after
+      // issuing the next step's loads.  Left to themselves, the older wave
+      // on each SIMD wins issue arbitration and runs ahead: on MI355X waves
+      // 0-3 finished long70b at ~233 us and waves 4-7 at ~306 us, so the CU
+      // streamed with half its loads in flight for the last quarter.  Only
+      // the steps that every wave of the workgroup has (nmin) take the
+      // barrier, so each wave passes the same number of them.
+      const int nmin = (s1 - s0) / phases;
       for (; k + 2 < nsteps; k += 2) {
         load_pids(k + 2, pa0, pb0);
         __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
         issue(k + 1, pa1, pb1, kB, vB);
+        if (k + 2 < nmin) __builtin_amdgcn_s_barrier();
         compute(step_of(k), kA, vA);
         load_pids(k + 3, pa1, pb1);
         __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
         issue(k + 2, pa0, pb0, kA, vA);
+        if (k + 2 < nmin) __builtin_amdgcn_s_barrier();
         compute(step_of(k + 1), kB, vB);
       }
       if (k + 1 < nsteps) {
