@@ -175,26 +175,31 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   const int max_ctx = maxp << page_shift;
 
   // ---- per-block prefix over the batch of 32-token steps per sequence ----
+  // Each thread sums a run of sequences; a shuffle scan inside each wave and
+  // one exchange of wave totals through LDS make the prefix with two
+  // barriers (a tree over the workgroup took ~2 us of barriers).
   {
     const int per = (batch + nthreads - 1) / nthreads;
     const int lo = tid * per;
     const int hi = min(batch, lo + per);
     int sum = 0;
     for (int b = lo; b < hi; ++b) sum += seq_steps(clamp_len(lens[b], max_ctx), nq, window);
-    scan[tid] = sum;
-    __syncthreads();
-    for (int off = 1; off < nthreads; off <<= 1) {
-      int v = tid >= off ? scan[tid - off] : 0;
-      __syncthreads();
-      scan[tid] += v;
-      __syncthreads();
+    int incl = sum;  // inclusive prefix within the wave
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off, 64);
+      if ((tid & 63) >= off) incl += v;
     }
-    int run = scan[tid] - sum;
+    if ((tid & 63) == 63) scan[tid >> 6] = incl;  // wave totals
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < (tid >> 6); ++w) before += scan[w];
+    int run = before + incl - sum;
     for (int b = lo; b < hi; ++b) {
       pref[b] = run;
       run += seq_steps(clamp_len(lens[b], max_ctx), nq, window);
     }
-    if (tid == nthreads - 1) pref[batch] = scan[tid];
+    if (tid == nthreads - 1) pref[batch] = before + incl;
     __syncthreads();
   }
   if (blockIdx.x == 0) {
