@@ -75,9 +75,14 @@ struct Shape {
   static constexpr int kTileBytes = kVOffset + kStep * kVRowBytes;
   static constexpr int kAccBytes = 64 * kDT * 16;  // one wave's accumulator in LDS
   static_assert(kAccBytes <= kTileBytes, "accumulator exchange reuses the tile");
+  // The lengths read by the prefix scan stay in LDS for the pieces that
+  // follow (no second global read on the way to the first page ids); at
+  // D = 256 the tiles leave no room for them at the largest batch.
+  static constexpr bool kLensInLds = D != 256;
 };
 
 // LDS: [waves x tile][ml exchange waves x 16 x 2 floats][prefix batch+1 ints]
+// [lengths batch ints, when kLensInLds]
 template <int D>
 __host__ __device__ constexpr int ml_offset(int waves) { return waves * Shape<D>::kTileBytes; }
 template <int D>
@@ -167,6 +172,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   const int ngroups = hkv / hgs;    // kv-head groups per sequence
   const int ncols = group * nq;     // MFMA columns in use: (query token, head of the group)
   int32_t* pref = reinterpret_cast<int32_t*>(smem + pref_offset<D>(nwaves));
+  int32_t* lens_s = pref + batch + 1;  // clamped lengths (kLensInLds)
   float* ml_x = reinterpret_cast<float*>(smem + ml_offset<D>(nwaves));
   int32_t* scan = reinterpret_cast<int32_t*>(smem);  // reuses the tiles before the loop
 
@@ -183,7 +189,11 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     const int lo = tid * per;
     const int hi = min(batch, lo + per);
     int sum = 0;
-    for (int b = lo; b < hi; ++b) sum += seq_steps(clamp_len(lens[b], max_ctx), nq, window);
+    for (int b = lo; b < hi; ++b) {
+      const int L = clamp_len(lens[b], max_ctx);
+      if constexpr (S::kLensInLds) lens_s[b] = L;
+      sum += seq_steps(L, nq, window);
+    }
     int incl = sum;  // inclusive prefix within the wave
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -197,7 +207,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     int run = before + incl - sum;
     for (int b = lo; b < hi; ++b) {
       pref[b] = run;
-      run += seq_steps(clamp_len(lens[b], max_ctx), nq, window);
+      run += seq_steps(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx), nq, window);
     }
     if (tid == nthreads - 1) pref[batch] = before + incl;
     __syncthreads();
@@ -266,7 +276,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   while (true) {
     const int64_t remaining = xend - x;
     const int s1 = remaining < nb - s0 ? s0 + static_cast<int>(remaining) : nb;
-    const int L = uniform(clamp_len(lens[b], max_ctx));
+    const int L = uniform(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx));
     const int npages = (L + page - 1) >> page_shift;
     const int lo_seq = uniform(seq_start(L, nq, window));
     const int sb = lo_seq / kStep;                  // first step of the sequence
@@ -739,7 +749,8 @@ size_t attn_lds_bytes(int head_dim, int batch, int waves) {
   const int base = head_dim == 256   ? pref_offset<256>(waves)
                    : head_dim == 128 ? pref_offset<128>(waves)
                                      : pref_offset<64>(waves);
-  return static_cast<size_t>(base) + static_cast<size_t>(batch + 1) * sizeof(int32_t);
+  const bool lens_in_lds = head_dim == 256 ? Shape<256>::kLensInLds : Shape<128>::kLensInLds;
+  return static_cast<size_t>(base) + static_cast<size_t>(batch + 1 + (lens_in_lds ? batch : 0)) * sizeof(int32_t);
 }
 
 }  // namespace pda
