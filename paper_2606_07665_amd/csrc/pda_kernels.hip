@@ -93,6 +93,9 @@ __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirs
 // s_waitcnt vmcnt(0): wait for every outstanding vector memory load of the
 // wave (expcnt 7 and lgkmcnt 15 in the gfx9 encoding mean "do not wait").
 constexpr int kWaitAllVectorLoads = 0x0F70;
+// s_waitcnt vmcnt(n), n < 64: vmcnt is split over bits 3:0 and 15:14.
+constexpr int wait_vector_loads(int n) { return kWaitAllVectorLoads | (n & 15) | ((n >> 4) << 14); }
+constexpr int kIssueK = 1, kIssueV = 2;  // which loads of a step to issue
 
 __device__ __forceinline__ int clamp_len(int L, int max_ctx) {
   return L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
@@ -332,7 +335,10 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       return static_cast<int>(u < static_cast<unsigned>(num_pages) ? u : num_pages - 1);
     };
 
-    auto issue = [&](int k, int pa_raw, int pb_raw, u32x4 (&kr)[S::kLoads], u32x4 (&vv)[S::kLoads]) {
+    // which: kIssueK and/or kIssueV (the loads of a step, K and V interleaved
+    // when both are issued together)
+    auto issue = [&](int k, int pa_raw, int pb_raw, u32x4 (&kr)[S::kLoads], u32x4 (&vv)[S::kLoads],
+                     int which = kIssueK | kIssueV) {
       const int t0 = step_of(k) * kStep;
       // valid token rows in each 16-token half (0 for a step past the wave's last)
       const int live = k < nsteps ? L - t0 : 0;
@@ -348,11 +354,19 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
         const int bytesA = nA * tok_stride * 2, bytesB = nB * tok_stride * 2;
         const __amdgpu_buffer_rsrc_t rkA = page_rsrc(kg + oA, bytesA), rkB = page_rsrc(kg + oB, bytesB);
         const __amdgpu_buffer_rsrc_t rvA = page_rsrc(vg + oA, bytesA), rvB = page_rsrc(vg + oB, bytesB);
+        if (which == (kIssueK | kIssueV)) {
 #pragma unroll
-        for (int i = 0; i < S::kLoads; ++i) {
-          const bool hb = (S::kRowsPerLoad * i) >> 4;
-          kr[i] = ld16_stream(hb ? rkB : rkA, loff[i]);
-          vv[i] = ld16_stream(hb ? rvB : rvA, loff[i]);
+          for (int i = 0; i < S::kLoads; ++i) {
+            const bool hb = (S::kRowsPerLoad * i) >> 4;
+            kr[i] = ld16_stream(hb ? rkB : rkA, loff[i]);
+            vv[i] = ld16_stream(hb ? rvB : rvA, loff[i]);
+          }
+        } else if (which == kIssueK) {
+#pragma unroll
+          for (int i = 0; i < S::kLoads; ++i) kr[i] = ld16_stream((S::kRowsPerLoad * i) >> 4 ? rkB : rkA, loff[i]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < S::kLoads; ++i) vv[i] = ld16_stream((S::kRowsPerLoad * i) >> 4 ? rvB : rvA, loff[i]);
         }
       } else {
         // small pages: every lane looks up the page of its own token
@@ -365,10 +379,14 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
           // page_at keeps the address inside the pool; rows past the end are zeroed
           const bool ok = tok < t0 + live && tok >= lo_seq;
           const u32x4 zero = {0u, 0u, 0u, 0u};
-          const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kg + off));
-          const u32x4 vv_ = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vg + off));
-          kr[i] = ok ? kv : zero;
-          vv[i] = ok ? vv_ : zero;
+          if (which & kIssueK) {
+            const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kg + off));
+            kr[i] = ok ? kv : zero;
+          }
+          if (which & kIssueV) {
+            const u32x4 vv_ = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vg + off));
+            vv[i] = ok ? vv_ : zero;
+          }
         }
       }
     };
@@ -479,16 +497,23 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
         int pa0, pb0, pa1, pb1;
         load_pids(0, pa0, pb0);
         load_pids(1, pa1, pb1);
-        issue(0, pa0, pb0, kA, vA);
+        issue(0, pa0, pb0, kA, vA, kIssueK);
+        issue(0, pa0, pb0, kA, vA, kIssueV);
+        // A step's K rows are staged as soon as they arrive and the next
+        // step's K loads reuse their registers, then the same for V: the
+        // wave is never without loads in flight for a whole staging pass.
         for (int k = 0; k < nsteps; ++k) {
           load_pids(k + 2, pa0, pb0);
-          __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
-          stage_k(kA);
-          stage_v(vA);
-          lds_order();
           // past the last step the big-page path issues zero-size loads
           // (no traffic); the small-page path would read, so it stops
-          if (!kLanePages || k + 1 < nsteps) issue(k + 1, pa1, pb1, kA, vA);
+          const bool next = !kLanePages || k + 1 < nsteps;
+          __builtin_amdgcn_s_waitcnt(wait_vector_loads(S::kLoads));  // this step's K
+          stage_k(kA);
+          if (next) issue(k + 1, pa1, pb1, kA, vA, kIssueK);
+          __builtin_amdgcn_s_waitcnt(wait_vector_loads(S::kLoads));  // this step's V
+          stage_v(vA);
+          lds_order();
+          if (next) issue(k + 1, pa1, pb1, kA, vA, kIssueV);
           compute(step_of(k), kA, vA);
           pa1 = pa0;
           pb1 = pb0;
@@ -507,8 +532,9 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       // 0-3 finished long70b at ~233 us and waves 4-7 at ~306 us, so the CU
       // streamed with half its loads in flight for the last quarter.  Only
       // the steps that every wave of the workgroup has (nmin) take the
-      // barrier, so each wave passes the same number of them.
-      const int nmin = (s1 - s0) / phases;
+      // barrier, so each wave passes the same number of them.  (The
+      // small-page path, with its per-lane page lookups, would spill.)
+      const int nmin = kLanePages ? 0 : (s1 - s0) / phases;
       for (; k + 2 < nsteps; k += 2) {
         load_pids(k + 2, pa0, pb0);
         __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
