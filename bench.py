@@ -41,6 +41,9 @@ def parse():
                              "oproj_falcon3", "layer70b", "layer8b", "layer_falcon3"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of each oracle cpu_baseline sample (all cores, then one thread)")
+    ap.add_argument("--compute-path", default="mfma", choices=["mfma", "valu"],
+                    help="attention products on the matrix cores (default) or the vector-ALU variant "
+                         "(the measured alternative; head_dim 128 and <= 8 columns per kv head)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -203,6 +206,7 @@ def main():
     pda.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    pda.set_option(pda.OPT_COMPUTE_PATH, 1 if args.compute_path == "valu" else 0)
 
     def bf(a):
         return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
@@ -351,7 +355,8 @@ def main():
     nbytes = w.algorithmic_bytes()
     value = nbytes / (ms_per_step * 1e-3) / 1e9
     achieved = nbytes / (split_ms * 1e-3) / 1e9
-    traffic = _attention_traffic(args.traffic, args.workload)
+    traffic_key = args.workload if args.compute_path == "mfma" else f"{args.workload}@valu"
+    traffic = _attention_traffic(args.traffic, traffic_key)
     gpu_name = torch.cuda.get_device_name(0)
     res = {
         "metric": METRIC,
@@ -380,6 +385,7 @@ def main():
             "num_queries": w.num_queries, "window": w.window,
             "total_context_tokens": int(w.context_lens.astype(np.int64).sum()),
             "algorithmic_bytes": nbytes, "parallelism": "single GPU", "device": gpu_name,
+            "compute_path": args.compute_path,
         },
         "kernels_ms": {"split": round(split_ms, 5), "merge": round(merge_ms, 5)},
         "graph_us_per_call": None if graph_us is None else round(graph_us, 2),
@@ -391,7 +397,8 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-            "kernel": "attn_kernel (online-softmax pass over the paged KV)",
+            "kernel": "attn_kernel (online-softmax pass over the paged KV)" if args.compute_path == "mfma"
+            else "attn_kernel, vector-ALU variant (online-softmax pass over the paged KV)",
         },
     }
     if cpu is not None:

@@ -253,12 +253,23 @@ int32_t pda_version(void);
  *   PDA_OPT_MIN_STEPS      fewest 32-token steps a wave is given, >= 1
  *                          (default 2, env PDA_MIN_STEPS); a large value
  *                          forces fewer splits, 1 the most.
+ *   PDA_OPT_COMPUTE_PATH   where the attention kernel forms QK^T and P.V:
+ *                          0 = matrix cores (default, env PDA_COMPUTE_PATH),
+ *                          1 = vector ALU (bf16 dot2 products, DPP
+ *                          reductions across lanes, fp32 FMAs for P.V).
+ *                          Path 1 exists to measure the matrix-core choice
+ *                          against: it takes head_dim 128, page_size >= 16
+ *                          and at most 8 (query token, head) columns per kv
+ *                          head; other shapes fail with PDA_ERR_UNSUPPORTED
+ *                          while it is selected.  Outputs of the two paths
+ *                          agree within the attention tolerance, not bitwise.
  * Options are process-wide and apply to later calls.  pda_set_option
  * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
  * returns the current value or -1 for an unknown option.
  */
 #define PDA_OPT_BLOCKS_PER_CU 1
 #define PDA_OPT_MIN_STEPS 2
+#define PDA_OPT_COMPUTE_PATH 3
 int pda_set_option(int32_t option, int32_t value);
 int32_t pda_get_option(int32_t option);
 

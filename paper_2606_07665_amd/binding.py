@@ -337,6 +337,7 @@ def release_workspaces() -> None:
 
 OPT_BLOCKS_PER_CU = 1
 OPT_MIN_STEPS = 2
+OPT_COMPUTE_PATH = 3  # 0 = matrix cores (default), 1 = vector ALU (the measured alternative)
 
 
 def set_option(option: int, value: int) -> None:

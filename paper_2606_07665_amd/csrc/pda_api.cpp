@@ -52,6 +52,7 @@ constexpr int kMaxBlocksPerCu = 8;
 constexpr int kMaxMinSteps = 1 << 30;
 std::atomic<int> g_blocks_per_cu{-1};
 std::atomic<int> g_min_steps{-1};
+std::atomic<int> g_compute_path{-1};
 
 int blocks_per_cu() {
   int v = g_blocks_per_cu.load();
@@ -66,6 +67,15 @@ int min_steps_per_wave() {
   if (v < 0) {
     v = env_int("PDA_MIN_STEPS", 2, 1, kMaxMinSteps);
     g_min_steps.store(v);
+  }
+  return v;
+}
+
+int compute_path() {
+  int v = g_compute_path.load();
+  if (v < 0) {
+    v = env_int("PDA_COMPUTE_PATH", 0, 0, 1);
+    g_compute_path.store(v);
   }
   return v;
 }
@@ -104,6 +114,22 @@ int check_attention(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p
   if (rc) return rc;
   if (d == 256 && batch > PDA_MAX_BATCH_D256)
     return fail(PDA_ERR_UNSUPPORTED, "batch %d exceeds %d at head_dim 256", batch, PDA_MAX_BATCH_D256);
+  return PDA_OK;
+}
+
+// The compute path's own limits (PDA_OPT_COMPUTE_PATH): the vector-ALU
+// variant takes D = 128, pages of >= 16 tokens and <= 8 columns, and its LDS
+// tiles bound the batch.  *valu_cols = 0 (matrix cores) or 4 / 8.
+int check_compute_path(int32_t d, int32_t p, int cols, int32_t batch, int* valu_cols) {
+  *valu_cols = 0;
+  if (compute_path() != 1) return PDA_OK;
+  if (d != 128 || p < 16 || cols > 8)
+    return fail(PDA_ERR_UNSUPPORTED,
+                "the vector-ALU compute path takes head_dim 128, page_size >= 16 and at most 8 columns "
+                "(got head_dim %d, page_size %d, %d columns)", d, p, cols);
+  if (pda::attn_lds_bytes(d, batch, pda::max_waves(d), true) > static_cast<size_t>(pda::kMaxLdsBytes))
+    return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has on the vector-ALU path", batch);
+  *valu_cols = cols <= 4 ? 4 : 8;
   return PDA_OK;
 }
 
@@ -501,6 +527,10 @@ int pda_set_option(int32_t option, int32_t value) {
       if (value < 1) return fail(PDA_ERR_SHAPE, "min steps per wave must be >= 1");
       g_min_steps.store(value);
       return PDA_OK;
+    case PDA_OPT_COMPUTE_PATH:
+      if (value < 0 || value > 1) return fail(PDA_ERR_SHAPE, "compute path must be 0 or 1");
+      g_compute_path.store(value);
+      return PDA_OK;
     default:
       return fail(PDA_ERR_UNSUPPORTED, "unknown option %d", option);
   }
@@ -510,6 +540,7 @@ int32_t pda_get_option(int32_t option) {
   switch (option) {
     case PDA_OPT_BLOCKS_PER_CU: return blocks_per_cu();
     case PDA_OPT_MIN_STEPS: return min_steps_per_wave();
+    case PDA_OPT_COMPUTE_PATH: return compute_path();
     default: return -1;
   }
 }
@@ -590,6 +621,8 @@ int paged_decode_attention_append(const void* q, const void* k_new, const void* 
   int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
+  int valu_cols = 0;
+  if ((rc = check_compute_path(head_dim, page_size, num_q_heads / num_kv_heads, batch, &valu_cols))) return rc;
   if (batch > 0 && (!q || !out)) return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
   if ((reinterpret_cast<uintptr_t>(q) & 15) || (reinterpret_cast<uintptr_t>(out) & 15))
     return fail(PDA_ERR_ALIGN, "q, k_cache, v_cache and out must be 16-byte aligned");
@@ -625,6 +658,9 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
     return fail(PDA_ERR_UNSUPPORTED, "num_queries %d x query group %d exceeds %d", num_queries,
                 num_q_heads / num_kv_heads, pda::kMaxCols);
   if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
+  const int cols = num_queries * (num_q_heads / num_kv_heads);
+  int valu_cols = 0;
+  if ((rc = check_compute_path(head_dim, page_size, cols, batch, &valu_cols))) return rc;
   if (batch == 0) return PDA_OK;
   if (!q || !k_cache || !v_cache || !block_table || !context_lens || !out)
     return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
@@ -642,9 +678,8 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   int cus = 0;
   if ((rc = device_cus(dev, &cus))) return rc;
-  const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
-                            num_queries * (num_q_heads / num_kv_heads));
-  if (pda::attn_lds_bytes(head_dim, batch, pl.waves) > static_cast<size_t>(pda::kMaxLdsBytes))
+  const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus, cols);
+  if (pda::attn_lds_bytes(head_dim, batch, pl.waves, valu_cols > 0) > static_cast<size_t>(pda::kMaxLdsBytes))
     return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has", batch);
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
@@ -675,6 +710,7 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
   a.scale = scale;
   a.nq = num_queries;
   a.window = window;
+  a.valu_cols = valu_cols;
 
   const Rec rec = prof_begin(0);
   const bool prof = rec.a != nullptr;

@@ -36,10 +36,11 @@ struct LaunchArgs {
   float scale;
   int nq;      // query tokens per sequence (causal among them)
   int window;  // sliding window in tokens, 0 = none
+  int valu_cols = 0;  // 0: products on the matrix cores; 4 or 8: vector-ALU variant for that many columns
 };
 
 hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st);
 hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st);
-size_t attn_lds_bytes(int head_dim, int batch, int waves);
+size_t attn_lds_bytes(int head_dim, int batch, int waves, bool valu = false);
 
 }  // namespace pda

@@ -44,6 +44,7 @@ namespace pda {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -54,7 +55,9 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-template <int D>
+// kValu: the vector-ALU variant of the step (see attn_kernel), which keeps
+// one register buffer like D = 256 and reads K and V back from LDS row-wise.
+template <int D, bool kValu = false>
 struct Shape {
   static constexpr int kQK = D / 32;            // MFMAs per 16-key tile for QK^T
   static constexpr int kDT = D / 16;            // 16-wide d tiles of the output
@@ -70,7 +73,7 @@ struct Shape {
   // step's K and V rows go to separate regions of the tile as soon as they
   // arrive, and the next step's loads reuse the registers.  Smaller heads
   // keep two register buffers and pass K, then V, through one region.
-  static constexpr bool kOneBuffer = D == 256;
+  static constexpr bool kOneBuffer = D == 256 || kValu;
   static constexpr int kVOffset = kOneBuffer ? kStep * kKRowBytes : 0;  // V region of the tile
   static constexpr int kTileBytes = kVOffset + kStep * kVRowBytes;
   static constexpr int kAccBytes = 64 * kDT * 16;  // one wave's accumulator in LDS
@@ -83,10 +86,12 @@ struct Shape {
 
 // LDS: [waves x tile][ml exchange waves x 16 x 2 floats][prefix batch+1 ints]
 // [lengths batch ints, when kLensInLds]
-template <int D>
-__host__ __device__ constexpr int ml_offset(int waves) { return waves * Shape<D>::kTileBytes; }
-template <int D>
-__host__ __device__ constexpr int pref_offset(int waves) { return ml_offset<D>(waves) + waves * 16 * 2 * 4; }
+template <int D, bool kValu = false>
+__host__ __device__ constexpr int ml_offset(int waves) { return waves * Shape<D, kValu>::kTileBytes; }
+template <int D, bool kValu = false>
+__host__ __device__ constexpr int pref_offset(int waves) {
+  return ml_offset<D, kValu>(waves) + waves * 16 * 2 * 4;
+}
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
@@ -159,7 +164,33 @@ __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t pa
   return ((x + 1) * parts - 1) / total;
 }
 
-template <int D, bool kLanePages>
+// Value of a partner lane in the same 16-lane row (DPP), for the vector-ALU
+// variant's reductions.
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f(float x) {
+  // (every source lane exists for the patterns used; bound_ctrl lets the
+  // compiler fold the move into the consuming add or max as a DPP operand)
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), kCtrl, 0xF, 0xF, true));
+}
+constexpr int kDppRor8 = 0x128;        // row_ror:8: lane ^ 8 within the row
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror: lane ^ 7 within each half row
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2,3,0,1]: lane ^ 2
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1,0,3,2]: lane ^ 1
+
+// Register slot of token slot `is` (0..7) in the vector-ALU variant's list of
+// partial scores (index head_slot * 8 + slot): the token bit that the last
+// reduce level splits comes first, the bits kept in the lane come last.
+template <int NC>
+__device__ __forceinline__ constexpr int valu_slot(int is) {
+  return NC == 8 ? (((is & 1) << 2) | (is >> 1)) : (((is & 1) << 2) | (is & 2) | (is >> 2));
+}
+
+// kNC = 0: QK^T and P.V on the matrix cores (the path every entry point
+// uses).  kNC = 4 or 8: the same pass with both products on the vector ALU
+// (bf16 dot2 for QK^T, fp32 FMA for P.V) for up to kNC (query token, head)
+// columns at D = 128 -- the measured alternative to the matrix cores,
+// selected with PDA_OPT_COMPUTE_PATH.
+template <int D, bool kLanePages, int kNC = 0>
 __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
@@ -167,16 +198,18 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_pref,
     int batch, int hq, int hkv, int group, int hgs, int page_shift, int num_pages, int maxp,
     int min_steps, float scale_log2, int nq, int window) {
-  using S = Shape<D>;
+  constexpr bool kValu = kNC > 0;
+  static_assert(!kValu || (D == 128 && !kLanePages && (kNC == 4 || kNC == 8)), "vector-ALU variant shapes");
+  using S = Shape<D, kValu>;
   extern __shared__ __align__(16) unsigned char smem[];
   const int nthreads = blockDim.x;
   const int nwaves = nthreads >> 6;
   const int phases = nwaves / hgs;  // waves per kv head, interleaving steps
   const int ngroups = hkv / hgs;    // kv-head groups per sequence
   const int ncols = group * nq;     // MFMA columns in use: (query token, head of the group)
-  int32_t* pref = reinterpret_cast<int32_t*>(smem + pref_offset<D>(nwaves));
+  int32_t* pref = reinterpret_cast<int32_t*>(smem + pref_offset<D, kValu>(nwaves));
   int32_t* lens_s = pref + batch + 1;  // clamped lengths (kLensInLds)
-  float* ml_x = reinterpret_cast<float*>(smem + ml_offset<D>(nwaves));
+  float* ml_x = reinterpret_cast<float*>(smem + ml_offset<D, kValu>(nwaves));
   int32_t* scan = reinterpret_cast<int32_t*>(smem);  // reuses the tiles before the loop
 
   const int tid = threadIdx.x;
@@ -237,6 +270,20 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   // take the last token's key range and a zero query)
   const int qj = c < ncols ? c / group : nq - 1;
   const int qh = c - (c / group) * group;
+  // Vector-ALU variant: lane (vr, vq) = (lane / 16, lane % 16) holds
+  // d = 8 vq .. 8 vq + 7 of token rows 4 i + vr of a step.  Its partial QK^T
+  // sums over those 8 d are added across the 16 lanes of the row by a
+  // transpose-reduce whose DPP partners are lane ^ 8, lane ^ 7 (within each
+  // half row), lane ^ 2 and lane ^ 1, halving the values a lane holds at each
+  // level.  Every lane lists heads and tokens XOR-permuted by its own lane
+  // bits (vMh, vMi), chosen so that at every level the half a lane keeps is
+  // the half its partner sends (no selects); at the end the lane holds the
+  // whole scores of column vMh for kNC / 2 tokens of its row.
+  const int vb0 = lane & 1, vb1 = (lane >> 1) & 1, vb2 = (lane >> 2) & 1, vb3 = (lane >> 3) & 1;
+  const int vd3 = vb1 ^ vb2, vd4 = vb0 ^ vb2;
+  const int vMh = kNC == 8 ? (vb3 << 2 | vb2 << 1 | vd3) : (vb3 << 1 | vb2);
+  const int vMi = kNC == 8 ? vd4 : (vd3 | vd4 << 1);
+  const int qjv = vMh < ncols ? vMh / group : nq - 1;  // query token of the lane's column
 
   const int64_t total = static_cast<int64_t>(pref[batch]) * ngroups;
   if (total == 0) return;
@@ -293,13 +340,35 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
 
     // query operand (B of QK^T): column c, d = 32*kk + 8*g4 + e
     bf16x8 qop[S::kQK];
-    {
+    if constexpr (!kValu) {
       const uint16_t* qrow = q + ((static_cast<int64_t>(b) * nq + qj) * hq + g * group + qh) * D + 8 * g4;
 #pragma unroll
       for (int kk = 0; kk < S::kQK; ++kk) {
         u32x4 v = {0u, 0u, 0u, 0u};
         if (c < ncols) v = ld16(qrow + 32 * kk);
         qop[kk] = __builtin_bit_cast(bf16x8, v);
+      }
+    }
+    // vector-ALU variant: q of column hs ^ vMh at d = 8 vq .. +7, as bf16 pairs;
+    // its accumulator accv[column][e] holds d = 8 vq + e over the lane's tokens
+    constexpr int kNCv = kValu ? kNC : 4;  // (arrays unused on the matrix-core path)
+    u32x4 qv[kNCv];
+    float accv[kNCv][8];
+    const int hi_v = L - nq + 1 + qjv;
+    const int lo_v = window > 0 ? max(0, hi_v - window) : 0;
+    if constexpr (kValu) {
+#pragma unroll
+      for (int hs = 0; hs < kNC; ++hs) {
+        const int cq = hs ^ vMh;
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (cq < ncols) {
+          const int jq = cq / group;
+          v = ld16(q + ((static_cast<int64_t>(b) * nq + jq) * hq + g * group + (cq - jq * group)) * D +
+                   8 * (lane & 15));
+        }
+        qv[hs] = v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) accv[hs][e] = 0.f;
       }
     }
     const uint16_t* kg = kc + static_cast<int64_t>(g) * D;
@@ -490,6 +559,118 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       lds_order();
     };
 
+    // Vector-ALU step (kValu): K and V rows are in the tile (K region, then V
+    // region).  QK^T by bf16 dot2 on the lane's 8 d, the DPP transpose-reduce,
+    // the online softmax on the lane's kNC / 2 scores, then the probabilities
+    // and the rescale factors go through LDS (over the K rows just read) and
+    // P.V is fp32 FMAs on the lane's 8 tokens x 8 d.
+    auto compute_valu = [&](int s) {
+      constexpr int NC = kNCv;
+      constexpr int n = 8 * NC;
+      constexpr int NL = NC / 2;
+      const int t0 = s * kStep;
+      const bool edge = t0 + kStep > hi_min || t0 < lo_max;
+      // The first two reduce levels are taken as the partial sums are made:
+      // head slots hs and hs + NC / 2 (the pair level 1 adds) for each token
+      // slot, then two such results hs and hs + NC / 4 (the pair level 2
+      // adds), re-reading the lane's K chunks from LDS for each head slot
+      // pair, so that few partial sums are live at once.
+      auto qk_l1 = [&](int hs, float (&t)[8]) {
+#pragma unroll
+        for (int is = 0; is < 8; ++is) {
+          const int i = is ^ vMi;
+          const u32x4 kk = *reinterpret_cast<const u32x4*>(tile + (4 * i + vr) * S::kKRowBytes + 16 * vq);
+          float d0 = 0.f, d1 = 0.f;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            // vector elements go through plain scalars: __builtin_bit_cast of
+            // an element subscript (kk[j]) reads element 0 with this compiler
+            const unsigned kw = kk[j], qa = qv[hs][j], qb = qv[hs + NC / 2][j];
+            const bf16x2 kj = __builtin_bit_cast(bf16x2, kw);
+            d0 = __builtin_amdgcn_fdot2_f32_bf16(kj, __builtin_bit_cast(bf16x2, qa), d0, false);
+            d1 = __builtin_amdgcn_fdot2_f32_bf16(kj, __builtin_bit_cast(bf16x2, qb), d1, false);
+          }
+          t[valu_slot<NC>(is)] = d0 + dpp_f<kDppRor8>(d1);
+        }
+      };
+      float v[n / 4];
+#pragma unroll
+      for (int hq = 0; hq < NC / 4; ++hq) {
+        float ta[8], tb[8];
+        qk_l1(hq, ta);
+        qk_l1(hq + NC / 4, tb);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) v[hq * 8 + x] = ta[x] + dpp_f<kDppHalfMirror>(tb[x]);
+      }
+#pragma unroll
+      for (int x = 0; x < n / 8; ++x) v[x] += dpp_f<kDppXor2>(v[x + n / 8]);
+#pragma unroll
+      for (int x = 0; x < n / 16; ++x) v[x] += dpp_f<kDppXor1>(v[x + n / 16]);
+      // v[u] = score of column vMh, token row 4 * tok(u) + vr
+      auto tok = [&](int u) { return NC == 8 ? 2 * u + vd4 : 4 * u + 2 * vd4 + vd3; };
+      float sv[NL];
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int u = 0; u < NL; ++u) {
+        float x = v[u] * scale_log2;
+        const int t = t0 + 4 * tok(u) + vr;
+        if (edge && (t >= hi_v || t < lo_v)) x = -__builtin_inff();
+        sv[u] = x;
+        mx = fmaxf(mx, x);
+      }
+      // the other lanes of the column: lane ^ 1 (and ^ 2 at NC = 4), other rows
+      mx = fmaxf(mx, dpp_f<kDppXor1>(mx));
+      if constexpr (NC == 4) mx = fmaxf(mx, dpp_f<kDppXor2>(mx));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx);
+      const float m_ref = m_new == -__builtin_inff() ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+      m_run = m_new;
+      float psum = 0.f;
+      float pv[NL];
+#pragma unroll
+      for (int u = 0; u < NL; ++u) {
+        pv[u] = __builtin_amdgcn_exp2f(sv[u] - m_ref);
+        psum += pv[u];
+      }
+      l_lane = l_lane * alpha + psum;
+      lds_order();  // the K rows are read; p and alpha go over them
+      float* pl = reinterpret_cast<float*>(tile);  // p[token row][column], then alpha[column]
+#pragma unroll
+      for (int u = 0; u < NL; ++u) pl[(4 * tok(u) + vr) * NC + vMh] = pv[u];
+      pl[kStep * NC + vMh] = alpha;  // the same value from every lane of the column
+      lds_order();
+#pragma unroll
+      for (int c4 = 0; c4 < NC / 4; ++c4) {
+        const f32x4 al = *reinterpret_cast<const f32x4*>(pl + kStep * NC + 4 * c4);
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) accv[4 * c4 + cc][e] *= al[cc];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int tau = 4 * i + vr;
+        const u32x4 vw = *reinterpret_cast<const u32x4*>(tile + S::kVOffset + tau * S::kVRowBytes + 16 * vq);
+        float vf[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          vf[2 * j] = __builtin_bit_cast(float, vw[j] << 16);
+          vf[2 * j + 1] = __builtin_bit_cast(float, vw[j] & 0xFFFF0000u);
+        }
+#pragma unroll
+        for (int c4 = 0; c4 < NC / 4; ++c4) {
+          const f32x4 pp = *reinterpret_cast<const f32x4*>(pl + tau * NC + 4 * c4);
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) accv[4 * c4 + cc][e] = fmaf(pp[cc], vf[e], accv[4 * c4 + cc][e]);
+        }
+      }
+      lds_order();
+    };
+
     // ---- this wave's steps
     if constexpr (S::kOneBuffer) {
       if (nsteps > 0) {
@@ -514,7 +695,10 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
           stage_v(vA);
           lds_order();
           if (next) issue(k + 1, pa1, pb1, kA, vA, kIssueV);
-          compute(step_of(k), kA, vA);
+          if constexpr (kValu)
+            compute_valu(step_of(k));
+          else
+            compute(step_of(k), kA, vA);
           pa1 = pa0;
           pb1 = pb0;
         }
@@ -554,6 +738,40 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       } else {
         compute(step_of(k), kA, vA);
       }
+    }
+
+    if constexpr (kValu) {
+      // Into the matrix-core layout that the rest of the piece expects: lane
+      // (g4, c) holds d = 16 dt + 4 g4 .. +3 of column c; the four rows' token
+      // partials are added here, and the column's sum l sits in g4 = 0.
+      constexpr int NC = kNCv;
+      float lt = l_lane + dpp_f<kDppXor1>(l_lane);
+      if constexpr (NC == 4) lt += dpp_f<kDppXor2>(lt);
+      lt += __shfl_xor(lt, 16);
+      lt += __shfl_xor(lt, 32);
+      float* xa = reinterpret_cast<float*>(tile);  // [row vr][column][D], then (m, l) per column
+      float* xm = xa + 4 * NC * D;
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) {
+        f32x4* dst = reinterpret_cast<f32x4*>(xa + (vr * NC + cc) * D + 8 * vq);
+        dst[0] = f32x4{accv[cc][0], accv[cc][1], accv[cc][2], accv[cc][3]};
+        dst[1] = f32x4{accv[cc][4], accv[cc][5], accv[cc][6], accv[cc][7]};
+      }
+      xm[2 * vMh] = m_run;  // the same values from every lane of the column
+      xm[2 * vMh + 1] = lt;
+      lds_order();
+#pragma unroll
+      for (int dt = 0; dt < S::kDT; ++dt) {
+        f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+        if (c < NC) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sum += *reinterpret_cast<const f32x4*>(xa + (r * NC + c) * D + 16 * dt + 4 * g4);
+        }
+        acc[dt] = sum;
+      }
+      m_run = c < NC ? xm[2 * c] : -__builtin_inff();
+      l_lane = (c < NC && g4 == 0) ? xm[2 * c + 1] : 0.f;
+      lds_order();
     }
 
     // ---- finish the piece: combine the phases of each kv head, then write
@@ -721,9 +939,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
       __builtin_bit_cast(u32x2, o);
 }
 
-template <int D, bool kLanePages>
+template <int D, bool kLanePages, int kNC = 0>
 static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
-  const size_t lds = attn_lds_bytes(D, a.batch, a.waves);
+  const size_t lds = attn_lds_bytes(D, a.batch, a.waves, kNC > 0);
   // the dynamic-LDS limit is raised once per device (bit = device ordinal)
   static std::atomic<uint64_t> attr_set{0};
   int dev = 0;
@@ -731,12 +949,12 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
   if (!bit || !(attr_set.load() & bit)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages>),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages, kNC>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
     if (e != hipSuccess) return e;
     attr_set.fetch_or(bit);
   }
-  hipLaunchKernelGGL((attn_kernel<D, kLanePages>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
+  hipLaunchKernelGGL((attn_kernel<D, kLanePages, kNC>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
                      a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.batch, a.hq, a.hkv, a.group,
                      a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e, a.nq, a.window);
   return hipGetLastError();
@@ -745,6 +963,11 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
 hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
   const bool lane_pages = a.page_shift < 4;
   if (a.waves > max_waves(a.head_dim)) return hipErrorInvalidValue;
+  if (a.valu_cols) {
+    // vector-ALU variant: D = 128, pages of 16 tokens or more, at most 8 columns
+    if (a.head_dim != 128 || lane_pages || a.group * a.nq > a.valu_cols) return hipErrorInvalidValue;
+    return a.valu_cols == 4 ? launch_attn<128, false, 4>(a, st) : launch_attn<128, false, 8>(a, st);
+  }
   if (a.head_dim == 128) return lane_pages ? launch_attn<128, true>(a, st) : launch_attn<128, false>(a, st);
   if (a.head_dim == 256) return lane_pages ? launch_attn<256, true>(a, st) : launch_attn<256, false>(a, st);
   return lane_pages ? launch_attn<64, true>(a, st) : launch_attn<64, false>(a, st);
@@ -771,9 +994,9 @@ hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
   return many ? launch_merge<64, 8>(a, st) : launch_merge<64, 1>(a, st);
 }
 
-size_t attn_lds_bytes(int head_dim, int batch, int waves) {
+size_t attn_lds_bytes(int head_dim, int batch, int waves, bool valu) {
   const int base = head_dim == 256   ? pref_offset<256>(waves)
-                   : head_dim == 128 ? pref_offset<128>(waves)
+                   : head_dim == 128 ? (valu ? pref_offset<128, true>(waves) : pref_offset<128>(waves))
                                      : pref_offset<64>(waves);
   const bool lens_in_lds = head_dim == 256 ? Shape<256>::kLensInLds : Shape<128>::kLensInLds;
   return static_cast<size_t>(base) + static_cast<size_t>(batch + 1 + (lens_in_lds ? batch : 0)) * sizeof(int32_t);

@@ -110,6 +110,28 @@ def test_planner_grid_scales_with_options(lib):
     assert B.get_option(99) == -1
 
 
+def test_compute_path_option(lib):
+    assert B.get_option(B.OPT_COMPUTE_PATH) == 0
+    with pytest.raises(B.PdaError):
+        B.set_option(B.OPT_COMPUTE_PATH, 2)
+    try:
+        B.set_option(B.OPT_COMPUTE_PATH, 1)
+        assert B.get_option(B.OPT_COMPUTE_PATH) == 1
+        # shapes outside the vector-ALU path fail before any device work
+        for kw in (dict(d=64), dict(p=8), dict(hq=64, hkv=4)):
+            assert call(**kw) == UNSUPPORTED and "vector-ALU" in B.last_error()
+        assert ext_call(tq=3) == UNSUPPORTED and "vector-ALU" in B.last_error()  # 12 columns
+        assert call(batch=4000) == UNSUPPORTED and "LDS" in B.last_error()
+        f = B.load().paged_decode_attention_append
+        rc = f(16, 16, 16, 16, 16, 16, 16, 16, 2, 32, 8, 64, 16, 64, 8, ctypes.c_float(0.1), None)
+        assert rc == UNSUPPORTED and "vector-ALU" in B.last_error()
+        # up to 8 columns per kv head are taken (batch 0: no device work)
+        assert call(batch=0) == OK and ext_call(batch=0, tq=2) == OK
+    finally:
+        B.set_option(B.OPT_COMPUTE_PATH, 0)
+    assert call(d=64, batch=0) == OK
+
+
 def test_profile_read_null_pointer(lib):
     assert lib.pda_profile_read(None, None, None) == NULL
     s, m, n = B.profile_read()
