@@ -288,6 +288,24 @@ int pda_profile_read_prelude(double* gemv_ms, double* epilogue_ms, int64_t* call
 int pda_profile_read_o_proj(double* gemv_ms, double* epilogue_ms, int64_t* calls);
 
 /*
+ * Streaming-read reference for measurement harnesses: one kernel that only
+ * reads `bytes` of device memory at `buf` (16-byte aligned, bytes a positive
+ * multiple of 16), each byte once, with the attention kernel's loads
+ * (16-byte non-temporal buffer loads).  Its bandwidth is what an HBM-bound
+ * kernel can reach on this GPU, beside the 8 TB/s specification.
+ *   sink           device uint32 the kernel writes only if the data XOR-folds
+ *                  to one fixed value (it keeps the reads from being
+ *                  optimised away); caller-owned
+ *   unroll         16-byte loads in flight per lane: 4, 8 or 16 (0 = 16)
+ *   blocks_per_cu  workgroups of 4 waves per compute unit, 1 .. 32 (0 = 1)
+ * Asynchronous on `stream` (NULL = default); time it with events.  Returns
+ * PDA_OK, PDA_ERR_NULL, PDA_ERR_SHAPE (bytes), PDA_ERR_ALIGN,
+ * PDA_ERR_UNSUPPORTED (unroll, blocks_per_cu) or PDA_ERR_HIP.
+ */
+int pda_stream_read(const void* buf, int64_t bytes, uint32_t* sink, int32_t unroll, int32_t blocks_per_cu,
+                    void* stream);
+
+/*
  * ---------------------------------------------------------------------------
  * Attention prelude: the paper's kernel family (i) (Method, "Principle-Driven
  * LLM Kernel Generator"): the QKV projection of the new token's hidden

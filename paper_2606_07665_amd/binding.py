@@ -88,6 +88,8 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.pda_profile_read_prelude.restype = ctypes.c_int
     lib.pda_profile_read_o_proj.argtypes = lib.pda_profile_read.argtypes
     lib.pda_profile_read_o_proj.restype = ctypes.c_int
+    lib.pda_stream_read.argtypes = [vp, i64, vp, i32, i32, vp]
+    lib.pda_stream_read.restype = ctypes.c_int
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -346,6 +348,17 @@ def set_option(option: int, value: int) -> None:
 
 def get_option(option: int) -> int:
     return int(load().pda_get_option(option))
+
+
+def stream_read(buf, sink, unroll: int = 0, blocks_per_cu: int = 0, stream=None) -> None:
+    """The streaming-read reference kernel over a whole contiguous GPU tensor
+    (any dtype, 16-byte aligned, a multiple of 16 bytes); sink: an int32 GPU
+    tensor of at least one element."""
+    import torch
+    if not buf.is_cuda or not buf.is_contiguous() or not sink.is_cuda or sink.dtype != torch.int32:
+        raise ValueError("buf must be a contiguous GPU tensor and sink an int32 GPU tensor")
+    _check(load().pda_stream_read(buf.data_ptr(), buf.numel() * buf.element_size(), sink.data_ptr(), unroll,
+                                  blocks_per_cu, _stream_ptr(stream)))
 
 
 def profile_enable(on: bool = True) -> None:

@@ -17,6 +17,7 @@
 
 #include "pda.h"
 #include "pda_append.h"
+#include "pda_probe.h"
 #include "pda_gemv.h"
 #include "pda_internal.h"
 
@@ -543,6 +544,31 @@ int32_t pda_get_option(int32_t option) {
     case PDA_OPT_COMPUTE_PATH: return compute_path();
     default: return -1;
   }
+}
+
+int pda_stream_read(const void* buf, int64_t bytes, uint32_t* sink, int32_t unroll, int32_t blocks_per_cu,
+                    void* stream) {
+  g_err.clear();
+  if (bytes <= 0 || bytes % 16) return fail(PDA_ERR_SHAPE, "bytes must be a positive multiple of 16");
+  if (unroll == 0) unroll = 16;
+  if (blocks_per_cu == 0) blocks_per_cu = 1;
+  if (unroll != 4 && unroll != 8 && unroll != 16) return fail(PDA_ERR_UNSUPPORTED, "unroll must be 4, 8 or 16");
+  if (blocks_per_cu < 1 || blocks_per_cu > 32) return fail(PDA_ERR_UNSUPPORTED, "blocks_per_cu must be in [1, 32]");
+  if (!buf || !sink) return fail(PDA_ERR_NULL, "a pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(buf) & 15) return fail(PDA_ERR_ALIGN, "buf must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(sink) & 3) return fail(PDA_ERR_ALIGN, "sink must be 4-byte aligned");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  int rc = device_cus(dev, &cus);
+  if (rc) return rc;
+  const int64_t blocks = static_cast<int64_t>(cus) * blocks_per_cu;
+  if ((bytes + blocks - 1) / blocks > (int64_t{1} << 31) - 1024)
+    return fail(PDA_ERR_SHAPE, "bytes too large for %lld workgroups", static_cast<long long>(blocks));
+  e = pda::launch_stream_read(buf, bytes, sink, unroll, static_cast<int>(blocks), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "stream read kernel launch");
+  return PDA_OK;
 }
 
 int pda_profile_enable(int32_t on) {

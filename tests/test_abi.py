@@ -132,6 +132,18 @@ def test_compute_path_option(lib):
     assert call(d=64, batch=0) == OK
 
 
+def test_stream_read_argument_errors(lib):
+    f = B.load().pda_stream_read
+    assert f(16, 0, 16, 0, 0, None) == SHAPE and "multiple of 16" in B.last_error()
+    assert f(16, 24, 16, 0, 0, None) == SHAPE
+    assert f(16, 1024, 16, 3, 0, None) == UNSUPPORTED and "unroll" in B.last_error()
+    assert f(16, 1024, 16, 8, 33, None) == UNSUPPORTED and "blocks_per_cu" in B.last_error()
+    assert f(0, 1024, 16, 8, 8, None) == NULL
+    assert f(16, 1024, 0, 8, 8, None) == NULL
+    assert f(8, 1024, 16, 8, 8, None) == ALIGN
+    assert f(16, 1024, 18, 8, 8, None) == ALIGN
+
+
 def test_profile_read_null_pointer(lib):
     assert lib.pda_profile_read(None, None, None) == NULL
     s, m, n = B.profile_read()
