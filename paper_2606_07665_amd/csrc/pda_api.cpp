@@ -505,11 +505,12 @@ int pda_release_workspaces(void) {
   for (auto& kv : g_ws) {
     if (!kv.second.ptr) continue;
     int cur = 0;
-    hipGetDevice(&cur);
-    hipSetDevice(kv.first.first);
-    hipError_t e = hipStreamSynchronize(kv.first.second);
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess) e = hipSetDevice(kv.first.first);
+    if (e == hipSuccess) e = hipStreamSynchronize(kv.first.second);
     if (e == hipSuccess) e = hipFree(kv.second.ptr);
-    hipSetDevice(cur);
+    const hipError_t back = hipSetDevice(cur);
+    if (e == hipSuccess) e = back;
     if (e != hipSuccess) rc = hip_fail(e, "releasing a workspace");
   }
   g_ws.clear();

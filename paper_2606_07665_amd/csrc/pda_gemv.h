@@ -21,6 +21,23 @@ __host__ __device__ constexpr int gemv_min_waves_per_simd(int nbt, int r) {
   return gemv_blocks_per_cu(nbt, r) == 2 ? 2 : 1;
 }
 constexpr int kGemvMinTiles = 4;                // fewest k tiles per wave (on average)
+constexpr int kGemvGroupedUnits = 8;            // fewest units per workgroup to group row tiles of one batch tile
+// Thin-GEMM form (batches of more than 16): kXWaves waves per workgroup, one
+// row tile each, activations staged in LDS kXChunk k tiles at a time.
+constexpr int kXWaves = 8;
+constexpr int kXBlocksPerCu = 1;  // one workgroup per CU: fewer workgroups per row group, smaller partials
+// Measured on batch 64 (3072..8192 square and 3072 x 5120 weights): chunks
+// of 4 k tiles with one chunk in flight ran as fast as or faster than chunks
+// of 2 or 8 and than two or three chunks of weights in flight.
+constexpr int kXChunk = 4;        // k tiles per chunk
+constexpr int kXDepth = 1;        // chunks of weights in flight ahead of the one computing
+constexpr int kXRing = kXDepth + 1;
+constexpr int kXRowBytes = kXChunk * 64 + 16;  // one activation row of a chunk in LDS (padded)
+// s_waitcnt for a chunk's x and weights: with weights two or more chunks
+// ahead, only the kXChunk weight loads issued after the chunk's x may still
+// be in flight; with one, nothing
+constexpr int kWaitVmcntWeights = kXDepth > 1 ? (0x0F70 | (kXChunk & 15) | ((kXChunk >> 4) << 14)) : 0x0F70;
+__host__ __device__ constexpr int gemv_xlds_lds_bytes(int nbt) { return kXRing * nbt * 16 * kXRowBytes; }
 constexpr int kGemvMaxSlots = 16;               // most workgroups sharing one row group
 constexpr int kTileRows = 16;                   // rows of W per MFMA tile
 constexpr int kTileK = 32;                      // k per MFMA tile
@@ -33,7 +50,8 @@ constexpr int kPackThreads = 256;
 // the j-th workgroup that touched row group g, for its tile i.  GemvPlan says how
 // the waves split the work.
 struct GemvPlan {
-  int grid;     // workgroups of kGemvWaves waves
+  bool xlds;    // thin-GEMM form (gemv_xlds_kernel, kXWaves waves) instead of gemv_kernel
+  int grid;     // workgroups
   int slots;    // partial slots per row group (an upper bound)
   int group;    // 16-row tiles per work unit (x fragments are reused across them)
   int64_t blocks, units;

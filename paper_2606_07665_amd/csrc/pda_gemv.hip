@@ -34,6 +34,9 @@
 // norm spans all hidden features of a sequence.
 #include "pda_gemv.h"
 
+#include <atomic>
+#include <cstdlib>
+
 namespace pda {
 namespace {
 
@@ -78,7 +81,8 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
 // streams the same number of packed weight tiles whatever the matrix shape.
 // A row group is kR consecutive 16-row tiles: each x fragment a wave loads
 // feeds kR MFMAs, which keeps x reads (L2) at or below the weight reads
-// (HBM) when the batch spans several 16-column tiles.  Inside a workgroup
+// (HBM) when the batch spans several 16-column tiles, and cuts them 4x
+// within one tile of more than 4 sequences.  Inside a workgroup
 // the 4 waves split each group segment's k tiles into contiguous quarters
 // and add their accumulators in LDS; the workgroup then writes one partial
 // (kR tiles x batch, fp32) per row group its range touches, into slot
@@ -189,6 +193,132 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_waves_per_simd(kNBT, kR)) vo
       if (b < batch) *reinterpret_cast<f32x4*>(slot + (i * batch + b) * kTileRows + 4 * g4) = sum;
     }
     __syncthreads();  // red is rewritten by the next segment
+    u = seg_end;
+  }
+}
+
+// Thin-GEMM form of the same stream-K GEMV for batches of more than 16
+// sequences.  A workgroup of kXWaves waves works on row groups of kXWaves
+// row tiles, wave w on tile w of the group, over the group's k range in
+// chunks of kXChunk k tiles: the chunk's activations (batch x kXChunk x 32
+// bf16) are loaded once per workgroup with row-contiguous reads and staged
+// in LDS, where every wave reads its B fragments; the weights come straight
+// from the packed tiles into registers, kXDepth chunks ahead.  Compared with
+// gemv_kernel (x fragments loaded per wave, 16 rows x 64 bytes per load,
+// reused across the group's row tiles in registers), the x reads from L2
+// halve and are contiguous, and no cross-wave reduction is needed since each
+// wave owns its rows.  Partials and their layout are gemv_kernel's (group =
+// kXWaves tiles), so the epilogues are shared.
+template <int kNBT>
+__global__ __launch_bounds__(kXWaves * 64, 1) void gemv_xlds_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ wp, float* __restrict__ part, int batch, int n,
+    int k, int slots) {
+  extern __shared__ __align__(16) unsigned char xs[];  // [kXRing][kNBT * 16 rows][kXRowBytes]
+  constexpr int kRows = kNBT * kTileRows;
+  constexpr int kBuf = kRows * kXRowBytes;
+  constexpr int kRowPieces = kXChunk * kTileK / 8;                       // 16-byte pieces per row and chunk
+  constexpr int kPieces = kRows * kRowPieces;
+  constexpr int kPer = (kPieces + kXWaves * 64 - 1) / (kXWaves * 64);  // per thread
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = uniform(tid >> 6);
+  const int64_t blocks = gridDim.x;
+  const int64_t blk = blockIdx.x;
+  const int kt_count = k / kTileK;
+  const int64_t units = static_cast<int64_t>(n / (kTileRows * kXWaves)) * kt_count;
+  int64_t u = blk * units / blocks;
+  const int64_t u_end = (blk + 1) * units / blocks;
+  // x rows at or past the batch fall outside the descriptor and read as zeros
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(batch) * k * 2u);
+  const int r = lane & 15;
+  const int g4 = lane >> 4;
+  constexpr uint32_t kOutside = 0x80000000u;  // a buffer offset past any descriptor: reads zero
+
+  while (u < u_end) {
+    const int g = static_cast<int>(u / kt_count);
+    const int64_t seg_end = u_end < static_cast<int64_t>(g + 1) * kt_count ? u_end
+                                                                           : static_cast<int64_t>(g + 1) * kt_count;
+    const int kt_a = static_cast<int>(u - static_cast<int64_t>(g) * kt_count);
+    const int seg = static_cast<int>(seg_end - u);
+    const int nch = (seg + kXChunk - 1) / kXChunk;
+    // this wave's row tile over the segment; k tiles past it read as zeros
+    const uint16_t* wbase = wp + ((static_cast<int64_t>(g) * kXWaves + wv) * kt_count + kt_a) * (kTileRows * kTileK);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(wbase, static_cast<uint32_t>(seg) * 1024u);
+
+    f32x4 acc[kNBT];
+#pragma unroll
+    for (int bt = 0; bt < kNBT; ++bt) acc[bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    u32x4 wa[kXRing][kXChunk];
+    u32x4 xr[kPer];
+    // chunks past the segment load nothing (zero-size reads), so every
+    // iteration issues the same loads and the waits are one count
+    auto load_w = [&](int buf, int c) {
+#pragma unroll
+      for (int j = 0; j < kXChunk; ++j)
+        wa[buf][j] = __builtin_amdgcn_raw_buffer_load_b128(rw, (c * kXChunk + j) * 1024 + 16 * lane, 0, kCachePolicyNT);
+    };
+    // piece q: row q / kRowPieces, 16 bytes at k 8 (q % kRowPieces) of the chunk
+    auto load_x = [&](int c) {
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int q = tid + i * kXWaves * 64;
+        const int row = q / kRowPieces;
+        const int kk = c * kXChunk * kTileK + 8 * (q % kRowPieces);  // k within the segment
+        const bool live = q < kPieces && kk < seg * kTileK;
+        const uint32_t off = live ? static_cast<uint32_t>((row * k + kt_a * kTileK + kk) * 2) : kOutside;
+        xr[i] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
+      }
+    };
+    auto store_x = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < kPer; ++i) {
+        const int q = tid + i * kXWaves * 64;
+        if (q < kPieces)
+          *reinterpret_cast<u32x4*>(xs + buf * kBuf + (q / kRowPieces) * kXRowBytes + 16 * (q % kRowPieces)) = xr[i];
+      }
+    };
+    auto mma = [&](int buf) {
+#pragma unroll
+      for (int j = 0; j < kXChunk; ++j) {
+#pragma unroll
+        for (int bt = 0; bt < kNBT; ++bt) {
+          const u32x4 b = *reinterpret_cast<const u32x4*>(xs + buf * kBuf + (16 * bt + r) * kXRowBytes + 64 * j + 16 * g4);
+          acc[bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[buf][j]),
+                                                            __builtin_bit_cast(bf16x8, b), acc[bt], 0, 0, 0);
+        }
+      }
+    };
+    // x of chunk c + 1 and the weights of chunk c + kXDepth are in flight
+    // while chunk c computes; x goes through a ring of kXRing LDS buffers,
+    // so one barrier per chunk orders its writes after the last reads
+    load_x(0);
+#pragma unroll
+    for (int d = 0; d < kXDepth; ++d) load_w(d, d);
+    for (int c0 = 0; c0 < nch; c0 += kXRing) {
+#pragma unroll
+      for (int sl = 0; sl < kXRing; ++sl) {
+        const int c = c0 + sl;
+        if (c < nch) {
+          // everything but the weights issued after x of chunk c has arrived
+          __builtin_amdgcn_s_waitcnt(kWaitVmcntWeights);
+          store_x(sl);
+          load_x(c + 1);
+          load_w((sl + kXDepth) % kXRing, c + kXDepth);
+          __syncthreads();
+          mma(sl);
+        }
+      }
+    }
+    // this wave's rows of the group: one partial per (workgroup, group)
+    const int64_t first = (static_cast<int64_t>(g) * kt_count * blocks + blocks - 1) / units;  // first block of g
+    float* slot = part + (static_cast<int64_t>(g) * slots + (blk - first)) * kXWaves * batch * kTileRows;
+#pragma unroll
+    for (int bt = 0; bt < kNBT; ++bt) {
+      const int b = 16 * bt + r;
+      if (b < batch) *reinterpret_cast<f32x4*>(slot + (wv * batch + b) * kTileRows + 4 * g4) = acc[bt];
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // the loads issued past the segment
+    __syncthreads();                     // the LDS buffers are rewritten by the next segment
     u = seg_end;
   }
 }
@@ -390,8 +520,46 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
   GemvPlan p;
   const int nbt = (batch + 15) / 16;
   const int tiles = n / kTileRows;
-  p.group = (nbt > 1 && tiles % nbt == 0) ? nbt : 1;
+  // Several row tiles per unit share each x fragment: as many as there are
+  // 16-column batch tiles.  Within one batch tile of more than 4 sequences,
+  // four, when every workgroup still gets at least kGemvGroupedUnits units
+  // (x rows past the batch read as zeros with no traffic, so a few
+  // sequences gain nothing; at 8 and 16 sequences four tiles per unit ran
+  // 7% and 24% faster on 8192 x 8192 and 15% on 3072 x 5120, but 20% slower
+  // on 3072 x 3072, where the larger partials of too few units per
+  // workgroup cost more than the x reads saved).
   p.kt_count = k / kTileK;
+  p.xlds = false;
+  p.group = 1;
+  // batches of more than 16: the thin-GEMM form when the row tiles split
+  // into groups of kXWaves (PDA_GEMV_THIN=0 in the environment selects
+  // gemv_kernel instead, for measurement)
+  static const bool thin_ok = [] {
+    const char* e = std::getenv("PDA_GEMV_THIN");
+    return !(e && e[0] == '0');
+  }();
+  if (thin_ok && nbt > 1 && tiles % kXWaves == 0) {
+    p.xlds = true;
+    p.group = kXWaves;
+    p.units = static_cast<int64_t>(tiles / kXWaves) * p.kt_count;
+    int64_t grid = static_cast<int64_t>(num_cus) * kXBlocksPerCu;
+    const int64_t most = (p.units + kGemvMinTiles - 1) / kGemvMinTiles;  // >= kGemvMinTiles tiles per wave
+    if (grid > most) grid = most;
+    const int64_t cap = static_cast<int64_t>(kGemvMaxSlots - 1) * (tiles / kXWaves);
+    if (grid > cap) grid = cap;
+    if (grid < 1) grid = 1;
+    p.grid = static_cast<int>(grid);
+    p.blocks = grid;
+    p.slots = static_cast<int>((static_cast<int64_t>(p.kt_count) * p.blocks + p.units - 1) / p.units + 1);
+    return p;
+  }
+  if (nbt > 1 && tiles % nbt == 0) {
+    p.group = nbt;
+  } else if (nbt == 1 && batch > 4 && tiles % 4 == 0 &&
+             static_cast<int64_t>(tiles / 4) * p.kt_count >=
+                 static_cast<int64_t>(kGemvGroupedUnits) * num_cus * gemv_blocks_per_cu(1, 4)) {
+    p.group = 4;
+  }
   p.units = static_cast<int64_t>(tiles / p.group) * p.kt_count;
   // workgroups resident per CU: the kernel's registers (its launch bounds)
   // and the LDS of the cross-wave reduction (4 waves x group x column tiles
@@ -420,15 +588,40 @@ int64_t gemv_partial_floats(const GemvPlan& p, int batch, int n) {
   return static_cast<int64_t>(n / kTileRows) * p.slots * batch * kTileRows;  // groups * group tiles = n / 16
 }
 
+template <int kNBT>
+hipError_t launch_xlds(const GemvArgs& a, hipStream_t st) {
+  constexpr int lds = gemv_xlds_lds_bytes(kNBT);
+  // the dynamic-LDS limit is raised once per device (bit = device ordinal)
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
+  if (!bit || !(attr_set.load() & bit)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_xlds_kernel<kNBT>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    attr_set.fetch_or(bit);
+  }
+  hipLaunchKernelGGL((gemv_xlds_kernel<kNBT>), dim3(a.plan.grid), dim3(kXWaves * 64), lds, st, a.x, a.wp, a.part,
+                     a.batch, a.n, a.k, a.plan.slots);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
   const dim3 grid(a.plan.grid);
   const int nbt = (a.batch + 15) / 16;
   const int sl = a.plan.slots;
+  if (a.plan.xlds) {
+    if (nbt == 2) return launch_xlds<2>(a, st);
+    if (nbt == 3) return launch_xlds<3>(a, st);
+    return launch_xlds<4>(a, st);
+  }
   const bool grouped = a.plan.group > 1;
 #define PDA_GEMV(NBT, R) \
   hipLaunchKernelGGL((gemv_kernel<NBT, R>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl)
   switch (nbt) {
-    case 1: PDA_GEMV(1, 1); break;
+    case 1: if (grouped) PDA_GEMV(1, 4); else PDA_GEMV(1, 1); break;
     case 2: if (grouped) PDA_GEMV(2, 2); else PDA_GEMV(2, 1); break;
     case 3: if (grouped) PDA_GEMV(3, 3); else PDA_GEMV(3, 1); break;
     default: if (grouped) PDA_GEMV(4, 4); else PDA_GEMV(4, 1); break;

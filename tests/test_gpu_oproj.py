@@ -47,7 +47,14 @@ def ref(w):
     return oracle.o_proj_residual_norm(w.attn, w.w_o, w.residual, w.norm_w, w.eps)
 
 
-SMALL = [(1, 32, 16), (3, 96, 48), (17, 4096, 2560), (64, 512, 1024), (5, 64, 32768), (33, 8192, 256)]
+SMALL = [(1, 32, 16), (3, 96, 48), (17, 4096, 2560), (64, 512, 1024), (5, 64, 32768), (33, 8192, 256),
+         # one batch tile of more than 4 sequences: four row tiles share each x
+         # fragment when the row tiles divide by four (1040 rows do not)
+         (8, 96, 48), (12, 2048, 1040), (16, 3072, 3072), (9, 1024, 4096),
+         # more than 16 sequences: the thin-GEMM form when the row tiles divide
+         # by 8, otherwise the per-wave form with 2, 3 or 4 row tiles per unit
+         # (1056 rows: 66 tiles; 1088: 68) or one (1040: 65)
+         (32, 256, 1056), (48, 512, 1056), (64, 512, 1088), (40, 1024, 1040), (64, 4096, 4096)]
 
 
 @pytest.mark.parametrize("b,k,h", SMALL, ids=[f"B{c[0]}-K{c[1]}-H{c[2]}" for c in SMALL])
