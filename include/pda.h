@@ -24,7 +24,8 @@
  * Arithmetic: bf16 inputs, fp32 accumulation (scores, running max and sum,
  * the probability-times-value products on bf16 matrix cores with each
  * probability carried as a sum of two bf16 values, ~2^-17 relative), bf16
- * round-to-nearest-even output.
+ * round-to-nearest-even output.  Scores are formed in fp32: scale * q.k must
+ * stay within the fp32 range.
  *
  * Memory: every pointer argument of paged_decode_attention is a DEVICE
  * pointer on the current HIP device.  The caller allocates and owns all of
