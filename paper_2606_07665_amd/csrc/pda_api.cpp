@@ -158,8 +158,7 @@ int heads_per_group(int hkv, int max_waves) {
 // context the page table allows.  Partial slots: one per (workgroup,
 // sequence piece), at most grid + batch * kv-head groups, each holding `cols`
 // (query token, head) rows per kv head.
-Plan make_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus,
-               int cols) {
+Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
   Plan pl;
   const int max_waves = pda::max_waves(d);
   pl.hgs = heads_per_group(hkv, max_waves);
@@ -472,7 +471,7 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
   int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
   if (rc) return rc;
   if (num_cus <= 0) return fail(PDA_ERR_SHAPE, "num_cus must be positive");
-  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus,
+  Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus,
                       pda::kMaxCols);
   *grid_blocks = batch ? pl.grid : 0;
   *waves = batch ? pl.grid * pl.waves : 0;
@@ -492,7 +491,7 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
   int cus = 0;
   if ((rc = device_cus(dev, &cus))) return rc;
   // sized for the most (query token, head) columns, so any num_queries fits
-  Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
+  Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
                       pda::kMaxCols);
   void* ptr = nullptr;
   return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, &ptr);
@@ -705,7 +704,7 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   int cus = 0;
   if ((rc = device_cus(dev, &cus))) return rc;
-  const Plan pl = make_plan(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus, cols);
+  const Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus, cols);
   if (pda::attn_lds_bytes(head_dim, batch, pl.waves, valu_cols > 0) > static_cast<size_t>(pda::kMaxLdsBytes))
     return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has", batch);
   hipStream_t st = static_cast<hipStream_t>(stream);
