@@ -36,7 +36,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="long70b",
                     choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16",
-                             "falcon3", "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
+                             "falcon3", "tokenpage", "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
                              "prelude_falcon3", "oproj_qwen3_4b", "oproj_llama8b", "oproj_70b",
                              "oproj_falcon3", "layer70b", "layer8b", "layer_falcon3"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,

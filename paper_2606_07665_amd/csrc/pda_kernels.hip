@@ -149,15 +149,6 @@ __device__ __forceinline__ u32x4 ld16_stream(__amdgpu_buffer_rsrc_t r, int byte_
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCachePolicyNT);
 }
 
-// physical page of logical page j of a sequence, clamped so that a bad page
-// table entry or a token past the end can never address outside the pool
-__device__ __forceinline__ int page_at(const int32_t* __restrict__ bt_row, int j, int npages,
-                                      int num_pages) {
-  j = j < npages ? j : npages - 1;
-  unsigned p = static_cast<unsigned>(bt_row[j]);
-  return static_cast<int>(p < static_cast<unsigned>(num_pages) ? p : num_pages - 1);
-}
-
 // Workgroup that owns flattened step x of `total`, when `parts` workgroups
 // split [0, total) into ranges [w*total/parts, (w+1)*total/parts).
 __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t parts) {
@@ -393,11 +384,22 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     };
     auto load_pids = [&](int k, int& pa, int& pb) {
       const int t0 = step_of(k) * kStep;
-      int ja = t0 >> page_shift, jb = (t0 + 16) >> page_shift;
-      ja = ja < npages ? ja : npages - 1;
-      jb = jb < npages ? jb : npages - 1;
-      pa = bt_row[ja];
-      pb = bt_row[jb];
+      if constexpr (!kLanePages) {
+        // each 16-token half of the step lies in one page: two ids, wave-uniform
+        int ja = t0 >> page_shift, jb = (t0 + 16) >> page_shift;
+        ja = ja < npages ? ja : npages - 1;
+        jb = jb < npages ? jb : npages - 1;
+        pa = bt_row[ja];
+        pb = bt_row[jb];
+      } else {
+        // pages of fewer than 16 tokens: the step spans 32 / P pages; lane l
+        // holds the id of the step's page l (l mod 32 / P), read by the
+        // lanes that load its rows with a lane shuffle at issue time
+        int j = (t0 >> page_shift) + (lane & ((kStep >> page_shift) - 1));
+        j = j < npages ? j : npages - 1;
+        pa = bt_row[j];
+        pb = 0;
+      }
     };
     auto clamp_pid = [&](int p) {
       const unsigned u = static_cast<unsigned>(uniform(p));
@@ -438,24 +440,20 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
           for (int i = 0; i < S::kLoads; ++i) vv[i] = ld16_stream((S::kRowsPerLoad * i) >> 4 ? rvB : rvA, loff[i]);
         }
       } else {
-        // small pages: every lane looks up the page of its own token
+        // small pages: every lane takes the id of its own token's page from
+        // the lane that loaded it (two steps ahead, in load_pids)
 #pragma unroll
         for (int i = 0; i < S::kLoads; ++i) {
           const int tau = S::kRowsPerLoad * i + vr;
           const int tok = t0 + tau;
-          const int pg = page_at(bt_row, tok >> page_shift, npages, num_pages);
+          const unsigned raw = static_cast<unsigned>(__shfl(pa_raw, tau >> page_shift, 64));
+          const int pg = static_cast<int>(raw < static_cast<unsigned>(num_pages) ? raw : num_pages - 1);
           const int64_t off = pg * page_stride + static_cast<int64_t>(tok & (page - 1)) * tok_stride + 8 * vq;
-          // page_at keeps the address inside the pool; rows past the end are zeroed
-          const bool ok = tok < t0 + live && tok >= lo_seq;
-          const u32x4 zero = {0u, 0u, 0u, 0u};
-          if (which & kIssueK) {
-            const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kg + off));
-            kr[i] = ok ? kv : zero;
-          }
-          if (which & kIssueV) {
-            const u32x4 vv_ = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vg + off));
-            vv[i] = ok ? vv_ : zero;
-          }
+          // the clamp keeps the address inside the pool; rows past the end
+          // are replaced by zeros when staged (a select here would wait for
+          // the load and serialise the step's loads)
+          if (which & kIssueK) kr[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kg + off));
+          if (which & kIssueV) vv[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vg + off));
         }
       }
     };
@@ -466,14 +464,29 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
 
-    // K and V rows of a step -> the tile; rows past the end arrived as zeros
-    // (never NaN * 0 in the P.V product)
-    auto stage_k = [&](const u32x4 (&kr)[S::kLoads]) {
-#pragma unroll
-      for (int i = 0; i < S::kLoads; ++i)
-        *reinterpret_cast<u32x4*>(tile + (S::kRowsPerLoad * i + vr) * S::kKRowBytes + 16 * vq) = kr[i];
+    // K and V rows of the step starting at token t0 -> the tile.  Rows past
+    // the end (and, with a window, before the first key) must be zeros, never
+    // NaN * 0 in the P.V product: with big pages they arrived as zeros; with
+    // small pages they are selected here.
+    auto live_row = [&](int t0, int i) {
+      const int tok = t0 + S::kRowsPerLoad * i + vr;
+      return tok < L && tok >= lo_seq;
     };
-    auto stage_v = [&](const u32x4 (&vv)[S::kLoads]) {
+    auto stage_k = [&](const u32x4 (&kr)[S::kLoads], int t0) {
+#pragma unroll
+      for (int i = 0; i < S::kLoads; ++i) {
+        u32x4 val = kr[i];
+        if constexpr (kLanePages) val = live_row(t0, i) ? val : u32x4{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4*>(tile + (S::kRowsPerLoad * i + vr) * S::kKRowBytes + 16 * vq) = val;
+      }
+    };
+    auto stage_v = [&](const u32x4 (&vv_in)[S::kLoads], int t0) {
+      u32x4 vv[S::kLoads];
+#pragma unroll
+      for (int i = 0; i < S::kLoads; ++i) {
+        vv[i] = vv_in[i];
+        if constexpr (kLanePages) vv[i] = live_row(t0, i) ? vv[i] : u32x4{0u, 0u, 0u, 0u};
+      }
 #pragma unroll
       for (int i = 0; i < S::kLoads; ++i)
         *reinterpret_cast<u32x4*>(tile + S::kVOffset + (S::kRowsPerLoad * i + vr) * S::kVRowBytes + 16 * vq) =
@@ -484,7 +497,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       const int t0 = s * kStep;
       const bool edge = t0 + kStep > hi_min || t0 < lo_max;  // some key of the step is masked
       if constexpr (!S::kOneBuffer) {
-        stage_k(kr);
+        stage_k(kr, t0);
         lds_order();
       }
       // S^T = K Q^T: rows = keys 16T + 4*g4 + i, column = head c; the A operand
@@ -503,7 +516,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       }
       if constexpr (!S::kOneBuffer) {
         lds_order();
-        stage_v(vv);  // over the K rows just read
+        stage_v(vv, t0);  // over the K rows just read
       }
       // online softmax in log2 units
       float sv[2][4];
@@ -689,10 +702,10 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
           // (no traffic); the small-page path would read, so it stops
           const bool next = !kLanePages || k + 1 < nsteps;
           __builtin_amdgcn_s_waitcnt(wait_vector_loads(S::kLoads));  // this step's K
-          stage_k(kA);
+          stage_k(kA, step_of(k) * kStep);
           if (next) issue(k + 1, pa1, pb1, kA, vA, kIssueK);
           __builtin_amdgcn_s_waitcnt(wait_vector_loads(S::kLoads));  // this step's V
-          stage_v(vA);
+          stage_v(vA, step_of(k) * kStep);
           lds_order();
           if (next) issue(k + 1, pa1, pb1, kA, vA, kIssueV);
           if constexpr (kValu)
@@ -717,17 +730,22 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       // streamed with half its loads in flight for the last quarter.  Only
       // the steps that every wave of the workgroup has (nmin) take the
       // barrier, so each wave passes the same number of them.  (The
-      // small-page path, with its per-lane page lookups, would spill.)
+      // small-page path runs ~3% slower with it: its waves already wait on
+      // their page-id shuffles at every issue.)
       const int nmin = kLanePages ? 0 : (s1 - s0) / phases;
+      // (Small pages read their page ids with vector loads, which the wait
+      // for all vector loads would also wait for: they are issued after it.)
       for (; k + 2 < nsteps; k += 2) {
-        load_pids(k + 2, pa0, pb0);
+        if constexpr (!kLanePages) load_pids(k + 2, pa0, pb0);
         __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
         issue(k + 1, pa1, pb1, kB, vB);
+        if constexpr (kLanePages) load_pids(k + 2, pa0, pb0);
         if (k + 2 < nmin) __builtin_amdgcn_s_barrier();
         compute(step_of(k), kA, vA);
-        load_pids(k + 3, pa1, pb1);
+        if constexpr (!kLanePages) load_pids(k + 3, pa1, pb1);
         __builtin_amdgcn_s_waitcnt(kWaitAllVectorLoads);
         issue(k + 2, pa0, pb0, kA, vA);
+        if constexpr (kLanePages) load_pids(k + 3, pa1, pb1);
         if (k + 2 < nmin) __builtin_amdgcn_s_barrier();
         compute(step_of(k + 1), kB, vB);
       }

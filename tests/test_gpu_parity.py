@@ -303,3 +303,8 @@ def test_ragged_sampled(lib):
         picks |= set(int(x) for x in rng.choice(w.batch, 12, replace=False))
         return [(b, int(rng.integers(0, w.num_kv_heads))) for b in sorted(picks)] + [(int(order[-1]), 0)]
     _sampled(lib, "ragged", pairs)
+
+
+def test_tokenpage_sampled(lib):
+    # pages of one token: every row of a step comes from its own page
+    _sampled(lib, "tokenpage", lambda w: [(0, 0), (7, 3), (31, 5), (63, 7), (40, 1)])

@@ -141,9 +141,13 @@ CONFIGS: Dict[str, Config] = {
         "falcon3", 16, 12, 4, 256, 16, 8, "uniform:16:32768", "exact",
         description="Falcon3-7B-shaped layer with head_dim 256, batch 16, 12:4 heads "
                     "(G=3), L~U[16,32768], P=16"),
+    "tokenpage": Config(
+        "tokenpage", 64, 32, 8, 128, 1, 9, "uniform:128:8192", "exact",
+        description="batched with pages of one token (a token-granular cache), "
+                    "batch 64, 32:8 heads, D=128, L~U[128,8192], P=1, shuffled pool"),
 }
 CONFIG_ORDER = ["tiny", "llama8b", "batched", "long70b", "ragged"]
-VARIANT_ORDER = ["window", "multiq", "gqa16", "falcon3"]
+VARIANT_ORDER = ["window", "multiq", "gqa16", "falcon3", "tokenpage"]
 
 
 def window_start(length: int, num_queries: int, window: int) -> int:
