@@ -178,7 +178,8 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   pl.off_acc = 0;
   pl.off_ml = align256(rows * d * 4);
   pl.off_pref = pl.off_ml + align256(rows * 2 * 4);
-  pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1) * 4);
+  // steps prefix [batch + 1], then the split list [grid] (see the kernels)
+  pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1 + pl.grid) * 4);
   return pl;
 }
 

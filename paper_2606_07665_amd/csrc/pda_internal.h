@@ -27,7 +27,7 @@ struct LaunchArgs {
   uint16_t* out;
   float* ws_acc;      // [slots, hgs, nq * group, head_dim] partial accumulators
   float* ws_ml;       // [slots, hgs, nq * group, 2] partial (max in log2 units, sum)
-  int32_t* ws_pref;   // [batch + 1] steps prefix, written by the attention kernel
+  int32_t* ws_pref;   // [batch + 1] steps prefix, then [grid] split list, written by the attention kernel
   int batch, hq, hkv, group, head_dim, page_shift, num_pages, maxp;
   int hgs;            // kv heads per workgroup (a divisor of hkv, at most max_waves(head_dim))
   int waves;          // waves per workgroup: hgs x step phases

@@ -289,13 +289,23 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   const int vMi = kNC == 8 ? vd4 : (vd3 | vd4 << 1);
   const int qjv = vMh < ncols ? vMh / group : nq - 1;  // query token of the lane's column
 
+  // ws_split[blk]: the (sequence, kv-head group) whose first split point
+  // is this workgroup's start, else -1 -- the list of pieces to merge when
+  // the batch has more sequences than workgroups (merge_kernel<.., true>)
+  int32_t* ws_split = ws_pref + batch + 1;
+  const int blk = blockIdx.x;
   const int64_t total = static_cast<int64_t>(pref[batch]) * ngroups;
-  if (total == 0) return;
+  if (total == 0) {
+    if (tid == 0) ws_split[blk] = -1;
+    return;
+  }
   const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
   int64_t beff = (total + per_block_min - 1) / per_block_min;
   beff = beff < gridDim.x ? beff : gridDim.x;
-  const int blk = blockIdx.x;
-  if (blk >= beff) return;
+  if (blk >= beff) {
+    if (tid == 0) ws_split[blk] = -1;
+    return;
+  }
   int64_t x = (static_cast<int64_t>(blk) * total) / beff;
   const int64_t xend = (static_cast<int64_t>(blk + 1) * total) / beff;
 
@@ -314,6 +324,8 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   int rel = static_cast<int>(x - static_cast<int64_t>(uniform(pref[b])) * ngroups);
   int hg = rel / nb;
   int s0 = rel - hg * nb;
+  // a sequence split across workgroups w0 .. w1 is listed once, by w0 + 1
+  if (tid == 0) ws_split[blk] = (s0 > 0 && owner_of(x - s0, total, beff) == blk - 1) ? b * ngroups + hg : -1;
 
   unsigned char* tile = smem + wid * S::kTileBytes;
   const int vr = lane / S::kChunks;   // row within one wave load (K and V alike)
@@ -880,7 +892,11 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
 // pieces, float4 column); kPG piece groups are folded through LDS.  kPG = 8
 // suits plans where a sequence spans many workgroups (long contexts), kPG = 1
 // plans where it spans a few (then a workgroup covers more heads).
-template <int D, int kPG>
+// kBySplit: the grid runs over the attention workgroups instead of the
+// sequences, workgroup j merging the sequence listed in ws_split[j] (if
+// any), for batches with more sequences than attention workgroups, where
+// most sequences are whole and a grid over all of them only returns.
+template <int D, int kPG, bool kBySplit = false>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
     uint16_t* __restrict__ out, const float* __restrict__ ws_acc, const float* __restrict__ ws_ml,
     const int32_t* __restrict__ ws_pref, int batch, int hq, int hkv, int group, int hgs, int min_steps,
@@ -895,8 +911,12 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   const int ncols = group * nq;   // (query token, head) columns per kv head
   const int heads = hgs * ncols;  // query rows of one kv-head group
   const int chunks = (heads + kHPB - 1) / kHPB;
-  const int e = blockIdx.x / chunks;
+  int e = blockIdx.x / chunks;
   const int chunk = blockIdx.x - e * chunks;
+  if constexpr (kBySplit) {
+    e = ws_pref[batch + 1 + e];  // ws_split
+    if (e < 0) return;
+  }
   const int b = e / ngroups;
   const int hg = e - b * ngroups;
   const int nb = ws_pref[b + 1] - ws_pref[b];
@@ -1004,13 +1024,13 @@ hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
   return lane_pages ? launch_attn<64, true>(a, st) : launch_attn<64, false>(a, st);
 }
 
-template <int D, int kPG>
+template <int D, int kPG, bool kBySplit = false>
 static hipError_t launch_merge(const LaunchArgs& a, hipStream_t st) {
   constexpr int kHPB = kMergeThreads / (kPG * (D / 4));
   const int heads = a.hgs * a.group * a.nq;
   const int chunks = (heads + kHPB - 1) / kHPB;
-  const dim3 grid(a.batch * (a.hkv / a.hgs) * chunks);
-  hipLaunchKernelGGL((merge_kernel<D, kPG>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml,
+  const dim3 grid((kBySplit ? a.grid : a.batch * (a.hkv / a.hgs)) * chunks);
+  hipLaunchKernelGGL((merge_kernel<D, kPG, kBySplit>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml,
                      a.ws_pref, a.batch, a.hq, a.hkv, a.group, a.hgs, a.min_steps, a.waves / a.hgs, a.grid,
                      a.nq);
   return hipGetLastError();
@@ -1020,9 +1040,14 @@ hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
   // expected pieces per split sequence: workgroups per kv-head-group sequence
   const int64_t seqs = static_cast<int64_t>(a.batch) * (a.hkv / a.hgs);
   const bool many = a.grid >= 8 * seqs;
-  if (a.head_dim == 128) return many ? launch_merge<128, 8>(a, st) : launch_merge<128, 1>(a, st);
-  if (a.head_dim == 256) return many ? launch_merge<256, 4>(a, st) : launch_merge<256, 1>(a, st);
-  return many ? launch_merge<64, 8>(a, st) : launch_merge<64, 1>(a, st);
+  // more sequences than attention workgroups: at most one split sequence
+  // per workgroup boundary, listed by the attention kernel
+  const bool by_split = seqs > a.grid;
+  if (a.head_dim == 128)
+    return many ? launch_merge<128, 8>(a, st) : by_split ? launch_merge<128, 1, true>(a, st) : launch_merge<128, 1>(a, st);
+  if (a.head_dim == 256)
+    return many ? launch_merge<256, 4>(a, st) : by_split ? launch_merge<256, 1, true>(a, st) : launch_merge<256, 1>(a, st);
+  return many ? launch_merge<64, 8>(a, st) : by_split ? launch_merge<64, 1, true>(a, st) : launch_merge<64, 1>(a, st);
 }
 
 size_t attn_lds_bytes(int head_dim, int batch, int waves, bool valu) {
