@@ -1,0 +1,209 @@
+/*
+ * A plain C client of the library: the C ABI of include/pda.h as an engine
+ * written in C would use it, with device memory and streams from the HIP
+ * runtime's C API and no Python or torch anywhere.
+ *
+ *   pda_client errors     argument checks that return before any HIP call
+ *                         (runs without a GPU); prints "ok <check>" lines
+ *   pda_client run DIR    decode attention on the device: reads DIR/meta.txt
+ *                         ("batch hq hkv head_dim page_size num_pages maxp
+ *                         scale") and the raw little-endian arrays DIR/q.bin,
+ *                         k.bin, v.bin (bf16 bits), bt.bin and lens.bin
+ *                         (int32); runs the call on a created stream after
+ *                         reserving its workspace, and again on the null
+ *                         stream, checks that both outputs are bitwise
+ *                         equal, and writes the first to DIR/out.bin
+ *
+ * Exit status 0 when every check holds.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "pda.h"
+
+static int failures = 0;
+
+static void expect(const char* what, int got, int want) {
+  if (got == want) {
+    printf("ok %s\n", what);
+  } else {
+    printf("FAIL %s: status %d, expected %d (%s)\n", what, got, want, pda_last_error());
+    ++failures;
+  }
+}
+
+static int run_errors(void) {
+  /* Any 16-byte aligned non-NULL address: these calls must reject their
+     arguments before touching memory or the device. */
+  void* p = (void*)(uintptr_t)0x1000;
+  const int32_t* ip = (const int32_t*)p;
+  expect("null q", paged_decode_attention(NULL, p, p, ip, ip, p, 2, 32, 8, 128, 16, 64, 8, 0.088f, NULL),
+         PDA_ERR_NULL);
+  if (failures == 0 && strlen(pda_last_error()) == 0) {
+    printf("FAIL empty error message\n");
+    ++failures;
+  }
+  expect("head_dim 96", paged_decode_attention(p, p, p, ip, ip, p, 2, 32, 8, 96, 16, 64, 8, 0.088f, NULL),
+         PDA_ERR_UNSUPPORTED);
+  expect("group 32", paged_decode_attention(p, p, p, ip, ip, p, 2, 64, 2, 128, 16, 64, 8, 0.088f, NULL),
+         PDA_ERR_UNSUPPORTED);
+  expect("heads not a multiple", paged_decode_attention(p, p, p, ip, ip, p, 2, 30, 8, 128, 16, 64, 8, 0.088f, NULL),
+         PDA_ERR_SHAPE);
+  expect("misaligned q",
+         paged_decode_attention((void*)(uintptr_t)0x1008, p, p, ip, ip, p, 2, 32, 8, 128, 16, 64, 8, 0.088f, NULL),
+         PDA_ERR_ALIGN);
+  expect("nan scale", paged_decode_attention(p, p, p, ip, ip, p, 2, 32, 8, 128, 16, 64, 8, nanf(""), NULL),
+         PDA_ERR_SCALE);
+  expect("empty batch", paged_decode_attention(NULL, NULL, NULL, NULL, NULL, NULL, 0, 32, 8, 128, 16, 64, 8, 0.088f,
+                                               NULL),
+         PDA_OK);
+  if (strlen(pda_last_error()) != 0) {
+    printf("FAIL error message not cleared by a successful call\n");
+    ++failures;
+  }
+  expect("version", pda_version(), PDA_VERSION);
+
+  int32_t grid = 0, waves = 0;
+  int64_t ws = 0;
+  expect("plan", pda_plan(4, 64, 8, 128, 16, 8192, 256, &grid, &waves, &ws), PDA_OK);
+  if (grid != 256 || waves != 256 * 8 || ws <= 0) {
+    printf("FAIL plan: grid %d waves %d workspace %lld\n", grid, waves, (long long)ws);
+    ++failures;
+  } else {
+    printf("ok plan shape: grid %d waves %d workspace %lld\n", grid, waves, (long long)ws);
+  }
+  return failures ? 1 : 0;
+}
+
+#define HIP_OK(call)                                                              \
+  do {                                                                            \
+    hipError_t e_ = (call);                                                       \
+    if (e_ != hipSuccess) {                                                       \
+      fprintf(stderr, "%s failed: %s\n", #call, hipGetErrorString(e_));          \
+      exit(2);                                                                    \
+    }                                                                             \
+  } while (0)
+
+/* Reads DIR/name into a new host buffer of exactly `bytes` bytes. */
+static void* read_file(const char* dir, const char* name, size_t bytes) {
+  char path[4096];
+  snprintf(path, sizeof path, "%s/%s", dir, name);
+  FILE* f = fopen(path, "rb");
+  if (!f) {
+    fprintf(stderr, "cannot open %s\n", path);
+    exit(2);
+  }
+  void* buf = malloc(bytes ? bytes : 1);
+  if (!buf || fread(buf, 1, bytes, f) != bytes || fgetc(f) != EOF) {
+    fprintf(stderr, "%s does not hold %zu bytes\n", path, bytes);
+    exit(2);
+  }
+  fclose(f);
+  return buf;
+}
+
+static void* to_device(const void* host, size_t bytes) {
+  void* dev = NULL;
+  HIP_OK(hipMalloc(&dev, bytes ? bytes : 16));
+  if (bytes) HIP_OK(hipMemcpy(dev, host, bytes, hipMemcpyHostToDevice));
+  return dev;
+}
+
+static int run_device(const char* dir) {
+  char path[4096];
+  snprintf(path, sizeof path, "%s/meta.txt", dir);
+  FILE* f = fopen(path, "r");
+  if (!f) {
+    fprintf(stderr, "cannot open %s\n", path);
+    return 2;
+  }
+  int batch, hq, hkv, d, page, num_pages, maxp;
+  float scale;
+  if (fscanf(f, "%d %d %d %d %d %d %d %f", &batch, &hq, &hkv, &d, &page, &num_pages, &maxp, &scale) != 8) {
+    fprintf(stderr, "bad meta.txt\n");
+    return 2;
+  }
+  fclose(f);
+  const size_t q_bytes = (size_t)batch * hq * d * 2;
+  const size_t kv_bytes = (size_t)num_pages * page * hkv * d * 2;
+  const size_t bt_bytes = (size_t)batch * maxp * 4;
+  const size_t lens_bytes = (size_t)batch * 4;
+
+  void* hq_ = read_file(dir, "q.bin", q_bytes);
+  void* hk = read_file(dir, "k.bin", kv_bytes);
+  void* hv = read_file(dir, "v.bin", kv_bytes);
+  void* hbt = read_file(dir, "bt.bin", bt_bytes);
+  void* hlens = read_file(dir, "lens.bin", lens_bytes);
+  void* q = to_device(hq_, q_bytes);
+  void* k = to_device(hk, kv_bytes);
+  void* v = to_device(hv, kv_bytes);
+  int32_t* bt = (int32_t*)to_device(hbt, bt_bytes);
+  int32_t* lens = (int32_t*)to_device(hlens, lens_bytes);
+  void* out1 = NULL;
+  void* out2 = NULL;
+  HIP_OK(hipMalloc(&out1, q_bytes));
+  HIP_OK(hipMalloc(&out2, q_bytes));
+  HIP_OK(hipMemset(out1, 0xFF, q_bytes)); /* NaN bf16 bits: every row must be written */
+  HIP_OK(hipMemset(out2, 0xFF, q_bytes));
+
+  hipStream_t st;
+  HIP_OK(hipStreamCreate(&st));
+  expect("workspace reserve", pda_workspace_reserve(batch, hq, hkv, d, page, maxp, st), PDA_OK);
+  expect("attention on a stream",
+         paged_decode_attention(q, k, v, bt, lens, out1, batch, hq, hkv, d, page, num_pages, maxp, scale, st),
+         PDA_OK);
+  expect("attention on the null stream",
+         paged_decode_attention(q, k, v, bt, lens, out2, batch, hq, hkv, d, page, num_pages, maxp, scale, NULL),
+         PDA_OK);
+  HIP_OK(hipStreamSynchronize(st));
+  HIP_OK(hipDeviceSynchronize());
+
+  unsigned char* o1 = (unsigned char*)malloc(q_bytes);
+  unsigned char* o2 = (unsigned char*)malloc(q_bytes);
+  if (!o1 || !o2) return 2;
+  HIP_OK(hipMemcpy(o1, out1, q_bytes, hipMemcpyDeviceToHost));
+  HIP_OK(hipMemcpy(o2, out2, q_bytes, hipMemcpyDeviceToHost));
+  if (memcmp(o1, o2, q_bytes) != 0) {
+    printf("FAIL the two streams' outputs differ\n");
+    ++failures;
+  } else {
+    printf("ok outputs bitwise equal across streams\n");
+  }
+  snprintf(path, sizeof path, "%s/out.bin", dir);
+  f = fopen(path, "wb");
+  if (!f || fwrite(o1, 1, q_bytes, f) != q_bytes) {
+    fprintf(stderr, "cannot write %s\n", path);
+    return 2;
+  }
+  fclose(f);
+
+  expect("release workspaces", pda_release_workspaces(), PDA_OK);
+  HIP_OK(hipStreamDestroy(st));
+  HIP_OK(hipFree(q));
+  HIP_OK(hipFree(k));
+  HIP_OK(hipFree(v));
+  HIP_OK(hipFree(bt));
+  HIP_OK(hipFree(lens));
+  HIP_OK(hipFree(out1));
+  HIP_OK(hipFree(out2));
+  free(hq_);
+  free(hk);
+  free(hv);
+  free(hbt);
+  free(hlens);
+  free(o1);
+  free(o2);
+  return failures ? 1 : 0;
+}
+
+int main(int argc, char** argv) {
+  if (argc == 2 && strcmp(argv[1], "errors") == 0) return run_errors();
+  if (argc == 3 && strcmp(argv[1], "run") == 0) return run_device(argv[2]);
+  fprintf(stderr, "usage: %s errors | run DIR\n", argv[0]);
+  return 2;
+}
