@@ -308,3 +308,31 @@ def test_ragged_sampled(lib):
 def test_tokenpage_sampled(lib):
     # pages of one token: every row of a step comes from its own page
     _sampled(lib, "tokenpage", lambda w: [(0, 0), (7, 3), (31, 5), (63, 7), (40, 1)])
+
+
+@pytest.mark.parametrize("p", [1, 4])
+def test_small_pages_pool_over_2gib(lib, p):
+    # a pool of more than 2 GiB takes the small-page path's 64-bit
+    # addresses: the workload's pages are moved past the 2 GiB mark of a
+    # larger, otherwise unwritten pool (rows past a sequence's end in its
+    # last page hold whatever that memory holds and must not leak in)
+    import torch
+    w = W.build([1, 5, 33, 300, 1000], 32, 8, 128, p, seed=40 + p, pool="holes:0.2", poison=True)
+    page_bytes = p * 8 * 128 * 2
+    big = (int(2.3 * 2 ** 30) // page_bytes) + w.k_cache.shape[0]
+    shift = big - w.k_cache.shape[0]
+    assert shift * page_bytes > 2 ** 31
+    log(f"small pages P={p}: pool of {big} pages ({big * page_bytes / 2 ** 30:.2f} GiB each for K and V)")
+    dev = to_gpu(w)
+    kb = torch.empty((big,) + tuple(dev["k"].shape[1:]), dtype=torch.bfloat16, device="cuda")
+    vb = torch.empty_like(kb)
+    kb[shift:] = dev["k"]
+    vb[shift:] = dev["v"]
+    bt = torch.where(dev["bt"] >= 0, dev["bt"] + shift, dev["bt"])
+    out = torch.full(tuple(w.q.shape), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lib.paged_decode_attention(dev["q"], kb, vb, bt, dev["lens"], out, float(w.scale))
+    torch.cuda.synchronize()
+    got = out.float().cpu().numpy().astype(np.float64)
+    del kb, vb
+    torch.cuda.empty_cache()
+    check(got, ref(w), f"P={p} pool over 2 GiB")
