@@ -329,10 +329,22 @@ __device__ __forceinline__ float gemv_result(const float* __restrict__ part, con
   const int t = row >> 4;
   const int g = t / p.group;
   const int i = t - g * p.group;
-  const int64_t x0 = static_cast<int64_t>(g) * p.kt_count;
-  const int64_t first = ((x0 + 1) * p.blocks - 1) / p.units;
-  const int64_t last = ((x0 + p.kt_count) * p.blocks - 1) / p.units;
-  const int cnt = static_cast<int>(last - first + 1);  // at most kGemvMaxSlots (plan_gemv)
+  // workgroups whose unit ranges meet group g's: at most kGemvMaxSlots
+  // (plan_gemv).  In 32-bit arithmetic when every product below fits (a
+  // uniform branch; on 256 CUs every supported shape does), since each
+  // 64-bit division is a long instruction sequence and an epilogue lane
+  // computes this for every row it owns
+  int cnt;
+  if (((p.units * p.blocks) >> 32) == 0) {
+    const uint32_t x0 = static_cast<uint32_t>(g) * p.kt_count;
+    const uint32_t nb = static_cast<uint32_t>(p.blocks), nu = static_cast<uint32_t>(p.units);
+    cnt = static_cast<int>(((x0 + p.kt_count) * nb - 1) / nu - ((x0 + 1) * nb - 1) / nu + 1);
+  } else {
+    const int64_t x0 = static_cast<int64_t>(g) * p.kt_count;
+    const int64_t first = ((x0 + 1) * p.blocks - 1) / p.units;
+    const int64_t last = ((x0 + p.kt_count) * p.blocks - 1) / p.units;
+    cnt = static_cast<int>(last - first + 1);
+  }
   const int64_t slot_floats = static_cast<int64_t>(p.group) * batch * kTileRows;
   const float* q = part + static_cast<int64_t>(g) * p.slots * slot_floats + (static_cast<int64_t>(i) * batch + b) * kTileRows +
                    (row & 15);
