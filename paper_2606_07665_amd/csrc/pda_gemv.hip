@@ -323,38 +323,53 @@ __global__ __launch_bounds__(kXWaves * 64, 1) void gemv_xlds_kernel(
   }
 }
 
-// y[b][row]: the sum, in wave order, of the partials of row's group.
-__device__ __forceinline__ float gemv_result(const float* __restrict__ part, const GemvPlan& p, int batch, int b,
-                                             int row) {
-  const int t = row >> 4;
-  const int g = t / p.group;
-  const int i = t - g * p.group;
-  // workgroups whose unit ranges meet group g's: at most kGemvMaxSlots
-  // (plan_gemv).  In 32-bit arithmetic when every product below fits (a
-  // uniform branch; on 256 CUs every supported shape does), since each
-  // 64-bit division is a long instruction sequence and an epilogue lane
-  // computes this for every row it owns
-  int cnt;
+// y[b][rows[r]] for kRows rows: for each, the sum in workgroup order of the
+// partials of its row group (kSlots >= the plan's slots, the most
+// workgroups that touch one group).  All partial counts are worked out
+// first, under one uniform branch (32-bit arithmetic when every product
+// fits, as on 256 CUs for every supported shape; each 64-bit division is a
+// long instruction sequence), then every load is issued unconditionally:
+// slots past a group's count re-read its last slot and are dropped by a
+// select after the load.  As `j < cnt ? load : 0`, each load sat behind a
+// branch of its own and a lane waited for one row's partials before it
+// requested the next row's.
+template <int kSlots, int kRows>
+__device__ __forceinline__ void gemv_rows(const float* __restrict__ part, const GemvPlan& p, int batch, int b,
+                                          const int (&rows)[kRows], float (&y)[kRows]) {
+  int g[kRows], cnt[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) g[r] = (rows[r] >> 4) / p.group;
   if (((p.units * p.blocks) >> 32) == 0) {
-    const uint32_t x0 = static_cast<uint32_t>(g) * p.kt_count;
     const uint32_t nb = static_cast<uint32_t>(p.blocks), nu = static_cast<uint32_t>(p.units);
-    cnt = static_cast<int>(((x0 + p.kt_count) * nb - 1) / nu - ((x0 + 1) * nb - 1) / nu + 1);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      const uint32_t x0 = static_cast<uint32_t>(g[r]) * p.kt_count;
+      cnt[r] = static_cast<int>(((x0 + p.kt_count) * nb - 1) / nu - ((x0 + 1) * nb - 1) / nu + 1);
+    }
   } else {
-    const int64_t x0 = static_cast<int64_t>(g) * p.kt_count;
-    const int64_t first = ((x0 + 1) * p.blocks - 1) / p.units;
-    const int64_t last = ((x0 + p.kt_count) * p.blocks - 1) / p.units;
-    cnt = static_cast<int>(last - first + 1);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      const int64_t x0 = static_cast<int64_t>(g[r]) * p.kt_count;
+      cnt[r] = static_cast<int>(((x0 + p.kt_count) * p.blocks - 1) / p.units - ((x0 + 1) * p.blocks - 1) / p.units + 1);
+    }
   }
   const int64_t slot_floats = static_cast<int64_t>(p.group) * batch * kTileRows;
-  const float* q = part + static_cast<int64_t>(g) * p.slots * slot_floats + (static_cast<int64_t>(i) * batch + b) * kTileRows +
-                   (row & 15);
-  float v[kGemvMaxSlots];
+  float v[kRows][kSlots];
 #pragma unroll
-  for (int j = 0; j < kGemvMaxSlots; ++j) v[j] = j < cnt ? q[j * slot_floats] : 0.f;
-  float s = 0.f;
+  for (int r = 0; r < kRows; ++r) {
+    const int i = (rows[r] >> 4) - g[r] * p.group;
+    const float* q = part + static_cast<int64_t>(g[r]) * p.slots * slot_floats +
+                     (static_cast<int64_t>(i) * batch + b) * kTileRows + (rows[r] & 15);
 #pragma unroll
-  for (int j = 0; j < kGemvMaxSlots; ++j) s += v[j];
-  return s;
+    for (int j = 0; j < kSlots; ++j) v[r][j] = q[(j < cnt[r] ? j : cnt[r] - 1) * slot_floats];
+  }
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < kSlots; ++j) s += j < cnt[r] ? v[r][j] : 0.f;
+    y[r] = s;
+  }
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
@@ -367,7 +382,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 
 // One wave per (sequence b, head h) of the projection: h < hq is a q head,
 // then hkv k heads, then hkv v heads.  Lane owns elements lane + 64 j.
-template <int D>
+template <int D, int kSlots>
 __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
   constexpr int E = D / 64;
   __shared__ float s[D];
@@ -377,15 +392,46 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
   const int lane = threadIdx.x;
   const bool is_q = h < a.hq;
   const bool is_k = !is_q && h < a.hq + a.hkv;
+  const uint16_t* nw = is_q ? a.q_norm : (is_k ? a.k_norm : nullptr);
 
+  // Everything the wave reads is requested before any of it is used: the
+  // length, then (for an append) the page id of the new token's slot, the
+  // partials, the bias and the norm weights.
+  const int L = a.lens[b];
+  const int pos = L > 0 ? L - 1 : 0;
+  const bool kv_head = !is_q;
+  const int g = kv_head ? (is_k ? h - a.hq : h - a.hq - a.hkv) : 0;
+  uint16_t* cache = kv_head ? (is_k ? a.k_cache : a.v_cache) : nullptr;
+  int64_t row = 0;
+  if (cache) {
+    const int max_ctx = a.maxp << a.page_shift;
+    const int Lc = L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
+    if (Lc == 0) {
+      cache = nullptr;  // no token in this slot: nothing to append
+    } else {
+      const int t = Lc - 1;
+      const unsigned raw = static_cast<unsigned>(a.bt[static_cast<int64_t>(b) * a.maxp + (t >> a.page_shift)]);
+      const int64_t page = raw < static_cast<unsigned>(a.num_pages) ? raw : a.num_pages - 1;
+      row = (((page << a.page_shift) + (t & ((1 << a.page_shift) - 1))) * a.hkv + g) * D;
+    }
+  }
+  // bias and norm weights are loaded whether present or not (from the
+  // partials, a valid address, when absent; dropped by a select), so that
+  // no load waits behind a branch
+  const uint16_t* bias_p = a.bias ? a.bias + h * D : reinterpret_cast<const uint16_t*>(a.part);
+  const uint16_t* nw_p = nw ? nw : reinterpret_cast<const uint16_t*>(a.part);
+  int rows[E];
   float v[E];
+  uint16_t bias_h[E], wn_h[E];
 #pragma unroll
   for (int j = 0; j < E; ++j) {
-    const int e = lane + 64 * j;
-    v[j] = gemv_result(a.part, a.plan, a.batch, b, h * D + e);
-    if (a.bias) v[j] += bf16_to_f32(a.bias[h * D + e]);
+    rows[j] = h * D + lane + 64 * j;
+    bias_h[j] = bias_p[lane + 64 * j];
+    wn_h[j] = nw_p[lane + 64 * j];
   }
-  const uint16_t* nw = is_q ? a.q_norm : (is_k ? a.k_norm : nullptr);
+  gemv_rows<kSlots>(a.part, a.plan, a.batch, b, rows, v);
+#pragma unroll
+  for (int j = 0; j < E; ++j) v[j] += a.bias ? bf16_to_f32(bias_h[j]) : 0.f;
   if (nw) {
     float ss = 0.f;
 #pragma unroll
@@ -394,10 +440,8 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
     for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
     const float inv = rsqrtf(ss / D + a.eps);
 #pragma unroll
-    for (int j = 0; j < E; ++j) v[j] = v[j] * inv * bf16_to_f32(nw[lane + 64 * j]);
+    for (int j = 0; j < E; ++j) v[j] = v[j] * inv * bf16_to_f32(wn_h[j]);
   }
-  const int L = a.lens[b];
-  const int pos = L > 0 ? L - 1 : 0;
   if ((is_q || is_k) && a.rotary_dim > 0) {
 #pragma unroll
     for (int j = 0; j < E; ++j) s[lane + 64 * j] = v[j];
@@ -434,27 +478,11 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
 
   // outputs: q to q_out; k and v to k_out / v_out and, with a cache, to the page slot
   uint16_t* dst = nullptr;
-  uint16_t* cache = nullptr;
-  int64_t row = 0;
   if (is_q) {
     dst = a.q_out + (static_cast<int64_t>(b) * a.hq + h) * D;
   } else {
-    const int g = is_k ? h - a.hq : h - a.hq - a.hkv;
     uint16_t* out = is_k ? a.k_out : a.v_out;
     if (out) dst = out + (static_cast<int64_t>(b) * a.hkv + g) * D;
-    cache = is_k ? a.k_cache : a.v_cache;
-    if (cache) {
-      const int max_ctx = a.maxp << a.page_shift;
-      const int Lc = L < 0 ? 0 : (L > max_ctx ? max_ctx : L);
-      if (Lc == 0) {
-        cache = nullptr;  // no token in this slot: nothing to append
-      } else {
-        const int t = Lc - 1;
-        const unsigned raw = static_cast<unsigned>(a.bt[static_cast<int64_t>(b) * a.maxp + (t >> a.page_shift)]);
-        const int64_t page = raw < static_cast<unsigned>(a.num_pages) ? raw : a.num_pages - 1;
-        row = (((page << a.page_shift) + (t & ((1 << a.page_shift) - 1))) * a.hkv + g) * D;
-      }
-    }
   }
 #pragma unroll
   for (int j = 0; j < E; ++j) {
@@ -468,6 +496,7 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
 // per thread: z = y + residual (fp32 to scratch, bf16 to residual_out) and
 // the chunk's sum of z^2 (fixed reduction order).  residual_out may be the
 // residual buffer: each feature is read and written by the same thread.
+template <int kSlots>
 __global__ __launch_bounds__(kOProjChunk) void oproj_residual_kernel(OProjArgs a) {
   __shared__ float wsum[kOProjChunk / 64];
   const int chunks = oproj_chunks(a.hidden);
@@ -477,7 +506,10 @@ __global__ __launch_bounds__(kOProjChunk) void oproj_residual_kernel(OProjArgs a
   const int64_t at = static_cast<int64_t>(b) * a.hidden + n;
   float z = 0.f;
   if (n < a.hidden) {
-    z = gemv_result(a.part, a.plan, a.batch, b, n) + bf16_to_f32(a.residual[at]);
+    const int rows[1] = {n};
+    float y[1];
+    gemv_rows<kSlots>(a.part, a.plan, a.batch, b, rows, y);
+    z = y[0] + bf16_to_f32(a.residual[at]);
     a.z[at] = z;
     a.residual_out[at] = f32_to_bf16(z);
   }
@@ -512,10 +544,34 @@ __global__ __launch_bounds__(kOProjChunk) void oproj_norm_kernel(OProjArgs a) {
 
 }  // namespace
 
+// Instantiations of the epilogues by the plan's partial slots per group.
+template <int kSlots>
+hipError_t launch_oproj_residual(const OProjArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((oproj_residual_kernel<kSlots>), dim3(a.batch * oproj_chunks(a.hidden)), dim3(kOProjChunk), 0,
+                     st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_prelude(const PreludeArgs& a, hipStream_t st) {
+  const dim3 grid(a.batch * (a.hq + 2 * a.hkv));
+  if (a.plan.slots <= 4)
+    hipLaunchKernelGGL((prelude_epilogue<D, 4>), grid, dim3(64), 0, st, a);
+  else if (a.plan.slots <= 8)
+    hipLaunchKernelGGL((prelude_epilogue<D, 8>), grid, dim3(64), 0, st, a);
+  else if (a.plan.slots <= 12)
+    hipLaunchKernelGGL((prelude_epilogue<D, 12>), grid, dim3(64), 0, st, a);
+  else
+    hipLaunchKernelGGL((prelude_epilogue<D, kGemvMaxSlots>), grid, dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_oproj_epilogue(const OProjArgs& a, hipStream_t st) {
   const dim3 grid(a.batch * oproj_chunks(a.hidden));
-  hipLaunchKernelGGL(oproj_residual_kernel, grid, dim3(kOProjChunk), 0, st, a);
-  hipError_t e = hipGetLastError();
+  const hipError_t e = a.plan.slots <= 4   ? launch_oproj_residual<4>(a, st)
+                       : a.plan.slots <= 8  ? launch_oproj_residual<8>(a, st)
+                       : a.plan.slots <= 12 ? launch_oproj_residual<12>(a, st)
+                                            : launch_oproj_residual<kGemvMaxSlots>(a, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(oproj_norm_kernel, grid, dim3(kOProjChunk), 0, st, a);
   return hipGetLastError();
@@ -643,14 +699,9 @@ hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_prelude_epilogue(const PreludeArgs& a, hipStream_t st) {
-  const dim3 grid(a.batch * (a.hq + 2 * a.hkv));
-  if (a.d == 64)
-    hipLaunchKernelGGL((prelude_epilogue<64>), grid, dim3(64), 0, st, a);
-  else if (a.d == 128)
-    hipLaunchKernelGGL((prelude_epilogue<128>), grid, dim3(64), 0, st, a);
-  else
-    hipLaunchKernelGGL((prelude_epilogue<256>), grid, dim3(64), 0, st, a);
-  return hipGetLastError();
+  if (a.d == 64) return launch_prelude<64>(a, st);
+  if (a.d == 128) return launch_prelude<128>(a, st);
+  return launch_prelude<256>(a, st);
 }
 
 }  // namespace pda
