@@ -534,12 +534,17 @@ __global__ __launch_bounds__(kOProjChunk) void oproj_norm_kernel(OProjArgs a) {
   const int c = blockIdx.x - b * chunks;
   const int n = c * kOProjChunk + threadIdx.x;
   if (n >= a.hidden) return;
+  // z and the weight are requested before the chunk sums (scalar loads,
+  // eight in flight at a time), whose latency hides theirs
+  const int64_t at = static_cast<int64_t>(b) * a.hidden + n;
+  const float z = a.z[at];
+  const float w = bf16_to_f32(a.norm_w[n]);
   const float* ss = a.chunk_ss + static_cast<int64_t>(b) * chunks;
   float tot = 0.f;
+#pragma unroll 8
   for (int i = 0; i < chunks; ++i) tot += ss[i];
   const float inv = rsqrtf(tot / a.hidden + a.eps);
-  const int64_t at = static_cast<int64_t>(b) * a.hidden + n;
-  a.normed_out[at] = f32_to_bf16(a.z[at] * inv * bf16_to_f32(a.norm_w[n]));
+  a.normed_out[at] = f32_to_bf16(z * inv * w);
 }
 
 }  // namespace
