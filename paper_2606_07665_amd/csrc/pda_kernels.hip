@@ -919,16 +919,22 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   }
   const int b = e / ngroups;
   const int hg = e - b * ngroups;
-  const int nb = ws_pref[b + 1] - ws_pref[b];
-  if (nb == 0) return;  // zero row written by the attention kernel
-  const int64_t total = static_cast<int64_t>(ws_pref[batch]) * ngroups;
+  // The three prefix entries are requested together and the one early
+  // return needs all of them (with a return on nb == 0 first, the total
+  // was requested only once nb had arrived: one more dependent load).
+  const int pb0 = ws_pref[b], pb1 = ws_pref[b + 1], pbt = ws_pref[batch];
+  const int nb = pb1 - pb0;
+  int64_t total = static_cast<int64_t>(pbt) * ngroups;
+  total = total > 0 ? total : 1;  // an all-empty batch returns below (nb == 0)
   const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
   int64_t beff = (total + per_block_min - 1) / per_block_min;
   beff = beff < grid_blocks ? beff : grid_blocks;
-  const int64_t x0 = static_cast<int64_t>(ws_pref[b]) * ngroups + static_cast<int64_t>(hg) * nb;
+  const int64_t x0 = static_cast<int64_t>(pb0) * ngroups + static_cast<int64_t>(hg) * nb;
   const int64_t w0 = owner_of(x0, total, beff);
-  const int64_t w1 = owner_of(x0 + nb - 1, total, beff);
-  if (w0 == w1) return;  // one workgroup covered the sequence and wrote it
+  const int64_t w1 = owner_of(x0 + (nb > 0 ? nb : 1) - 1, total, beff);
+  // an empty sequence (its zero row written by the attention kernel), or one
+  // that a single workgroup covered and wrote
+  if (nb == 0 || w0 == w1) return;
 
   const int tid = threadIdx.x;
   const int hs = tid / (kPG * kCols);
