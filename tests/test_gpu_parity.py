@@ -310,19 +310,20 @@ def test_tokenpage_sampled(lib):
     _sampled(lib, "tokenpage", lambda w: [(0, 0), (7, 3), (31, 5), (63, 7), (40, 1)])
 
 
-@pytest.mark.parametrize("p", [1, 4])
-def test_small_pages_pool_over_2gib(lib, p):
-    # a pool of more than 2 GiB takes the small-page path's 64-bit
-    # addresses: the workload's pages are moved past the 2 GiB mark of a
-    # larger, otherwise unwritten pool (rows past a sequence's end in its
-    # last page hold whatever that memory holds and must not leak in)
+@pytest.mark.parametrize("p", [1, 4, 16])
+def test_pool_over_4gib(lib, p):
+    # pages past the 4 GiB mark of the pool: 64-bit addresses on the
+    # small-page path, page descriptors with 64-bit bases on the big-page
+    # path.  The workload's pages are moved to the end of a larger,
+    # otherwise unwritten pool (rows past a sequence's end in its last page
+    # hold whatever that memory holds and must not leak in).
     import torch
     w = W.build([1, 5, 33, 300, 1000], 32, 8, 128, p, seed=40 + p, pool="holes:0.2", poison=True)
     page_bytes = p * 8 * 128 * 2
-    big = (int(2.3 * 2 ** 30) // page_bytes) + w.k_cache.shape[0]
+    big = (int(4.2 * 2 ** 30) // page_bytes) + w.k_cache.shape[0]
     shift = big - w.k_cache.shape[0]
-    assert shift * page_bytes > 2 ** 31
-    log(f"small pages P={p}: pool of {big} pages ({big * page_bytes / 2 ** 30:.2f} GiB each for K and V)")
+    assert shift * page_bytes > 2 ** 32
+    log(f"pages of {p} tokens: pool of {big} pages ({big * page_bytes / 2 ** 30:.2f} GiB each for K and V)")
     dev = to_gpu(w)
     kb = torch.empty((big,) + tuple(dev["k"].shape[1:]), dtype=torch.bfloat16, device="cuda")
     vb = torch.empty_like(kb)
@@ -335,4 +336,4 @@ def test_small_pages_pool_over_2gib(lib, p):
     got = out.float().cpu().numpy().astype(np.float64)
     del kb, vb
     torch.cuda.empty_cache()
-    check(got, ref(w), f"P={p} pool over 2 GiB")
+    check(got, ref(w), f"P={p} pool over 4 GiB")
