@@ -63,6 +63,7 @@ def test_c_client_decode_matches_oracle(client, tmp_path, gpu_lib):
     log(res.stdout)
     assert res.returncode == 0, res.stdout + res.stderr
     assert "ok outputs bitwise equal across streams" in res.stdout
+    assert "ok graph replays bitwise equal" in res.stdout
     out = np.fromfile(tmp_path / "out.bin", dtype=np.uint16).reshape(w.q.shape)
     got = W.bf16_bits_to_f32(out).astype(np.float64)
     ref = oracle.attend(w.q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale)[0]
