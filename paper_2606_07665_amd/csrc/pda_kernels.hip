@@ -489,10 +489,15 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
 
-    // K and V rows of the step starting at token t0 -> the tile.  Rows past
-    // the end (and, with a window, before the first key) must be zeros, never
-    // NaN * 0 in the P.V product: with big pages they arrived as zeros; with
-    // small pages they are selected here.
+    // K and V rows of the step starting at token t0 -> the tile.  V rows past
+    // the end, and with a window before the first key, must be zeros, never
+    // NaN * 0 in the P.V product (their scores are masked by a select, so K
+    // rows need no such care on the big-page path).  With big pages, rows
+    // past the end arrive as zeros (the descriptor ends there); the earlier
+    // rows of the half-step that holds a window's first key are read from
+    // the page, so the step that starts before that key zeroes them here
+    // (a wave-uniform branch taken once per sequence piece).  With small
+    // pages every dead row is selected here.
     auto live_row = [&](int t0, int i) {
       const int tok = t0 + S::kRowsPerLoad * i + vr;
       return tok < L && tok >= lo_seq;
@@ -511,6 +516,13 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       for (int i = 0; i < S::kLoads; ++i) {
         vv[i] = vv_in[i];
         if constexpr (kLanePages) vv[i] = live_row(t0, i) ? vv[i] : u32x4{0u, 0u, 0u, 0u};
+      }
+      if constexpr (!kLanePages) {
+        if (t0 < lo_seq) {
+#pragma unroll
+          for (int i = 0; i < S::kLoads; ++i)
+            vv[i] = t0 + S::kRowsPerLoad * i + vr >= lo_seq ? vv[i] : u32x4{0u, 0u, 0u, 0u};
+        }
       }
 #pragma unroll
       for (int i = 0; i < S::kLoads; ++i)

@@ -37,6 +37,25 @@ def run(lib, w, dev=None, out=None, stream=None, fill=float("nan")):
     return out.float().cpu().numpy().astype(np.float64)
 
 
+def q4(w):
+    """q of a workload as [B, Tq, Hq, D]."""
+    return w.q if w.q.ndim == 4 else w.q[:, None]
+
+
+def run_ext(lib, w, dev=None, stream=None):
+    """paged_decode_attention_ext on workload w (its query tokens and
+    window); returns out as float64 numpy [B, Tq, Hq, D]."""
+    import torch
+    if dev is None:
+        dev = to_gpu(w)
+    q = dev["q"] if dev["q"].dim() == 4 else dev["q"].unsqueeze(1)
+    out = torch.full(tuple(q.shape), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lib.paged_decode_attention_ext(q.contiguous(), dev["k"], dev["v"], dev["bt"], dev["lens"], out,
+                                   float(w.scale), window=w.window, stream=stream)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy().astype(np.float64)
+
+
 def bf16_round(x):
     import workloads as W
     return W.bf16_bits_to_f32(W.f32_to_bf16_bits(np.asarray(x, dtype=np.float32))).astype(np.float64)
@@ -61,3 +80,32 @@ def check(got, ref, what="", max_ulps=1.0):
     if max_ulps is not None:
         assert ulps <= max_ulps, f"{what}: {ulps:.2f} bf16 ulps"
     return mx, mean
+
+
+def check_full(name, run_fn, tmpdir, max_ulps=1.0):
+    """Every output of the named workload against the fp64 oracle.
+
+    The oracle runs in a fresh interpreter (tests/_oracle_job.py) fanned out
+    over the host cores, started before this process builds the same seeded
+    workload and runs `run_fn(w)` (which returns the GPU output as float64),
+    so the two overlap.  Checks the required tolerance (max and mean over all
+    outputs) and one bf16 spacing everywhere."""
+    import _oracle_job
+    import workloads as W
+    job = _oracle_job.start(name, str(tmpdir))
+    try:
+        log(f"workload {name}: generating")
+        w = W.make(name)
+        log(f"workload {name}: running")
+        got = run_fn(w)
+        del w
+        log(f"workload {name}: waiting for the oracle over every output")
+        r = job.result().reshape(got.shape)
+    finally:
+        if job.proc.poll() is None:
+            job.proc.kill()
+            job.proc.wait()
+    check(got, r, f"{name} (every output)", max_ulps)
+    rb = bf16_round(r)
+    log(f"  {name}: {100 * float((got == rb).mean()):.2f}% bitwise equal to RN(oracle)")
+    return got, r

@@ -11,7 +11,7 @@ import pytest
 import oracle
 import workloads as W
 from _golden import cases as golden_cases
-from _gpu import bf16_round, bf16_ulps, check, log, run, to_gpu
+from _gpu import bf16_round, bf16_ulps, check, check_full, log, run, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -271,43 +271,11 @@ def test_named_workload_full_oracle(lib, name):
     assert d.max() <= 1.0
 
 
-def _sampled(lib, name, pairs_fn):
-    log(f"workload {name}: generating")
-    w = W.make(name)
-    log(f"workload {name}: running")
-    got = run(lib, w)
-    assert np.isfinite(got).all()
-    g = w.num_q_heads // w.num_kv_heads
-    pairs = pairs_fn(w)
-    log(f"workload {name}: oracle on {len(pairs)} sampled (b, g) pairs")
-    res = oracle.attend_pairs(w.q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale, pairs)
-    errs = []
-    for (b, kv), (o, _) in res.items():
-        errs.append(np.abs(got[b, kv * g:(kv + 1) * g] - o))
-    e = np.concatenate([x.ravel() for x in errs])
-    u = np.concatenate([bf16_ulps(got[b, kv * g:(kv + 1) * g], o).ravel() for (b, kv), (o, _) in res.items()])
-    log(f"  {name}: sampled max|err|={e.max():.3e} mean|err|={e.mean():.3e} max={u.max():.2f} bf16 ulp (n={e.size})")
-    assert e.max() <= 1e-2 and e.mean() <= 1e-3 and u.max() <= 1.0
-
-
-def test_long70b_sampled(lib):
-    _sampled(lib, "long70b", lambda w: [(0, 0), (1, 3), (2, 7), (3, 4)])
-
-
-def test_ragged_sampled(lib):
-    def pairs(w):
-        lens = w.context_lens
-        order = np.argsort(lens, kind="stable")
-        rng = np.random.default_rng(1)
-        picks = {int(order[0]), int(order[-1]), int(order[-2]), int(order[len(order) // 2])}
-        picks |= set(int(x) for x in rng.choice(w.batch, 12, replace=False))
-        return [(b, int(rng.integers(0, w.num_kv_heads))) for b in sorted(picks)] + [(int(order[-1]), 0)]
-    _sampled(lib, "ragged", pairs)
-
-
-def test_tokenpage_sampled(lib):
-    # pages of one token: every row of a step comes from its own page
-    _sampled(lib, "tokenpage", lambda w: [(0, 0), (7, 3), (31, 5), (63, 7), (40, 1)])
+@pytest.mark.parametrize("name", ["long70b", "ragged", "tokenpage"])
+def test_named_workload_every_output(lib, name, tmp_path):
+    # the full-size long-context, ragged and one-token-page workloads, every
+    # output against the oracle (fanned out over the host cores)
+    check_full(name, lambda w: run(lib, w), tmp_path)
 
 
 @pytest.mark.parametrize("p", [1, 4, 16])
@@ -337,3 +305,185 @@ def test_pool_over_4gib(lib, p):
     del kb, vb
     torch.cuda.empty_cache()
     check(got, ref(w), f"P={p} pool over 4 GiB")
+
+
+# ------------------------------------------------------ numerical edge cases
+# Every input above is N(0, 1); these reach the max shift, the exponent
+# reference of columns that have seen no key, the hi + lo probability split
+# and the merge with scores in the thousands.  Head sizes 64, 128 and 256,
+# pages of >= 16 tokens (one page descriptor per half-step) and of fewer
+# (a page id per row), and plans with one-step pieces (min_steps = 1: most
+# step boundaries are split points) as well as the default.
+EDGE_SHAPES = [(64, 16), (64, 4), (128, 32), (128, 1), (256, 16), (256, 4)]
+EDGE_IDS = [f"D{d}-P{p}" for d, p in EDGE_SHAPES]
+
+
+def _token_slot(w, b, t):
+    p = w.k_cache.shape[1]
+    return int(w.block_table[b, t // p]), t % p
+
+
+def _mean_v(w):
+    """Mean of V over each sequence's tokens, per kv head, repeated over the
+    query heads of the group ([B, Hq, D]); zero rows for empty sequences."""
+    bsz, hq, d = w.q.shape
+    hkv = w.k_cache.shape[2]
+    g = hq // hkv
+    out = np.zeros((bsz, hq, d))
+    for b in range(bsz):
+        L = int(w.context_lens[b])
+        if L == 0:
+            continue
+        rows = np.stack([oracle.bf16_to_f64(w.v_cache[_token_slot(w, b, t)]) for t in range(L)])  # [L, Hkv, D]
+        out[b] = np.repeat(rows.mean(axis=0), g, axis=0)
+    return out
+
+
+@pytest.mark.parametrize("min_steps", [1, 2])
+@pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
+def test_zero_query_gives_mean_of_v(lib, d, p, min_steps):
+    # q = 0: every score is 0, the weights are uniform and out is the mean
+    # of V (pinned by its own gather, not by the oracle's softmax)
+    w = W.build([1, 33, 700, 0, 4099], 16, 4, d, p, seed=90 + d + p, pool="holes:0.2")
+    w.q[:] = 0
+    lib.set_option(lib.OPT_MIN_STEPS, min_steps)
+    log(f"case q=0 D={d} P={p} min_steps={min_steps}")
+    check(run(lib, w), _mean_v(w), "q = 0")
+
+
+@pytest.mark.parametrize("min_steps", [1, 2])
+@pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
+def test_equal_keys_give_mean_of_v(lib, d, p, min_steps):
+    # every key of a (sequence, kv head) equal: every score of a query head
+    # is the same number, so again the mean of V whatever q is
+    w = W.build([2, 47, 700, 4099], 16, 4, d, p, seed=100 + d + p, pool="holes:0.2")
+    rng = np.random.default_rng(d + p)
+    for b in range(w.batch):
+        for g in range(4):
+            key = W.f32_to_bf16_bits(rng.standard_normal(d, dtype=np.float32))
+            for t in range(int(w.context_lens[b])):
+                page, slot = _token_slot(w, b, t)
+                w.k_cache[page, slot, g] = key
+    lib.set_option(lib.OPT_MIN_STEPS, min_steps)
+    log(f"case equal keys D={d} P={p} min_steps={min_steps}")
+    check(run(lib, w), _mean_v(w), "equal keys")
+
+
+def _plant_dominant(w, b, g, t, score):
+    """Give every query head of kv head g in sequence b the same query u and
+    put the key lambda * u at token t, lambda chosen for a score of about
+    `score`; returns the bf16 bits of that key."""
+    G = w.q.shape[-2] // w.k_cache.shape[2]
+    u_bits = w.q[b, ..., g * G, :].copy()
+    w.q[b, ..., g * G:(g + 1) * G, :] = u_bits[..., None, :] if w.q.ndim == 4 else u_bits
+    u = oracle.bf16_to_f64(u_bits.reshape(-1, u_bits.shape[-1])[0])
+    lam = score / (float(np.float32(w.scale)) * float(u @ u))
+    key = W.f32_to_bf16_bits((lam * u).astype(np.float32))
+    page, slot = _token_slot(w, b, t)
+    w.k_cache[page, slot, g] = key
+    return key, u
+
+
+@pytest.mark.parametrize("min_steps", [1, 2])
+@pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
+def test_dominant_key_returns_its_value(lib, d, p, min_steps):
+    # one key per (sequence, kv head) scores ~1e3 against the group's query
+    # (scale * q.k far beyond exp's fp32 range without the max shift): the
+    # output is that token's v, bitwise (every other weight is below 2^-1400).
+    # The key sits mid-step, on either side of a 32-token step boundary (a
+    # split point of most one-step-piece plans) or on the last token of a
+    # partly filled page; past the end of that page a masked key scoring
+    # ~2e3 (its V left NaN) must carry no weight.
+    lens = [4099, 701, 2067]
+    w = W.build(lens, 16, 4, d, p, seed=110 + d + p, pool="holes:0.2", poison=True)
+    G = 4
+    planted = {}
+    for b, L in enumerate(lens):
+        mid = (L // 2) // 32 * 32
+        for g, t in enumerate([37, L - 1, mid, mid - 1]):
+            key, u = _plant_dominant(w, b, g, t, 1000.0)
+            planted[(b, g)] = t
+            if L % p:  # slot L of the last page: past the end
+                page, slot = _token_slot(w, b, L)
+                w.k_cache[page, slot, g] = W.f32_to_bf16_bits((2.0 * oracle.bf16_to_f64(key)).astype(np.float32))
+                assert np.isnan(W.bf16_bits_to_f32(w.v_cache[page, slot, g])).all()
+    lib.set_option(lib.OPT_MIN_STEPS, min_steps)
+    log(f"case dominant key D={d} P={p} min_steps={min_steps}")
+    got = run(lib, w)
+    check(got, ref(w), "dominant key")
+    for (b, g), t in planted.items():
+        v = oracle.bf16_to_f64(w.v_cache[_token_slot(w, b, t)][g])
+        assert np.array_equal(got[b, g * G:(g + 1) * G], np.broadcast_to(v, (G, d))), (b, g, t)
+
+
+@pytest.mark.parametrize("min_steps", [1, 2])
+@pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
+def test_two_dominant_keys_split_the_weight(lib, d, p, min_steps):
+    # two keys scoring ~1000 and ~1000 - ln 2, far apart in the sequence (in
+    # different pieces of a split plan): the merge combines two pieces whose
+    # maxima are in the thousands, weights ~2/3 and ~1/3
+    lens = [4099, 2067]
+    w = W.build(lens, 16, 4, d, p, seed=120 + d + p, pool="holes:0.2", poison=True)
+    for b, L in enumerate(lens):
+        for g in range(4):
+            key, u = _plant_dominant(w, b, g, 5 + 7 * g, 1000.0)
+            second = W.f32_to_bf16_bits((oracle.bf16_to_f64(key) * (1.0 - np.log(2.0) / 1000.0)).astype(np.float32))
+            page, slot = _token_slot(w, b, L - 40 - 9 * g)
+            w.k_cache[page, slot, g] = second
+    lib.set_option(lib.OPT_MIN_STEPS, min_steps)
+    log(f"case two dominant keys D={d} P={p} min_steps={min_steps}")
+    check(run(lib, w), ref(w), "two dominant keys")
+
+
+@pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
+def test_dominant_key_outside_window_carries_no_weight(lib, d, p):
+    # a sliding window of 100 with two query tokens: the key just before the
+    # window of the later query (visible to the earlier one only) and the
+    # key just before the earlier query's window score ~1e3; the slots of
+    # the same page before those keys hold NaN values.  Only the earlier
+    # query may see the first key.
+    from _gpu import run_ext
+    window, tq = 100, 2
+    lens = [4099, 701, 163]
+    w = W.build(lens, 8, 4, d, p, seed=130 + d + p, pool="holes:0.2", poison=True, num_queries=tq,
+                window=window)
+    for b, L in enumerate(lens):
+        lo_last = L - window          # first key of the later query
+        for g in range(4):
+            key, u = _plant_dominant(w, b, g, lo_last - 1, 1000.0)      # seen by query 0 only
+            page, slot = _token_slot(w, b, lo_last - 2)                  # seen by neither
+            if page < 0:
+                continue  # a page wholly before the window: released
+            w.k_cache[page, slot, g] = key
+            for t in range(lo_last - 2 - (lo_last - 2) % p, lo_last - 2):
+                pg, sl = _token_slot(w, b, t)
+                w.v_cache[pg, sl, g] = W.BF16_NAN
+    log(f"case dominant key outside a window D={d} P={p}")
+    got = run_ext(lib, w)
+    r = oracle.attend_masked(w.q, w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale, window)[0]
+    check(got, r, "window edge")
+    G = 2
+    for b, L in enumerate(lens):
+        for g in range(4):
+            v = oracle.bf16_to_f64(w.v_cache[_token_slot(w, b, L - window - 1)][g])
+            assert np.array_equal(got[b, 0, g * G:(g + 1) * G], np.broadcast_to(v, (G, d)))
+
+
+@pytest.mark.parametrize("d", [64, 128, 256])
+def test_window_pre_window_slots_of_a_live_page_are_not_read(lib, d):
+    # pages of 32 tokens, a window that starts mid-page: the slots of that
+    # page before the first visible key hold NaN (keys and values); the
+    # outputs are finite and match the oracle
+    from _gpu import run_ext
+    lens = [4099, 701, 2067, 90]
+    window = 70
+    w = W.build(lens, 16, 4, d, 32, seed=140 + d, pool="holes:0.2", poison=True, window=window)
+    for b, L in enumerate(lens):
+        lo = max(0, L - window)
+        for t in range(lo - lo % 32, lo):
+            pg, sl = _token_slot(w, b, t)
+            w.k_cache[pg, sl] = W.BF16_NAN
+            w.v_cache[pg, sl] = W.BF16_NAN
+    got = run_ext(lib, w)
+    r = oracle.attend_masked(w.q[:, None], w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale, window)[0]
+    check(got, r, f"pre-window NaN D={d}")

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 import workloads as W
-from _gpu import bf16_round, bf16_ulps, check, log, to_gpu
+from _gpu import bf16_round, bf16_ulps, check, check_full, log, q4, run_ext, to_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -31,25 +31,9 @@ def default_options(gpu_lib):
     gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
 
 
-def q4(w):
-    return w.q if w.q.ndim == 4 else w.q[:, None]
-
-
 def ref(w):
     return oracle.attend_masked(q4(w), w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale,
                                 w.window)[0]
-
-
-def run_ext(lib, w, dev=None, stream=None):
-    import torch
-    if dev is None:
-        dev = to_gpu(w)
-    q = dev["q"] if dev["q"].dim() == 4 else dev["q"].unsqueeze(1)
-    out = torch.full(tuple(q.shape), float("nan"), dtype=torch.bfloat16, device="cuda")
-    lib.paged_decode_attention_ext(q.contiguous(), dev["k"], dev["v"], dev["bt"], dev["lens"], out,
-                                   float(w.scale), window=w.window, stream=stream)
-    torch.cuda.synchronize()
-    return out.float().cpu().numpy().astype(np.float64)
 
 
 # (head_dim, Hq, Hkv, page_size, lengths, query tokens, window)
@@ -147,31 +131,8 @@ def test_variant_graph_capture_replay(lib):
         check(out.float().cpu().numpy().astype(np.float64), r, f"replay {rep}")
 
 
-def _sampled_variant(lib, name, seqs):
-    log(f"workload {name}: generating")
-    w = W.make(name)
-    log(f"workload {name}: running")
-    got = run_ext(lib, w)
-    assert np.isfinite(got).all()
-    log(f"workload {name}: oracle on sequences {seqs}")
-    r = oracle.attend_masked(q4(w)[seqs], w.k_cache, w.v_cache, w.block_table[seqs], w.context_lens[seqs],
-                             w.scale, w.window)[0]
-    check(got[seqs], r, name)
-    rb = bf16_round(r)
-    log(f"  {name}: {100 * float((got[seqs] == rb).mean()):.2f}% bitwise equal to RN(oracle)")
-
-
-def test_window_workload_sampled(lib):
-    _sampled_variant(lib, "window", [0, 17, 63])
-
-
-def test_multiq_workload_sampled(lib):
-    _sampled_variant(lib, "multiq", [0, 5, 31, 62, 63])
-
-
-def test_gqa16_workload_sampled(lib):
-    _sampled_variant(lib, "gqa16", [0, 31])
-
-
-def test_falcon3_workload_sampled(lib):
-    _sampled_variant(lib, "falcon3", [0, 7, 15])
+@pytest.mark.parametrize("name", ["window", "multiq", "gqa16", "falcon3"])
+def test_variant_workload_every_output(lib, name, tmp_path):
+    # the named variant workloads (sliding window, four query tokens, G = 16,
+    # head_dim 256), every output against the oracle
+    check_full(name, lambda w: run_ext(lib, w), tmp_path)
