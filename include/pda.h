@@ -189,6 +189,35 @@ int paged_decode_attention_append(const void* q, const void* k_new, const void* 
                                   int32_t max_pages_per_seq, float scale, void* stream);
 
 /*
+ * paged_decode_attention_noalloc -- paged_decode_attention for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops and harnesses that forbid hipMalloc.  Same operation, arguments,
+ * layouts and errors, and the same kernels; the split partials, the steps
+ * prefix and the split list go to a fixed buffer the library holds on each
+ * device it runs on (a static device array of PDA_NOALLOC_SCRATCH_BYTES,
+ * kept until the process ends) instead of the per-(device, stream)
+ * workspace.  The call makes no hipMalloc or hipFree and needs no
+ * pda_workspace_reserve; the caller still passes every input and output.
+ *   - A shape whose plan needs more than PDA_NOALLOC_SCRATCH_BYTES fails
+ *     with PDA_ERR_UNSUPPORTED before any launch.  pda_plan's
+ *     workspace_bytes bounds the need (it covers 16 query columns per kv
+ *     head; one query token needs G).
+ *   - Every call on one device shares that device's buffer: two calls whose
+ *     executions overlap on one device (different streams, or graphs
+ *     replayed concurrently) race and give wrong results.  Order them.
+ *   - The buffer keeps the last call's contents; nothing in it needs to
+ *     start at any value.
+ *   - PDA_DEBUG_VALIDATE and the kernel timing (pda_profile_enable) do not
+ *     apply to this entry point.
+ */
+#define PDA_NOALLOC_SCRATCH_BYTES (64 * 1024 * 1024)
+int paged_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* context_lens, void* out,
+                                   int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                   int32_t head_dim, int32_t page_size, int32_t num_pages,
+                                   int32_t max_pages_per_seq, float scale, void* stream);
+
+/*
  * pda_plan -- host-only dry run of the split planner: how the context of the
  * batch is spread over waves (the paper's split across CTAs, sized here to
  * fill the given number of compute units).  No HIP call.

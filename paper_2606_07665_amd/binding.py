@@ -41,6 +41,9 @@ def _declare(lib: ctypes.CDLL) -> None:
     i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
     lib.paged_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp]
     lib.paged_decode_attention.restype = ctypes.c_int
+    lib.paged_decode_attention_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
+                                                   vp]
+    lib.paged_decode_attention_noalloc.restype = ctypes.c_int
     lib.paged_decode_attention_ext.argtypes = [vp] * 6 + [i32] * 9 + [f32, vp]
     lib.paged_decode_attention_ext.restype = ctypes.c_int
     dims_p = ctypes.POINTER(PreludeDims)
@@ -140,13 +143,9 @@ def _stream_ptr(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
-    """out[b, h] = softmax(scale * q[b, h] . K_b^T) V_b over the paged cache.
-
-    q, out: bf16 [B, Hq, D]; k_cache, v_cache: bf16 [N, P, Hkv, D];
-    block_table: int32 [B, maxp]; context_lens: int32 [B]; all contiguous on
-    one GPU.  Launches on ``stream`` (default: torch's current stream).
-    """
+def _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out):
+    """dtype, device, contiguity and shape checks of a one-query attention
+    call; returns (B, Hq, D, num_pages, page_size, Hkv)."""
     import torch
     for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
                         ("v_cache", v_cache, torch.bfloat16), ("out", out, torch.bfloat16),
@@ -163,10 +162,36 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, 
     n, p, hkv, d2 = k_cache.shape
     if d2 != d or block_table.dim() != 2 or block_table.shape[0] != b or context_lens.shape != (b,):
         raise ValueError("inconsistent shapes between q, caches, block_table and context_lens")
+    return b, hq, d, n, p, hkv
+
+
+def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
+    """out[b, h] = softmax(scale * q[b, h] . K_b^T) V_b over the paged cache.
+
+    q, out: bf16 [B, Hq, D]; k_cache, v_cache: bf16 [N, P, Hkv, D];
+    block_table: int32 [B, maxp]; context_lens: int32 [B]; all contiguous on
+    one GPU.  Launches on ``stream`` (default: torch's current stream).
+    """
+    b, hq, d, n, p, hkv = _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out)
     _check(raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
                     context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1],
                     float(scale), _stream_ptr(stream)))
     return out
+
+
+def paged_decode_attention_noalloc(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
+    """:func:`paged_decode_attention` through the entry point that allocates
+    nothing: its partials go to the library's fixed per-device scratch
+    (NOALLOC_SCRATCH_BYTES).  Calls on one device must not overlap in time."""
+    b, hq, d, n, p, hkv = _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out)
+    _check(load().paged_decode_attention_noalloc(
+        q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(),
+        out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1], ctypes.c_float(float(scale)),
+        _stream_ptr(stream)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024  # PDA_NOALLOC_SCRATCH_BYTES of include/pda.h
 
 
 def paged_decode_attention_ext(q, k_cache, v_cache, block_table, context_lens, out, scale, window=0,

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB_DIR = os.path.join(PKG, "_lib")
 LIB_PATH = os.path.join(LIB_DIR, "libpda.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("pda_kernels.hip", "pda_append.hip", "pda_gemv.hip", "pda_probe.hip", "pda_api.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("pda_kernels.hip", "pda_append.hip", "pda_gemv.hip", "pda_probe.hip", "pda_scratch.hip", "pda_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -348,6 +348,7 @@ int maybe_validate(const int32_t* block_table, const int32_t* context_lens, int3
   return validate_paging(block_table, context_lens, batch, maxp, page_size, num_pages, st);
 }
 
+
 // ---------------------------------------------------------------- prelude
 bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
 
@@ -449,6 +450,103 @@ int run_prelude(const void* x, const void* w_packed, const void* bias, const voi
   ep.log2_theta = std::log2(static_cast<double>(d.rope_theta));
   ep.eps = d.eps;
   if ((e = pda::launch_prelude_epilogue(ep, st)) != hipSuccess) return hip_fail(e, "prelude epilogue launch");
+  if (prof) {
+    if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    prof_push(rec);
+  }
+  return PDA_OK;
+}
+
+// The attention entry points: argument checks, plan, workspace, launches.
+// noalloc: the workspace is the library's fixed per-device scratch (no
+// allocation, no paging validation, no profiling events) instead of the
+// (device, stream) workspace, and shapes whose plan needs more than it
+// holds are rejected.
+int attention_call(const void* q, const void* k_cache, const void* v_cache, const int32_t* block_table,
+                   const int32_t* context_lens, void* out, int32_t batch, int32_t num_q_heads,
+                   int32_t num_kv_heads, int32_t head_dim, int32_t page_size, int32_t num_pages,
+                   int32_t max_pages_per_seq, int32_t num_queries, int32_t window, float scale, void* stream,
+                   bool noalloc) {
+  g_err.clear();
+  int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
+  if (rc) return rc;
+  if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
+  if (num_queries < 1) return fail(PDA_ERR_SHAPE, "num_queries must be >= 1 (got %d)", num_queries);
+  if (window < 0) return fail(PDA_ERR_SHAPE, "window must be >= 0 (got %d)", window);
+  if (num_queries > pda::kMaxCols || num_queries * (num_q_heads / num_kv_heads) > pda::kMaxCols)
+    return fail(PDA_ERR_UNSUPPORTED, "num_queries %d x query group %d exceeds %d", num_queries,
+                num_q_heads / num_kv_heads, pda::kMaxCols);
+  if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
+  const int cols = num_queries * (num_q_heads / num_kv_heads);
+  int valu_cols = 0;
+  if ((rc = check_compute_path(head_dim, page_size, cols, batch, &valu_cols))) return rc;
+  if (batch == 0) return PDA_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !context_lens || !out)
+    return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
+  auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
+  if (misaligned(q, 16) || misaligned(k_cache, 16) || misaligned(v_cache, 16) || misaligned(out, 16))
+    return fail(PDA_ERR_ALIGN, "q, k_cache, v_cache and out must be 16-byte aligned");
+  if (misaligned(block_table, 4) || misaligned(context_lens, 4))
+    return fail(PDA_ERR_ALIGN, "block_table and context_lens must be 4-byte aligned");
+  if (!noalloc && (rc = maybe_validate(block_table, context_lens, batch, max_pages_per_seq, page_size,
+                                       num_pages, static_cast<hipStream_t>(stream))))
+    return rc;
+
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int cus = 0;
+  if ((rc = device_cus(dev, &cus))) return rc;
+  const Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus, cols);
+  if (pda::attn_lds_bytes(head_dim, batch, pl.waves, valu_cols > 0) > static_cast<size_t>(pda::kMaxLdsBytes))
+    return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has", batch);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  if (noalloc) {
+    if (pl.bytes > PDA_NOALLOC_SCRATCH_BYTES)
+      return fail(PDA_ERR_UNSUPPORTED,
+                  "this shape needs %lld bytes of workspace; the no-allocation entry point holds %lld",
+                  static_cast<long long>(pl.bytes), static_cast<long long>(PDA_NOALLOC_SCRATCH_BYTES));
+    if ((e = pda::noalloc_scratch(dev, &ws)) != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+  } else if ((rc = workspace_for(dev, st, pl.bytes, &ws))) {
+    return rc;
+  }
+
+  pda::LaunchArgs a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k_cache);
+  a.v = static_cast<const uint16_t*>(v_cache);
+  a.bt = block_table;
+  a.lens = context_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.ws_acc = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_acc);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_ml);
+  a.ws_pref = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pl.off_pref);
+  a.batch = batch;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.group = num_q_heads / num_kv_heads;
+  a.head_dim = head_dim;
+  a.page_shift = log2i(page_size);
+  a.num_pages = num_pages;
+  a.maxp = max_pages_per_seq;
+  a.grid = pl.grid;
+  a.waves = pl.waves;
+  a.hgs = pl.hgs;
+  a.min_steps = min_steps_per_wave();
+  a.scale = scale;
+  a.nq = num_queries;
+  a.window = window;
+  a.valu_cols = valu_cols;
+
+  const Rec rec = noalloc ? Rec{nullptr, nullptr, nullptr, 0} : prof_begin(0);
+  const bool prof = rec.a != nullptr;
+  if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  if ((e = pda::launch_attn_kernel(a, st)) != hipSuccess) return hip_fail(e, "attention kernel launch");
+  if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  // with one workgroup every piece is a whole sequence: nothing to merge
+  if (pl.grid > 1 && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
+    return hip_fail(e, "merge kernel launch");
   if (prof) {
     if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
     prof_push(rec);
@@ -675,83 +773,18 @@ int paged_decode_attention_ext(const void* q, const void* k_cache, const void* v
                                int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                                int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
                                int32_t num_queries, int32_t window, float scale, void* stream) {
-  g_err.clear();
-  int rc = check_attention(batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq);
-  if (rc) return rc;
-  if (num_pages <= 0) return fail(PDA_ERR_SHAPE, "num_pages must be positive (got %d)", num_pages);
-  if (num_queries < 1) return fail(PDA_ERR_SHAPE, "num_queries must be >= 1 (got %d)", num_queries);
-  if (window < 0) return fail(PDA_ERR_SHAPE, "window must be >= 0 (got %d)", window);
-  if (num_queries > pda::kMaxCols || num_queries * (num_q_heads / num_kv_heads) > pda::kMaxCols)
-    return fail(PDA_ERR_UNSUPPORTED, "num_queries %d x query group %d exceeds %d", num_queries,
-                num_q_heads / num_kv_heads, pda::kMaxCols);
-  if (!std::isfinite(scale)) return fail(PDA_ERR_SCALE, "scale is not finite");
-  const int cols = num_queries * (num_q_heads / num_kv_heads);
-  int valu_cols = 0;
-  if ((rc = check_compute_path(head_dim, page_size, cols, batch, &valu_cols))) return rc;
-  if (batch == 0) return PDA_OK;
-  if (!q || !k_cache || !v_cache || !block_table || !context_lens || !out)
-    return fail(PDA_ERR_NULL, "a tensor pointer is NULL");
-  auto misaligned = [](const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; };
-  if (misaligned(q, 16) || misaligned(k_cache, 16) || misaligned(v_cache, 16) || misaligned(out, 16))
-    return fail(PDA_ERR_ALIGN, "q, k_cache, v_cache and out must be 16-byte aligned");
-  if (misaligned(block_table, 4) || misaligned(context_lens, 4))
-    return fail(PDA_ERR_ALIGN, "block_table and context_lens must be 4-byte aligned");
-  if ((rc = maybe_validate(block_table, context_lens, batch, max_pages_per_seq, page_size, num_pages,
-                           static_cast<hipStream_t>(stream))))
-    return rc;
+  return attention_call(q, k_cache, v_cache, block_table, context_lens, out, batch, num_q_heads, num_kv_heads,
+                        head_dim, page_size, num_pages, max_pages_per_seq, num_queries, window, scale, stream,
+                        false);
+}
 
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  int cus = 0;
-  if ((rc = device_cus(dev, &cus))) return rc;
-  const Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus, cols);
-  if (pda::attn_lds_bytes(head_dim, batch, pl.waves, valu_cols > 0) > static_cast<size_t>(pda::kMaxLdsBytes))
-    return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has", batch);
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  void* ws = nullptr;
-  if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;
-
-  pda::LaunchArgs a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k = static_cast<const uint16_t*>(k_cache);
-  a.v = static_cast<const uint16_t*>(v_cache);
-  a.bt = block_table;
-  a.lens = context_lens;
-  a.out = static_cast<uint16_t*>(out);
-  a.ws_acc = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_acc);
-  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_ml);
-  a.ws_pref = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + pl.off_pref);
-  a.batch = batch;
-  a.hq = num_q_heads;
-  a.hkv = num_kv_heads;
-  a.group = num_q_heads / num_kv_heads;
-  a.head_dim = head_dim;
-  a.page_shift = log2i(page_size);
-  a.num_pages = num_pages;
-  a.maxp = max_pages_per_seq;
-  a.grid = pl.grid;
-  a.waves = pl.waves;
-  a.hgs = pl.hgs;
-  a.min_steps = min_steps_per_wave();
-  a.scale = scale;
-  a.nq = num_queries;
-  a.window = window;
-  a.valu_cols = valu_cols;
-
-  const Rec rec = prof_begin(0);
-  const bool prof = rec.a != nullptr;
-  if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  if ((e = pda::launch_attn_kernel(a, st)) != hipSuccess) return hip_fail(e, "attention kernel launch");
-  if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  // with one workgroup every piece is a whole sequence: nothing to merge
-  if (pl.grid > 1 && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
-    return hip_fail(e, "merge kernel launch");
-  if (prof) {
-    if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    prof_push(rec);
-  }
-  return PDA_OK;
+int paged_decode_attention_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                   const int32_t* block_table, const int32_t* context_lens, void* out,
+                                   int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq, float scale,
+                                   void* stream) {
+  return attention_call(q, k_cache, v_cache, block_table, context_lens, out, batch, num_q_heads, num_kv_heads,
+                        head_dim, page_size, num_pages, max_pages_per_seq, 1, 0, scale, stream, true);
 }
 
 int pda_pack_weights(const void* w, void* w_packed, int32_t rows, int32_t cols, void* stream) {

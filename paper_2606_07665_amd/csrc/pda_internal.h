@@ -40,6 +40,10 @@ struct LaunchArgs {
 };
 
 hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st);
+// Device address of the fixed scratch of the no-allocation entry point on
+// device `dev` (which must be current); taken once per device.
+constexpr int kMaxDevices = 64;
+hipError_t noalloc_scratch(int dev, void** ptr);
 hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st);
 size_t attn_lds_bytes(int head_dim, int batch, int waves, bool valu = false);
 
