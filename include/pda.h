@@ -33,6 +33,13 @@
  * internal workspace per (device, stream), grown on demand (see
  * pda_workspace_reserve) and released by pda_release_workspaces.
  *
+ * Interface readings: the paper defines the operations (attention, its KV
+ * append, prelude and output projection), not a library interface.  Calls
+ * marked [library interface] below -- workspace management, planning,
+ * options, validation, timing, error reporting -- are this library's own,
+ * with no counterpart in the paper; so are the status codes and their
+ * numbering.
+ *
  * Errors: every entry point returns PDA_OK (0) or a PDA_ERR_* code and sets a
  * thread-local message readable with pda_last_error().  Argument checks run
  * before any HIP call; on an argument error nothing is launched and `out` is
@@ -60,7 +67,10 @@ enum pda_status {
   PDA_ERR_UNSUPPORTED = 3, /* valid but not implemented (head_dim, group, page)   */
   PDA_ERR_SCALE = 4,       /* scale is not a finite number                        */
   PDA_ERR_ALIGN = 5,       /* q, k_cache, v_cache or out not 16-byte aligned      */
-  PDA_ERR_HIP = 6          /* a HIP runtime call failed (message has the detail)  */
+  PDA_ERR_HIP = 6,         /* a HIP runtime call failed (message has the detail)  */
+  PDA_ERR_DTYPE = 7,       /* a tensor descriptor has the wrong element type      */
+  PDA_ERR_LAYOUT = 8       /* a tensor descriptor's strides are not the layout
+                              the operation reads (see pda_tensor)                */
 };
 
 /* Supported set of this version. */
@@ -104,6 +114,66 @@ int paged_decode_attention(const void* q, const void* k_cache, const void* v_cac
                            int32_t head_dim, int32_t page_size, int32_t num_pages,
                            int32_t max_pages_per_seq,
                            float scale, void* stream);
+
+/*
+ * Tensor descriptors: the dtype and layout half of the contract, for callers
+ * that hold tensors rather than bare pointers.  The paper's contract for a
+ * generated kernel names the tensor interface and its dtype rules (Problem
+ * Formulation, the contract-gated tier); its attention operates on bf16
+ * models (Experiments, Setup).  The descriptor form checks both before any
+ * HIP call:
+ *   data    device pointer of element [0, 0, ...].
+ *   dtype   a pda_dtype.
+ *   ndim    dimensions in use (1 .. PDA_MAX_DIMS); shape[i], stride[i] for
+ *           i < ndim, strides in elements.
+ * The attention reads dense row-major tensors: stride[ndim - 1] = 1 and
+ * stride[i] = stride[i + 1] * shape[i + 1]; the stride of a dimension of
+ * extent 1 is not looked at, and an empty tensor has no layout.  Other
+ * strides (transposed, sliced or padded views) give PDA_ERR_LAYOUT.
+ */
+typedef enum {
+  PDA_DTYPE_BF16 = 0,
+  PDA_DTYPE_F16 = 1,
+  PDA_DTYPE_F32 = 2,
+  PDA_DTYPE_I32 = 3,
+  PDA_DTYPE_I64 = 4
+} pda_dtype;
+
+#define PDA_MAX_DIMS 4
+typedef struct {
+  void* data;
+  int32_t dtype;
+  int32_t ndim;
+  int64_t shape[PDA_MAX_DIMS];
+  int64_t stride[PDA_MAX_DIMS];
+} pda_tensor;
+
+/*
+ * paged_decode_attention_desc -- paged_decode_attention with tensor
+ * descriptors:
+ *   q, out        PDA_DTYPE_BF16, ndim 3: [batch, num_q_heads, head_dim]
+ *   k_cache       PDA_DTYPE_BF16, ndim 4: [num_pages, page_size, num_kv_heads, head_dim]
+ *   v_cache       same dtype and shape as k_cache
+ *   block_table   PDA_DTYPE_I32, ndim 2: [batch, max_pages_per_seq]
+ *   context_lens  PDA_DTYPE_I32, ndim 1: [batch]
+ * all dense row-major.  The sizes come from the shapes; everything else
+ * (semantics, supported set, alignment, workspace, asynchrony, capture) is
+ * as for paged_decode_attention.  Errors, all before any HIP call:
+ *   PDA_ERR_NULL    a descriptor is NULL, or a non-empty tensor's data is NULL;
+ *   PDA_ERR_DTYPE   a dtype other than the one listed (fp16, fp32 or int64
+ *                   tensors are not converted);
+ *   PDA_ERR_SHAPE   an ndim other than the one listed, a negative extent, or
+ *                   shapes that disagree (out vs q, v_cache vs k_cache,
+ *                   head_dim of q vs the caches, batch of block_table and
+ *                   context_lens vs q, num_q_heads not a multiple of
+ *                   num_kv_heads) or exceed int32;
+ *   PDA_ERR_LAYOUT  strides other than the dense row-major ones;
+ *   then the checks of paged_decode_attention (PDA_ERR_UNSUPPORTED for
+ *   head_dim, page_size or group, PDA_ERR_SCALE, PDA_ERR_ALIGN, ...).
+ */
+int paged_decode_attention_desc(const pda_tensor* q, const pda_tensor* k_cache, const pda_tensor* v_cache,
+                                const pda_tensor* block_table, const pda_tensor* context_lens,
+                                const pda_tensor* out, float scale, void* stream);
 
 /*
  * paged_decode_attention_ext -- the same step with a key range per query:
@@ -218,7 +288,7 @@ int paged_decode_attention_noalloc(const void* q, const void* k_cache, const voi
                                    int32_t max_pages_per_seq, float scale, void* stream);
 
 /*
- * pda_plan -- host-only dry run of the split planner: how the context of the
+ * pda_plan [library interface] -- host-only dry run of the split planner: how the context of the
  * batch is spread over waves (the paper's split across CTAs, sized here to
  * fill the given number of compute units).  No HIP call.
  *   num_cus      compute units of the target device (256 on MI355X).
@@ -233,7 +303,7 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
              int32_t* grid_blocks, int32_t* waves, int64_t* workspace_bytes);
 
 /*
- * pda_workspace_reserve -- grow the workspace of (current device, stream) so
+ * pda_workspace_reserve [library interface] -- grow the workspace of (current device, stream) so
  * that a later call with this shape (any num_queries and window) allocates
  * nothing (e.g. before graph capture).  Synchronous; may call hipMalloc.
  * A graph captured on a stream keeps using the workspace it was captured
@@ -245,7 +315,8 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
                           int32_t head_dim, int32_t page_size, int32_t max_pages_per_seq,
                           void* stream);
 
-/* Free every workspace the library holds (synchronises their streams). */
+/* [library interface] Free every workspace the library holds (synchronises
+   their streams). */
 int pda_release_workspaces(void);
 
 /*
@@ -255,7 +326,7 @@ int pda_release_workspaces(void);
  */
 
 /*
- * pda_validate_paging -- debugging aid: synchronise `stream`, copy
+ * pda_validate_paging [library interface] -- debugging aid: synchronise `stream`, copy
  * context_lens [batch] and block_table [batch, max_pages_per_seq] (device
  * pointers) to the host and check 0 <= L_b <= max_pages_per_seq * page_size
  * and 0 <= block_table[b][j] < num_pages for every page a sequence uses.
@@ -268,14 +339,15 @@ int pda_release_workspaces(void);
 int pda_validate_paging(const int32_t* block_table, const int32_t* context_lens, int32_t batch,
                         int32_t max_pages_per_seq, int32_t page_size, int32_t num_pages, void* stream);
 
-/* Thread-local message of the last failing call on this thread ("" if none). */
+/* [library interface] Thread-local message of the last failing call on this
+   thread ("" if none). */
 const char* pda_last_error(void);
 
-/* PDA_VERSION of the built library. */
+/* [library interface] PDA_VERSION of the built library. */
 int32_t pda_version(void);
 
 /*
- * Planner options (tuning and testing).  The split planner spreads the
+ * Planner options [library interface] (tuning and testing).  The split planner spreads the
  * batch's context over min(num_cus * blocks_per_cu, ceil(total 32-token
  * steps / (min_steps * step phases))) workgroups of up to 8 waves.
  *   PDA_OPT_BLOCKS_PER_CU  workgroups per compute unit, 1..8
@@ -304,7 +376,7 @@ int pda_set_option(int32_t option, int32_t value);
 int32_t pda_get_option(int32_t option);
 
 /*
- * Kernel timing for measurement harnesses.  While enabled, every attention
+ * Kernel timing [library interface] for measurement harnesses.  While enabled, every attention
  * call (paged_decode_attention and its _ext / _append forms) and every
  * prelude call records HIP events on its stream around each kernel it
  * launches.  pda_profile_read synchronises those events, returns
@@ -318,7 +390,7 @@ int pda_profile_read_prelude(double* gemv_ms, double* epilogue_ms, int64_t* call
 int pda_profile_read_o_proj(double* gemv_ms, double* epilogue_ms, int64_t* calls);
 
 /*
- * Streaming-read reference for measurement harnesses: one kernel that only
+ * Streaming-read reference [library interface] for measurement harnesses: one kernel that only
  * reads `bytes` of device memory at `buf` (16-byte aligned, bytes a positive
  * multiple of 16), each byte once, with the attention kernel's loads
  * (16-byte non-temporal buffer loads).  Its bandwidth is what an HBM-bound
@@ -366,7 +438,7 @@ typedef struct {
 } pda_prelude_dims;
 
 /*
- * pda_pack_weights -- copy a bf16 [rows, cols] row-major weight matrix into
+ * pda_pack_weights [library interface] -- copy a bf16 [rows, cols] row-major weight matrix into
  * the packed order the prelude reads (16-row x 32-column tiles of 1 KB in
  * matrix-core operand order).  rows a multiple of 16, cols a multiple of 32;
  * w and w_packed (rows * cols bf16, caller-owned, not overlapping) 16-byte
@@ -408,7 +480,8 @@ int pda_attention_prelude_append(const void* x, const void* w_packed, const void
                                  int32_t page_size, int32_t num_pages, int32_t max_pages_per_seq,
                                  const pda_prelude_dims* dims, void* stream);
 
-/* Grow the (current device, stream) workspace for a prelude of these dims. */
+/* [library interface] Grow the (current device, stream) workspace for a
+   prelude of these dims. */
 int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream);
 
 /*
@@ -436,6 +509,8 @@ int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream);
 int pda_o_proj_residual_norm(const void* attn, const void* w_packed, const void* residual, const void* norm_w,
                              void* residual_out, void* normed_out, int32_t batch, int32_t in_features,
                              int32_t hidden, float eps, void* stream);
+/* [library interface] Grow the (current device, stream) workspace for an
+   o_proj call of this shape. */
 int pda_o_proj_workspace_reserve(int32_t batch, int32_t in_features, int32_t hidden, void* stream);
 
 #ifdef __cplusplus

@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(_PKG), "include", "pda.h")
 
 PDA_OK = 0
 ERRORS = {1: "PDA_ERR_NULL", 2: "PDA_ERR_SHAPE", 3: "PDA_ERR_UNSUPPORTED", 4: "PDA_ERR_SCALE",
-          5: "PDA_ERR_ALIGN", 6: "PDA_ERR_HIP"}
+          5: "PDA_ERR_ALIGN", 6: "PDA_ERR_HIP", 7: "PDA_ERR_DTYPE", 8: "PDA_ERR_LAYOUT"}
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -37,6 +37,48 @@ class PreludeDims(ctypes.Structure):
                 ("interleaved", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("eps", ctypes.c_float)]
 
 
+DTYPE_BF16, DTYPE_F16, DTYPE_F32, DTYPE_I32, DTYPE_I64 = range(5)  # pda_dtype
+MAX_DIMS = 4
+
+
+class Tensor(ctypes.Structure):
+    """pda_tensor of include/pda.h: device pointer, dtype, rank, extents and
+    strides in elements."""
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * MAX_DIMS), ("stride", ctypes.c_int64 * MAX_DIMS)]
+
+
+def tensor_desc(data_ptr, dtype: int, shape, stride=None) -> Tensor:
+    """A descriptor from a raw pointer; ``stride`` defaults to dense row-major."""
+    shape = [int(x) for x in shape]
+    if stride is None:
+        stride, acc = [], 1
+        for n in reversed(shape):
+            stride.insert(0, acc)
+            acc *= n
+    t = Tensor()
+    t.data = data_ptr
+    t.dtype = int(dtype)
+    t.ndim = len(shape)
+    for i, (n, st) in enumerate(zip(shape, stride)):
+        t.shape[i] = n
+        t.stride[i] = int(st)
+    return t
+
+
+def describe(t) -> Tensor:
+    """The descriptor of a torch tensor as it is (dtype, shape and strides
+    unchanged; the library decides whether it can read them)."""
+    import torch
+    codes = {torch.bfloat16: DTYPE_BF16, torch.float16: DTYPE_F16, torch.float32: DTYPE_F32,
+             torch.int32: DTYPE_I32, torch.int64: DTYPE_I64}
+    if t.dtype not in codes:
+        raise TypeError(f"no pda_dtype for {t.dtype}")
+    if t.dim() > MAX_DIMS:
+        raise ValueError(f"a descriptor holds at most {MAX_DIMS} dimensions")
+    return tensor_desc(t.data_ptr(), codes[t.dtype], t.shape, t.stride())
+
+
 def _declare(lib: ctypes.CDLL) -> None:
     i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
     lib.paged_decode_attention.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32, vp]
@@ -44,6 +86,9 @@ def _declare(lib: ctypes.CDLL) -> None:
     lib.paged_decode_attention_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, f32,
                                                    vp]
     lib.paged_decode_attention_noalloc.restype = ctypes.c_int
+    tp = ctypes.POINTER(Tensor)
+    lib.paged_decode_attention_desc.argtypes = [tp] * 6 + [f32, vp]
+    lib.paged_decode_attention_desc.restype = ctypes.c_int
     lib.paged_decode_attention_ext.argtypes = [vp] * 6 + [i32] * 9 + [f32, vp]
     lib.paged_decode_attention_ext.restype = ctypes.c_int
     dims_p = ctypes.POINTER(PreludeDims)
@@ -143,26 +188,59 @@ def _stream_ptr(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out):
-    """dtype, device, contiguity and shape checks of a one-query attention
-    call; returns (B, Hq, D, num_pages, page_size, Hkv)."""
-    import torch
-    for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
-                        ("v_cache", v_cache, torch.bfloat16), ("out", out, torch.bfloat16),
-                        ("block_table", block_table, torch.int32), ("context_lens", context_lens, torch.int32)):
+def _validate(specs, known=None):
+    """Argument checks of a wrapper, before any launch.  ``specs``: (name,
+    tensor or None, torch dtype, dims) with dims a space-separated list of
+    extents -- a number, ``*`` (any), or a symbol bound by the first tensor
+    that has it (or by ``known``) and checked on every other.  All shapes are
+    checked first, then dtypes, then that every tensor is on one GPU, then
+    contiguity, so a bad argument raises whichever it is.  Returns the
+    bound sizes."""
+    sizes = dict(known or {})
+    present = [sp for sp in specs if sp[1] is not None]
+    for name, t, _, dims in present:
+        syms = dims.split()
+        if t.dim() != len(syms):
+            raise ValueError(f"{name} must be [{', '.join(syms)}], got shape {tuple(t.shape)}")
+        for sym, ext in zip(syms, t.shape):
+            if sym == "*":
+                continue
+            if sym.isdigit():
+                want = int(sym)
+            elif sym in sizes:
+                want = sizes[sym]
+            else:
+                sizes[sym] = int(ext)
+                continue
+            if int(ext) != want:
+                raise ValueError(f"{name} must be [{', '.join(syms)}] with {sym} = {want}, got shape {tuple(t.shape)}")
+    for name, t, dt, _ in present:
         if t.dtype != dt:
             raise TypeError(f"{name} must be {dt}, got {t.dtype}")
+    for name, t, _, _ in present:
         if not t.is_cuda:
             raise ValueError(f"{name} must be a GPU tensor")
+    if len({t.device for _, t, _, _ in present}) > 1:
+        raise ValueError("all tensors must be on one GPU")
+    for name, t, _, _ in present:
         if not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
-    if q.dim() != 3 or k_cache.dim() != 4 or v_cache.shape != k_cache.shape or out.shape != q.shape:
-        raise ValueError("shapes: q/out [B,Hq,D], k_cache/v_cache [N,P,Hkv,D]")
-    b, hq, d = q.shape
-    n, p, hkv, d2 = k_cache.shape
-    if d2 != d or block_table.dim() != 2 or block_table.shape[0] != b or context_lens.shape != (b,):
-        raise ValueError("inconsistent shapes between q, caches, block_table and context_lens")
-    return b, hq, d, n, p, hkv
+    return sizes
+
+
+def _cache_specs(k_cache, v_cache, block_table, context_lens):
+    import torch
+    return [("k_cache", k_cache, torch.bfloat16, "N P Hkv D"), ("v_cache", v_cache, torch.bfloat16, "N P Hkv D"),
+            ("block_table", block_table, torch.int32, "B M"), ("context_lens", context_lens, torch.int32, "B")]
+
+
+def _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out):
+    """Checks of a one-query attention call; returns (B, Hq, D, num_pages,
+    page_size, Hkv)."""
+    import torch
+    sz = _validate([("q", q, torch.bfloat16, "B Hq D"), *_cache_specs(k_cache, v_cache, block_table, context_lens),
+                    ("out", out, torch.bfloat16, "B Hq D")])
+    return sz["B"], sz["Hq"], sz["D"], sz["N"], sz["P"], sz["Hkv"]
 
 
 def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
@@ -194,6 +272,22 @@ def paged_decode_attention_noalloc(q, k_cache, v_cache, block_table, context_len
 NOALLOC_SCRATCH_BYTES = 64 * 1024 * 1024  # PDA_NOALLOC_SCRATCH_BYTES of include/pda.h
 
 
+def desc_call(q, k_cache, v_cache, block_table, context_lens, out, scale, stream_ptr=None) -> int:
+    """paged_decode_attention_desc on six descriptors (Tensor or None);
+    returns the status code."""
+    ref = [None if t is None else ctypes.byref(t) for t in (q, k_cache, v_cache, block_table, context_lens, out)]
+    return load().paged_decode_attention_desc(*ref, ctypes.c_float(scale), stream_ptr)
+
+
+def paged_decode_attention_desc(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
+    """:func:`paged_decode_attention` through the descriptor entry point:
+    the tensors are passed as they are (dtype, shape, strides) and the
+    library checks them (PDA_ERR_DTYPE, PDA_ERR_SHAPE, PDA_ERR_LAYOUT)."""
+    _check(desc_call(*(describe(t) for t in (q, k_cache, v_cache, block_table, context_lens, out)), float(scale),
+                     _stream_ptr(stream)))
+    return out
+
+
 def paged_decode_attention_ext(q, k_cache, v_cache, block_table, context_lens, out, scale, window=0,
                                stream=None):
     """Several causal query tokens per sequence and an optional sliding window.
@@ -204,81 +298,49 @@ def paged_decode_attention_ext(q, k_cache, v_cache, block_table, context_lens, o
     :func:`paged_decode_attention`.
     """
     import torch
-    _check_cache_args(k_cache, v_cache, block_table, context_lens,
-                      (("q", q, torch.bfloat16), ("out", out, torch.bfloat16)))
-    if q.dim() != 4 or out.shape != q.shape:
-        raise ValueError("q and out must be [B, Tq, Hq, D]")
-    b, tq, hq, d = q.shape
-    n, p, hkv, d2 = k_cache.shape
-    if d2 != d or block_table.shape[0] != b or context_lens.shape != (b,):
-        raise ValueError("inconsistent shapes between q, caches, block_table and context_lens")
+    sz = _validate([("q", q, torch.bfloat16, "B T Hq D"), *_cache_specs(k_cache, v_cache, block_table, context_lens),
+                    ("out", out, torch.bfloat16, "B T Hq D")])
     _check(load().paged_decode_attention_ext(
         q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(),
-        out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1], tq, int(window), ctypes.c_float(float(scale)),
-        _stream_ptr(stream)))
+        out.data_ptr(), sz["B"], sz["Hq"], sz["Hkv"], sz["D"], sz["P"], sz["N"], sz["M"], sz["T"], int(window),
+        ctypes.c_float(float(scale)), _stream_ptr(stream)))
     return out
-
-
-def _check_cache_args(k_cache, v_cache, block_table, context_lens, extra):
-    import torch
-    for name, t, dt in (("k_cache", k_cache, torch.bfloat16), ("v_cache", v_cache, torch.bfloat16),
-                        ("block_table", block_table, torch.int32), ("context_lens", context_lens, torch.int32),
-                        *extra):
-        if t.dtype != dt:
-            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
-        if not t.is_cuda:
-            raise ValueError(f"{name} must be a GPU tensor")
-        if not t.is_contiguous():
-            raise ValueError(f"{name} must be contiguous")
-    if k_cache.dim() != 4 or v_cache.shape != k_cache.shape or block_table.dim() != 2:
-        raise ValueError("shapes: k_cache/v_cache [N,P,Hkv,D], block_table [B,maxp]")
 
 
 def kv_append(k_new, v_new, k_cache, v_cache, block_table, context_lens, stream=None):
     """Scatter each sequence's new key/value ([B, Hkv, D] bf16) into its page
     slot at position context_lens[b] - 1 (the length counts the new token)."""
     import torch
-    _check_cache_args(k_cache, v_cache, block_table, context_lens,
-                      (("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)))
-    n, p, hkv, d = k_cache.shape
-    b = block_table.shape[0]
-    if k_new.shape != (b, hkv, d) or v_new.shape != (b, hkv, d) or context_lens.shape != (b,):
-        raise ValueError("k_new/v_new must be [B, Hkv, D] and context_lens [B]")
+    sz = _validate([("k_new", k_new, torch.bfloat16, "B Hkv D"), ("v_new", v_new, torch.bfloat16, "B Hkv D"),
+                    *_cache_specs(k_cache, v_cache, block_table, context_lens)])
     _check(load().pda_kv_append(k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
-                                block_table.data_ptr(), context_lens.data_ptr(), b, hkv, d, p, n,
-                                block_table.shape[1], _stream_ptr(stream)))
+                                block_table.data_ptr(), context_lens.data_ptr(), sz["B"], sz["Hkv"], sz["D"], sz["P"],
+                                sz["N"], sz["M"], _stream_ptr(stream)))
 
 
 def kv_append_n(k_new, v_new, k_cache, v_cache, block_table, context_lens, stream=None):
     """Scatter T new tokens per sequence ([B, T, Hkv, D] bf16) to positions
     context_lens[b] - T + j (the lengths count all of them)."""
     import torch
-    _check_cache_args(k_cache, v_cache, block_table, context_lens,
-                      (("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)))
-    n, p, hkv, d = k_cache.shape
-    b = block_table.shape[0]
-    if k_new.dim() != 4 or k_new.shape[0] != b or k_new.shape[2:] != (hkv, d) or v_new.shape != k_new.shape:
-        raise ValueError("k_new/v_new must be [B, T, Hkv, D]")
+    sz = _validate([("k_new", k_new, torch.bfloat16, "B T Hkv D"), ("v_new", v_new, torch.bfloat16, "B T Hkv D"),
+                    *_cache_specs(k_cache, v_cache, block_table, context_lens)])
     _check(load().pda_kv_append_n(k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
-                                  block_table.data_ptr(), context_lens.data_ptr(), b, k_new.shape[1], hkv, d, p,
-                                  n, block_table.shape[1], _stream_ptr(stream)))
+                                  block_table.data_ptr(), context_lens.data_ptr(), sz["B"], sz["T"], sz["Hkv"],
+                                  sz["D"], sz["P"], sz["N"], sz["M"], _stream_ptr(stream)))
 
 
 def paged_decode_attention_append(q, k_new, v_new, k_cache, v_cache, block_table, context_lens, out, scale,
                                   stream=None):
     """kv_append then paged_decode_attention on the same stream."""
     import torch
-    _check_cache_args(k_cache, v_cache, block_table, context_lens,
-                      (("q", q, torch.bfloat16), ("out", out, torch.bfloat16),
-                       ("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16)))
-    b, hq, d = q.shape
-    n, p, hkv, d2 = k_cache.shape
-    if d2 != d or out.shape != q.shape or k_new.shape != (b, hkv, d) or v_new.shape != (b, hkv, d):
-        raise ValueError("inconsistent shapes")
+    sz = _validate([("q", q, torch.bfloat16, "B Hq D"), ("k_new", k_new, torch.bfloat16, "B Hkv D"),
+                    ("v_new", v_new, torch.bfloat16, "B Hkv D"),
+                    *_cache_specs(k_cache, v_cache, block_table, context_lens),
+                    ("out", out, torch.bfloat16, "B Hq D")])
     _check(load().paged_decode_attention_append(
         q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
-        block_table.data_ptr(), context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n,
-        block_table.shape[1], ctypes.c_float(float(scale)), _stream_ptr(stream)))
+        block_table.data_ptr(), context_lens.data_ptr(), out.data_ptr(), sz["B"], sz["Hq"], sz["Hkv"], sz["D"],
+        sz["P"], sz["N"], sz["M"], ctypes.c_float(float(scale)), _stream_ptr(stream)))
     return out
 
 
@@ -286,22 +348,11 @@ def _ptr(t):
     return None if t is None else t.data_ptr()
 
 
-def _check_bf16(**tensors):
-    import torch
-    for name, t in tensors.items():
-        if t is None:
-            continue
-        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous bf16 GPU tensor")
-
-
 def pack_weights(w, stream=None):
     """Pack a bf16 [rows, cols] weight into the prelude's tile order; returns
     a new tensor of the same shape holding the packed data."""
     import torch
-    _check_bf16(w=w)
-    if w.dim() != 2:
-        raise ValueError("w must be 2-D")
+    _validate([("w", w, torch.bfloat16, "R C")])
     out = torch.empty_like(w)
     _check(load().pda_pack_weights(w.data_ptr(), out.data_ptr(), w.shape[0], w.shape[1], _stream_ptr(stream)))
     return out
@@ -312,14 +363,30 @@ def prelude_dims(batch, hidden, hq, hkv, d, rotary_dim, interleaved, theta, eps)
                        float(theta), float(eps))
 
 
+def _prelude_specs(x, w_packed, context_lens, q_out, bias, q_norm, k_norm):
+    import torch
+    if (q_norm is None) != (k_norm is None):
+        raise ValueError("q_norm and k_norm must both be given or both be None")
+    bf = torch.bfloat16
+    return [("x", x, bf, "B H"), ("w_packed", w_packed, bf, "N H"), ("context_lens", context_lens, torch.int32, "B"),
+            ("q_out", q_out, bf, "B Hq D"), ("bias", bias, bf, "N"), ("q_norm", q_norm, bf, "D"),
+            ("k_norm", k_norm, bf, "D")]
+
+
 def attention_prelude(x, w_packed, context_lens, q_out, k_out, v_out, *, num_q_heads, num_kv_heads, head_dim,
                       rope_theta, rotary_dim=None, interleaved=False, bias=None, q_norm=None, k_norm=None,
                       eps=1e-6, stream=None):
     """QKV projection + optional per-head Q/K RMSNorm + RoPE of this step's
-    token (x: bf16 [B, H]; w_packed from :func:`pack_weights`)."""
-    _check_bf16(x=x, w_packed=w_packed, q_out=q_out, k_out=k_out, v_out=v_out, bias=bias, q_norm=q_norm,
-                k_norm=k_norm)
-    dims = prelude_dims(x.shape[0], x.shape[1], num_q_heads, num_kv_heads, head_dim,
+    token (x: bf16 [B, H]; w_packed [(Hq + 2 Hkv) D, H] from
+    :func:`pack_weights`; context_lens int32 [B]; q_out [B, Hq, D]; k_out,
+    v_out [B, Hkv, D]; bias [(Hq + 2 Hkv) D]; q_norm, k_norm [D])."""
+    import torch
+    known = dict(Hq=int(num_q_heads), Hkv=int(num_kv_heads), D=int(head_dim),
+                 N=(int(num_q_heads) + 2 * int(num_kv_heads)) * int(head_dim))
+    sz = _validate(_prelude_specs(x, w_packed, context_lens, q_out, bias, q_norm, k_norm) +
+                   [("k_out", k_out, torch.bfloat16, "B Hkv D"), ("v_out", v_out, torch.bfloat16, "B Hkv D")],
+                   known)
+    dims = prelude_dims(sz["B"], sz["H"], num_q_heads, num_kv_heads, head_dim,
                         head_dim if rotary_dim is None else rotary_dim, interleaved, rope_theta, eps)
     _check(load().pda_attention_prelude(x.data_ptr(), w_packed.data_ptr(), _ptr(bias), _ptr(q_norm), _ptr(k_norm),
                                         context_lens.data_ptr(), q_out.data_ptr(), k_out.data_ptr(),
@@ -330,16 +397,21 @@ def attention_prelude_append(x, w_packed, context_lens, q_out, k_cache, v_cache,
                              num_kv_heads, head_dim, rope_theta, rotary_dim=None, interleaved=False, bias=None,
                              q_norm=None, k_norm=None, eps=1e-6, stream=None):
     """The prelude with the KV append fused in: k, v go straight to their
-    page slot at position context_lens[b] - 1."""
-    _check_bf16(x=x, w_packed=w_packed, q_out=q_out, k_cache=k_cache, v_cache=v_cache, bias=bias, q_norm=q_norm,
-                k_norm=k_norm)
-    dims = prelude_dims(x.shape[0], x.shape[1], num_q_heads, num_kv_heads, head_dim,
+    page slot at position context_lens[b] - 1 (caches [N, P, Hkv, D],
+    block_table int32 [B, maxp]; other arguments as for
+    :func:`attention_prelude`)."""
+    import torch
+    known = dict(Hq=int(num_q_heads), Hkv=int(num_kv_heads), D=int(head_dim),
+                 N=(int(num_q_heads) + 2 * int(num_kv_heads)) * int(head_dim))
+    sz = _validate(_prelude_specs(x, w_packed, context_lens, q_out, bias, q_norm, k_norm) +
+                   [("k_cache", k_cache, torch.bfloat16, "Np P Hkv D"), ("v_cache", v_cache, torch.bfloat16, "Np P Hkv D"),
+                    ("block_table", block_table, torch.int32, "B M")], known)
+    dims = prelude_dims(sz["B"], sz["H"], num_q_heads, num_kv_heads, head_dim,
                         head_dim if rotary_dim is None else rotary_dim, interleaved, rope_theta, eps)
-    n, p = k_cache.shape[0], k_cache.shape[1]
     _check(load().pda_attention_prelude_append(
         x.data_ptr(), w_packed.data_ptr(), _ptr(bias), _ptr(q_norm), _ptr(k_norm), context_lens.data_ptr(),
-        q_out.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), p, n,
-        block_table.shape[1], ctypes.byref(dims), _stream_ptr(stream)))
+        q_out.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), sz["P"], sz["Np"],
+        sz["M"], ctypes.byref(dims), _stream_ptr(stream)))
 
 
 def prelude_workspace_reserve(dims: PreludeDims, stream=None) -> None:
@@ -409,16 +481,14 @@ def o_proj_residual_norm(attn, w_packed, residual, norm_w, residual_out, normed_
     """z = W_o attn + residual -> residual_out (bf16); RMSNorm(z) * norm_w ->
     normed_out.  attn [B, K], w_packed [H, K] from :func:`pack_weights`,
     residual / outputs [B, H], norm_w [H]; residual_out may be residual."""
-    _check_bf16(attn=attn, w_packed=w_packed, residual=residual, norm_w=norm_w, residual_out=residual_out,
-                normed_out=normed_out)
-    b, k = attn.shape
-    h = w_packed.shape[0]
-    if w_packed.shape[1] != k or residual.shape != (b, h) or residual_out.shape != (b, h) or \
-            normed_out.shape != (b, h) or norm_w.shape != (h,):
-        raise ValueError("inconsistent o_proj shapes")
+    import torch
+    bf = torch.bfloat16
+    sz = _validate([("attn", attn, bf, "B K"), ("w_packed", w_packed, bf, "H K"), ("residual", residual, bf, "B H"),
+                    ("norm_w", norm_w, bf, "H"), ("residual_out", residual_out, bf, "B H"),
+                    ("normed_out", normed_out, bf, "B H")])
     _check(load().pda_o_proj_residual_norm(attn.data_ptr(), w_packed.data_ptr(), residual.data_ptr(),
-                                           norm_w.data_ptr(), residual_out.data_ptr(), normed_out.data_ptr(), b, k,
-                                           h, ctypes.c_float(float(eps)), _stream_ptr(stream)))
+                                           norm_w.data_ptr(), residual_out.data_ptr(), normed_out.data_ptr(), sz["B"],
+                                           sz["K"], sz["H"], ctypes.c_float(float(eps)), _stream_ptr(stream)))
 
 
 def o_proj_workspace_reserve(batch, in_features, hidden, stream=None) -> None:
@@ -436,5 +506,7 @@ def profile_read_o_proj() -> Tuple[float, float, int]:
 def validate_paging(block_table, context_lens, num_pages, page_size, stream=None) -> None:
     """Check the device page table and lengths on the host (synchronises);
     raises PdaError naming the first bad entry."""
+    import torch
+    _validate([("block_table", block_table, torch.int32, "B M"), ("context_lens", context_lens, torch.int32, "B")])
     _check(load().pda_validate_paging(block_table.data_ptr(), context_lens.data_ptr(), block_table.shape[0],
                                       block_table.shape[1], page_size, num_pages, _stream_ptr(stream)))

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -348,6 +349,49 @@ int maybe_validate(const int32_t* block_table, const int32_t* context_lens, int3
   return validate_paging(block_table, context_lens, batch, maxp, page_size, num_pages, st);
 }
 
+
+// ---------------------------------------------------------------- descriptors
+const char* dtype_name(int32_t dt) {
+  switch (dt) {
+    case PDA_DTYPE_BF16: return "bf16";
+    case PDA_DTYPE_F16: return "fp16";
+    case PDA_DTYPE_F32: return "fp32";
+    case PDA_DTYPE_I32: return "int32";
+    case PDA_DTYPE_I64: return "int64";
+    default: return "unknown";
+  }
+}
+
+// Rank and extents of one descriptor (not NULL).
+int check_rank(const pda_tensor& t, const char* name, int32_t ndim) {
+  if (t.ndim != ndim) return fail(PDA_ERR_SHAPE, "%s: %d dimensions, expected %d", name, t.ndim, ndim);
+  for (int i = 0; i < ndim; ++i)
+    if (t.shape[i] < 0 || t.shape[i] > INT32_MAX)
+      return fail(PDA_ERR_SHAPE, "%s: extent %lld of dimension %d out of range", name,
+                  static_cast<long long>(t.shape[i]), i);
+  return PDA_OK;
+}
+
+bool desc_empty(const pda_tensor& t) {
+  for (int i = 0; i < t.ndim; ++i)
+    if (t.shape[i] == 0) return true;
+  return false;
+}
+
+// Dense row-major strides (extent-1 dimensions and empty tensors excepted).
+int check_dense(const pda_tensor& t, const char* name) {
+  if (desc_empty(t)) return PDA_OK;
+  int64_t want = 1;
+  for (int i = t.ndim - 1; i >= 0; --i) {
+    if (t.shape[i] != 1 && t.stride[i] != want)
+      return fail(PDA_ERR_LAYOUT, "%s: stride %lld in dimension %d, a dense row-major tensor has %lld", name,
+                  static_cast<long long>(t.stride[i]), i, static_cast<long long>(want));
+    if (want > (int64_t{1} << 50) / (t.shape[i] > 0 ? t.shape[i] : 1))
+      return fail(PDA_ERR_SHAPE, "%s: too many elements", name);
+    want *= t.shape[i];
+  }
+  return PDA_OK;
+}
 
 // ---------------------------------------------------------------- prelude
 bool misaligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
@@ -785,6 +829,47 @@ int paged_decode_attention_noalloc(const void* q, const void* k_cache, const voi
                                    void* stream) {
   return attention_call(q, k_cache, v_cache, block_table, context_lens, out, batch, num_q_heads, num_kv_heads,
                         head_dim, page_size, num_pages, max_pages_per_seq, 1, 0, scale, stream, true);
+}
+
+int paged_decode_attention_desc(const pda_tensor* q, const pda_tensor* k_cache, const pda_tensor* v_cache,
+                                const pda_tensor* block_table, const pda_tensor* context_lens,
+                                const pda_tensor* out, float scale, void* stream) {
+  g_err.clear();
+  const pda_tensor* ts[6] = {q, k_cache, v_cache, block_table, context_lens, out};
+  static const char* const names[6] = {"q", "k_cache", "v_cache", "block_table", "context_lens", "out"};
+  static const int32_t dtypes[6] = {PDA_DTYPE_BF16, PDA_DTYPE_BF16, PDA_DTYPE_BF16,
+                                    PDA_DTYPE_I32,  PDA_DTYPE_I32,  PDA_DTYPE_BF16};
+  static const int32_t ranks[6] = {3, 4, 4, 2, 1, 3};
+  for (int i = 0; i < 6; ++i)
+    if (!ts[i]) return fail(PDA_ERR_NULL, "%s: descriptor is NULL", names[i]);
+  for (int i = 0; i < 6; ++i)
+    if (ts[i]->dtype != dtypes[i])
+      return fail(PDA_ERR_DTYPE, "%s: dtype %s (%d), expected %s", names[i], dtype_name(ts[i]->dtype),
+                  ts[i]->dtype, dtype_name(dtypes[i]));
+  int rc;
+  for (int i = 0; i < 6; ++i)
+    if ((rc = check_rank(*ts[i], names[i], ranks[i]))) return rc;
+  const int64_t* qs = q->shape;
+  const int64_t* ks = k_cache->shape;
+  for (int i = 0; i < 3; ++i)
+    if (out->shape[i] != qs[i]) return fail(PDA_ERR_SHAPE, "out must have the shape of q");
+  for (int i = 0; i < 4; ++i)
+    if (v_cache->shape[i] != ks[i]) return fail(PDA_ERR_SHAPE, "v_cache must have the shape of k_cache");
+  if (ks[3] != qs[2])
+    return fail(PDA_ERR_SHAPE, "head_dim of q (%lld) and of the caches (%lld) differ", static_cast<long long>(qs[2]),
+                static_cast<long long>(ks[3]));
+  if (block_table->shape[0] != qs[0] || context_lens->shape[0] != qs[0])
+    return fail(PDA_ERR_SHAPE, "block_table and context_lens must have one row per sequence of q (%lld)",
+                static_cast<long long>(qs[0]));
+  for (int i = 0; i < 6; ++i)
+    if ((rc = check_dense(*ts[i], names[i]))) return rc;
+  for (int i = 0; i < 6; ++i)
+    if (!desc_empty(*ts[i]) && !ts[i]->data) return fail(PDA_ERR_NULL, "%s: data is NULL", names[i]);
+  return attention_call(q->data, k_cache->data, v_cache->data, static_cast<const int32_t*>(block_table->data),
+                        static_cast<const int32_t*>(context_lens->data), out->data, static_cast<int32_t>(qs[0]),
+                        static_cast<int32_t>(qs[1]), static_cast<int32_t>(ks[2]), static_cast<int32_t>(qs[2]),
+                        static_cast<int32_t>(ks[1]), static_cast<int32_t>(ks[0]),
+                        static_cast<int32_t>(block_table->shape[1]), 1, 0, scale, stream, false);
 }
 
 int pda_pack_weights(const void* w, void* w_packed, int32_t rows, int32_t cols, void* stream) {

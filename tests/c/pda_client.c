@@ -4,7 +4,9 @@
  * runtime's C API and no Python or torch anywhere.
  *
  *   pda_client errors     argument checks that return before any HIP call
- *                         (runs without a GPU); prints "ok <check>" lines
+ *                         (runs without a GPU), for the pointer and the
+ *                         tensor-descriptor entry points; prints "ok <check>"
+ *                         lines
  *   pda_client run DIR    decode attention on the device: reads DIR/meta.txt
  *                         ("batch hq hkv head_dim page_size num_pages maxp
  *                         scale") and the raw little-endian arrays DIR/q.bin,
@@ -40,6 +42,77 @@ static void expect(const char* what, int got, int want) {
   }
 }
 
+/* A dense row-major descriptor of `ndim` extents. */
+static pda_tensor desc(void* data, int32_t dtype, int32_t ndim, const int64_t* shape) {
+  pda_tensor t;
+  memset(&t, 0, sizeof t);
+  t.data = data;
+  t.dtype = dtype;
+  t.ndim = ndim;
+  int64_t acc = 1;
+  for (int i = ndim - 1; i >= 0; --i) {
+    t.shape[i] = shape[i];
+    t.stride[i] = acc;
+    acc *= shape[i];
+  }
+  return t;
+}
+
+/* The descriptor entry point with one argument spoiled at a time: each
+   validation error is returned before any HIP call. */
+static void run_descriptor_errors(void* p) {
+  const int64_t qs[3] = {2, 32, 128}, ks[4] = {64, 16, 8, 128}, bs[2] = {2, 8}, ls[1] = {2};
+  const pda_tensor q = desc(p, PDA_DTYPE_BF16, 3, qs), k = desc(p, PDA_DTYPE_BF16, 4, ks);
+  const pda_tensor bt = desc(p, PDA_DTYPE_I32, 2, bs), lens = desc(p, PDA_DTYPE_I32, 1, ls);
+  pda_tensor t;
+
+  expect("desc null descriptor", paged_decode_attention_desc(NULL, &k, &k, &bt, &lens, &q, 0.088f, NULL),
+         PDA_ERR_NULL);
+  t = desc(NULL, PDA_DTYPE_BF16, 4, ks);
+  expect("desc null data", paged_decode_attention_desc(&q, &t, &k, &bt, &lens, &q, 0.088f, NULL), PDA_ERR_NULL);
+  t = desc(p, PDA_DTYPE_F16, 3, qs);
+  expect("desc fp16 q", paged_decode_attention_desc(&t, &k, &k, &bt, &lens, &q, 0.088f, NULL), PDA_ERR_DTYPE);
+  t = desc(p, PDA_DTYPE_I64, 1, ls);
+  expect("desc int64 lengths", paged_decode_attention_desc(&q, &k, &k, &bt, &t, &q, 0.088f, NULL), PDA_ERR_DTYPE);
+  t = desc(p, PDA_DTYPE_BF16, 2, qs);
+  expect("desc q rank", paged_decode_attention_desc(&t, &k, &k, &bt, &lens, &q, 0.088f, NULL), PDA_ERR_SHAPE);
+  {
+    const int64_t bs3[2] = {3, 8};
+    t = desc(p, PDA_DTYPE_I32, 2, bs3);
+    expect("desc block_table rows", paged_decode_attention_desc(&q, &k, &k, &t, &lens, &q, 0.088f, NULL),
+           PDA_ERR_SHAPE);
+  }
+  {
+    const int64_t q30[3] = {2, 30, 128};
+    t = desc(p, PDA_DTYPE_BF16, 3, q30);
+    expect("desc heads not a multiple", paged_decode_attention_desc(&t, &k, &k, &bt, &lens, &t, 0.088f, NULL),
+           PDA_ERR_SHAPE);
+  }
+  {
+    const int64_t q96[3] = {2, 32, 96}, k96[4] = {64, 16, 8, 96};
+    const pda_tensor a = desc(p, PDA_DTYPE_BF16, 3, q96), c = desc(p, PDA_DTYPE_BF16, 4, k96);
+    expect("desc head_dim 96", paged_decode_attention_desc(&a, &c, &c, &bt, &lens, &a, 0.088f, NULL),
+           PDA_ERR_UNSUPPORTED);
+  }
+  {
+    const int64_t k24[4] = {64, 24, 8, 128};
+    t = desc(p, PDA_DTYPE_BF16, 4, k24);
+    expect("desc page_size 24", paged_decode_attention_desc(&q, &t, &t, &bt, &lens, &q, 0.088f, NULL),
+           PDA_ERR_UNSUPPORTED);
+  }
+  t = q;  /* a transposed view: heads and features swapped in memory */
+  t.stride[1] = 1;
+  t.stride[2] = 32;
+  expect("desc transposed q", paged_decode_attention_desc(&t, &k, &k, &bt, &lens, &q, 0.088f, NULL),
+         PDA_ERR_LAYOUT);
+  t = bt;  /* rows of a wider table */
+  t.stride[0] = 16;
+  expect("desc padded block_table", paged_decode_attention_desc(&q, &k, &k, &t, &lens, &q, 0.088f, NULL),
+         PDA_ERR_LAYOUT);
+  expect("desc nan scale", paged_decode_attention_desc(&q, &k, &k, &bt, &lens, &q, nanf(""), NULL),
+         PDA_ERR_SCALE);
+}
+
 static int run_errors(void) {
   /* Any 16-byte aligned non-NULL address: these calls must reject their
      arguments before touching memory or the device. */
@@ -70,6 +143,7 @@ static int run_errors(void) {
     ++failures;
   }
   expect("version", pda_version(), PDA_VERSION);
+  run_descriptor_errors(p);
 
   int32_t grid = 0, waves = 0;
   int64_t ws = 0;

@@ -2,6 +2,7 @@
 declares, and rejects bad arguments with the documented codes before making
 any HIP call (none of these calls touches a device)."""
 import ctypes
+import re
 import math
 
 import pytest
@@ -332,3 +333,184 @@ def test_validate_paging_argument_errors(lib):
     assert f(16, 16, 2, 0, 16, 64, None) == SHAPE
     assert f(0, 16, 2, 8, 16, 64, None) == NULL
     assert f(0, 0, 0, 8, 16, 64, None) == OK
+
+
+# ------------------------------------------------- tensor-descriptor entry
+DTYPE, LAYOUT = 7, 8
+BF, F16, F32, I32, I64 = B.DTYPE_BF16, B.DTYPE_F16, B.DTYPE_F32, B.DTYPE_I32, B.DTYPE_I64
+
+
+def _descs(batch=2, hq=32, hkv=8, d=128, p=16, n=64, maxp=8, ptr=0x1000):
+    T = B.tensor_desc
+    return dict(q=T(ptr, BF, (batch, hq, d)), k=T(ptr, BF, (n, p, hkv, d)), v=T(ptr, BF, (n, p, hkv, d)),
+                bt=T(ptr, I32, (batch, maxp)), lens=T(ptr, I32, (batch,)), out=T(ptr, BF, (batch, hq, d)))
+
+
+def desc_call(scale=0.088, **replace):
+    ds = _descs(**{k: replace.pop(k) for k in list(replace) if k in ("batch", "hq", "hkv", "d", "p", "n", "maxp")})
+    ds.update(replace)
+    return B.desc_call(ds["q"], ds["k"], ds["v"], ds["bt"], ds["lens"], ds["out"], scale)
+
+
+T = B.tensor_desc
+DESC_ERRORS = [
+    # a missing descriptor, or a non-empty tensor without data
+    (dict(q=None), NULL, "q: descriptor is NULL"),
+    (dict(lens=None), NULL, "context_lens: descriptor is NULL"),
+    (dict(k=T(0, BF, (64, 16, 8, 128))), NULL, "k_cache: data is NULL"),
+    # element types: nothing is converted
+    (dict(q=T(0x1000, F16, (2, 32, 128))), DTYPE, "q: dtype fp16"),
+    (dict(v=T(0x1000, F32, (64, 16, 8, 128))), DTYPE, "v_cache: dtype fp32"),
+    (dict(lens=T(0x1000, I64, (2,))), DTYPE, "context_lens: dtype int64"),
+    (dict(bt=T(0x1000, BF, (2, 8))), DTYPE, "block_table: dtype bf16"),
+    (dict(out=T(0x1000, 99, (2, 32, 128))), DTYPE, "out: dtype unknown"),
+    # ranks, extents and their agreement
+    (dict(q=T(0x1000, BF, (2, 4096))), SHAPE, "q: 2 dimensions"),
+    (dict(q=T(0x1000, BF, (2, -32, 128))), SHAPE, "out of range"),
+    (dict(out=T(0x1000, BF, (2, 32, 64))), SHAPE, "out must have the shape of q"),
+    (dict(v=T(0x1000, BF, (64, 16, 4, 128))), SHAPE, "v_cache must have the shape of k_cache"),
+    (dict(k=T(0x1000, BF, (64, 16, 8, 64)), v=T(0x1000, BF, (64, 16, 8, 64))), SHAPE, "head_dim"),
+    (dict(bt=T(0x1000, I32, (3, 8))), SHAPE, "one row per sequence"),
+    (dict(lens=T(0x1000, I32, (1,))), SHAPE, "one row per sequence"),
+    (dict(hq=30), SHAPE, "multiple"),
+    (dict(n=0), SHAPE, "num_pages"),
+    # supported set
+    (dict(d=96), UNSUPPORTED, "head_dim"),
+    (dict(p=24), UNSUPPORTED, "page_size"),
+    (dict(hq=64, hkv=2), UNSUPPORTED, "group"),
+    # layouts: transposed, sliced and padded views
+    (dict(q=T(0x1000, BF, (2, 32, 128), (4096, 1, 32))), LAYOUT, "q: stride"),
+    (dict(k=T(0x1000, BF, (64, 16, 8, 128), (16 * 8 * 128, 128, 16 * 128, 1))), LAYOUT, "k_cache: stride"),
+    (dict(bt=T(0x1000, I32, (2, 8), (16, 1))), LAYOUT, "block_table: stride"),
+    (dict(lens=T(0x1000, I32, (2,), (2,))), LAYOUT, "context_lens: stride"),
+    (dict(out=T(0x1000, BF, (2, 32, 128), (8192, 256, 1))), LAYOUT, "out: stride"),
+    # the rest of the pointer entry point's checks
+    (dict(scale=float("nan")), SCALE, "finite"),
+    (dict(q=T(0x1008, BF, (2, 32, 128))), ALIGN, "16-byte"),
+]
+
+
+@pytest.mark.parametrize("kwargs,code,text", DESC_ERRORS, ids=[f"{e[1]}-{e[2]}" for e in DESC_ERRORS])
+def test_descriptor_errors(lib, kwargs, code, text):
+    rc = desc_call(**kwargs)
+    assert rc == code, B.last_error()
+    assert text in B.last_error()
+
+
+def test_descriptor_extent_one_and_empty_tensors_have_no_layout(lib):
+    # the stride of an extent-1 dimension is not looked at, and an empty
+    # batch (no data pointers needed) returns before any HIP call
+    q = T(0x1000, BF, (1, 32, 128), (999, 128, 1))
+    assert desc_call(batch=1, q=q, out=T(0x1000, BF, (1, 32, 128), (7, 128, 1)), scale=float("nan")) == SCALE
+    e = _descs(batch=0, ptr=0)
+    e["k"], e["v"] = T(0x1000, BF, (64, 16, 8, 128)), T(0x1000, BF, (64, 16, 8, 128))
+    assert B.desc_call(e["q"], e["k"], e["v"], e["bt"], e["lens"], e["out"], 0.088) == OK
+    assert B.last_error() == ""
+
+
+# ------------------------------------------- binding argument checks (CPU)
+# CPU tensors: with every shape and dtype right, a wrapper stops at "must be
+# a GPU tensor"; a wrong shape or dtype is reported before that, so each bad
+# argument raises before any launch whichever it is.
+def _t(*shape, dtype=None):
+    import torch
+    return torch.zeros(shape, dtype=dtype or torch.bfloat16)
+
+
+def _i32(*shape):
+    import torch
+    return torch.zeros(shape, dtype=torch.int32)
+
+
+def _prelude_args(**over):
+    # B 2, H 64, Hq 4, Hkv 2, D 64: N = (4 + 4) * 64 = 512
+    a = dict(x=_t(2, 64), w_packed=_t(512, 64), context_lens=_i32(2), q_out=_t(2, 4, 64), k_out=_t(2, 2, 64),
+             v_out=_t(2, 2, 64), bias=_t(512), q_norm=_t(64), k_norm=_t(64))
+    a.update(over)
+    return a
+
+
+PRELUDE_BAD = [
+    (dict(w_packed=_t(448, 64)), "w_packed must be [N, H] with N = 512"),
+    (dict(x=_t(2, 96)), "w_packed must be [N, H] with H = 96"),
+    (dict(q_out=_t(2, 4, 32)), "q_out must be [B, Hq, D] with D = 64"),
+    (dict(k_out=_t(2, 3, 64)), "k_out must be [B, Hkv, D] with Hkv = 2"),
+    (dict(v_out=_t(3, 2, 64)), "v_out must be [B, Hkv, D] with B = 2"),
+    (dict(context_lens=_i32(3)), "context_lens must be [B] with B = 2"),
+    (dict(bias=_t(500)), "bias must be [N] with N = 512"),
+    (dict(q_norm=_t(32)), "q_norm must be [D] with D = 64"),
+    (dict(x=_t(2, 1, 64)), "x must be [B, H]"),
+]
+
+
+@pytest.mark.parametrize("over,text", PRELUDE_BAD, ids=[t for _, t in PRELUDE_BAD])
+def test_prelude_binding_shape_checks(over, text):
+    a = _prelude_args(**over)
+    with pytest.raises(ValueError, match=re.escape(text)):
+        B.attention_prelude(**a, num_q_heads=4, num_kv_heads=2, head_dim=64, rope_theta=1e4)
+
+
+def test_prelude_binding_dtype_device_and_norm_pair_checks():
+    import torch
+    kw = dict(num_q_heads=4, num_kv_heads=2, head_dim=64, rope_theta=1e4)
+    with pytest.raises(TypeError, match="context_lens must be torch.int32"):
+        B.attention_prelude(**_prelude_args(context_lens=torch.zeros(2, dtype=torch.int64)), **kw)
+    with pytest.raises(TypeError, match="bias must be torch.bfloat16"):
+        B.attention_prelude(**_prelude_args(bias=torch.zeros(512)), **kw)
+    with pytest.raises(ValueError, match="both be given"):
+        B.attention_prelude(**_prelude_args(k_norm=None), **kw)
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        B.attention_prelude(**_prelude_args(), **kw)
+
+
+def test_prelude_append_binding_checks_the_caches():
+    kw = dict(num_q_heads=4, num_kv_heads=2, head_dim=64, rope_theta=1e4)
+
+    def call(**over):
+        a = _prelude_args()
+        del a["k_out"], a["v_out"]
+        a.update(k_cache=_t(10, 16, 2, 64), v_cache=_t(10, 16, 2, 64), block_table=_i32(2, 5))
+        a.update(over)
+        B.attention_prelude_append(**a, **kw)
+    with pytest.raises(ValueError, match=re.escape("k_cache must be [Np, P, Hkv, D] with Hkv = 2")):
+        call(k_cache=_t(10, 16, 4, 64))
+    with pytest.raises(ValueError, match=re.escape("v_cache must be [Np, P, Hkv, D] with P = 16")):
+        call(v_cache=_t(10, 8, 2, 64))
+    with pytest.raises(ValueError, match=re.escape("block_table must be [B, M] with B = 2")):
+        call(block_table=_i32(3, 5))
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        call()
+
+
+def test_append_then_attend_binding_checks():
+    def call(**over):
+        a = dict(q=_t(2, 8, 64), k_new=_t(2, 2, 64), v_new=_t(2, 2, 64), k_cache=_t(10, 16, 2, 64),
+                 v_cache=_t(10, 16, 2, 64), block_table=_i32(2, 5), context_lens=_i32(2), out=_t(2, 8, 64))
+        a.update(over)
+        B.paged_decode_attention_append(**a, scale=0.125)
+    with pytest.raises(ValueError, match=re.escape("block_table must be [B, M] with B = 2")):
+        call(block_table=_i32(3, 5))
+    with pytest.raises(ValueError, match=re.escape("context_lens must be [B] with B = 2")):
+        call(context_lens=_i32(1))
+    with pytest.raises(ValueError, match=re.escape("q must be [B, Hq, D]")):
+        call(q=_t(2, 1, 8, 64))
+    with pytest.raises(ValueError, match=re.escape("k_new must be [B, Hkv, D] with D = 64")):
+        call(k_new=_t(2, 2, 32))
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        call()
+
+
+def test_o_proj_and_kv_append_binding_checks():
+    def oproj(**over):
+        a = dict(attn=_t(2, 64), w_packed=_t(32, 64), residual=_t(2, 32), norm_w=_t(32), residual_out=_t(2, 32),
+                 normed_out=_t(2, 32))
+        a.update(over)
+        B.o_proj_residual_norm(**a)
+    with pytest.raises(ValueError, match=re.escape("w_packed must be [H, K] with K = 64")):
+        oproj(w_packed=_t(32, 96))
+    with pytest.raises(ValueError, match=re.escape("norm_w must be [H] with H = 32")):
+        oproj(norm_w=_t(16))
+    with pytest.raises(ValueError, match="must be a GPU tensor"):
+        oproj()
+    with pytest.raises(ValueError, match=re.escape("v_new must be [B, Hkv, D] with Hkv = 2")):
+        B.kv_append(_t(2, 2, 64), _t(2, 1, 64), _t(10, 16, 2, 64), _t(10, 16, 2, 64), _i32(2, 5), _i32(2))

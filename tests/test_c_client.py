@@ -42,6 +42,11 @@ def test_c_client_argument_checks(client):
     assert res.returncode == 0, res.stdout + res.stderr
     for what in ("null q", "head_dim 96", "misaligned q", "nan scale", "empty batch", "version", "plan shape"):
         assert f"ok {what}" in res.stdout, res.stdout
+    # every validation error of the descriptor entry point, forced from C
+    for what in ("null descriptor", "null data", "fp16 q", "int64 lengths", "q rank", "block_table rows",
+                 "heads not a multiple", "head_dim 96", "page_size 24", "transposed q", "padded block_table",
+                 "nan scale"):
+        assert f"ok desc {what}" in res.stdout, res.stdout
 
 
 @pytest.mark.gpu

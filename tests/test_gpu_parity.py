@@ -487,3 +487,31 @@ def test_window_pre_window_slots_of_a_live_page_are_not_read(lib, d):
     got = run_ext(lib, w)
     r = oracle.attend_masked(w.q[:, None], w.k_cache, w.v_cache, w.block_table, w.context_lens, w.scale, window)[0]
     check(got, r, f"pre-window NaN D={d}")
+
+
+# --------------------------------------------- tensor-descriptor entry point
+def test_descriptor_entry_matches_pointer_entry(lib):
+    # the same call through pda_tensor descriptors: bitwise the pointer
+    # entry's output; a transposed view of q, an fp16 q and an int64 length
+    # vector are refused by the library with out untouched
+    import torch
+    w = W.build([1, 33, 700, 0, 4099], 32, 8, 128, 16, seed=150, pool="holes:0.2")
+    dev = to_gpu(w)
+    a = run(lib, w, dev)
+    out = torch.full(tuple(w.q.shape), float("nan"), dtype=torch.bfloat16, device="cuda")
+    lib.paged_decode_attention_desc(dev["q"], dev["k"], dev["v"], dev["bt"], dev["lens"], out, float(w.scale))
+    torch.cuda.synchronize()
+    assert np.array_equal(out.float().cpu().numpy().astype(np.float64), a)
+    check(a, ref(w), "descriptor entry")
+    out.fill_(3.0)
+    qt = dev["q"].transpose(1, 2).contiguous().transpose(1, 2)  # [B, Hq, D] view with permuted strides
+    bad = [(dict(q=qt), 8), (dict(q=dev["q"].to(torch.float16)), 7), (dict(lens=dev["lens"].to(torch.int64)), 7)]
+    for repl, code in bad:
+        args = dict(q=dev["q"], k=dev["k"], v=dev["v"], bt=dev["bt"], lens=dev["lens"])
+        args.update(repl)
+        with pytest.raises(lib.PdaError) as ei:
+            lib.paged_decode_attention_desc(args["q"], args["k"], args["v"], args["bt"], args["lens"], out,
+                                            float(w.scale))
+        assert ei.value.code == code, str(ei.value)
+    torch.cuda.synchronize()
+    assert bool((out == 3.0).all())
