@@ -45,6 +45,9 @@ def parse():
                     help="attention products on the matrix cores (default) or the vector-ALU variant "
                          "(the measured alternative; head_dim 128 and <= 8 columns per kv head)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extra", default="batched,ragged",
+                    help="comma-separated workloads timed in the same run after the headline one and reported "
+                         "under extra_workloads (with the default long70b headline only; '' for none)")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM traffic per launch (from rocprofv3 --pmc runs)")
@@ -436,7 +439,77 @@ def main():
     }
     if cpu is not None:
         res["cpu_baseline"] = cpu
+    extra = [x for x in args.extra.split(",") if x] if args.workload == "long70b" and not variant else []
+    if extra:
+        del q, k, v, bt, lens, out, bts, warm_call_bt
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        res["extra_workloads"] = {name: extra_workload(name, args, torch, pda, stream_ref["gbs"]) for name in extra}
     print(json.dumps(res), flush=True)
+
+
+def extra_workload(name, args, torch, pda, stream_gbs):
+    """One more attention workload timed in the same run: `steps` calls
+    between events on the launch stream after `warmup` calls, then the
+    library's per-kernel events over another `steps` calls."""
+    import workloads as W
+    t_gen = time.perf_counter()
+    w = W.make(name, poison=False)
+    print(f"[bench] generated {name} in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
+    dev = torch.device("cuda:0")
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    q, k, v = bf(w.q), bf(w.k_cache), bf(w.v_cache)
+    bt = torch.from_numpy(w.block_table).to(dev)
+    lens = torch.from_numpy(w.context_lens).to(dev)
+    out = torch.empty(tuple(w.q.shape), dtype=torch.bfloat16, device=dev)
+    scale = float(w.scale)
+    stream = torch.cuda.current_stream()
+    kv_bytes = 2 * k.numel() * k.element_size()
+    assert kv_bytes >= 512 * 2 ** 20, f"{name}: KV fits in the last-level cache; time it with --workload"
+
+    def call():
+        pda.paged_decode_attention(q, k, v, bt, lens, out, scale)
+
+    for _ in range(args.warmup):
+        call()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    pda.profile_enable(True)
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    split_ms, merge_ms, n = pda.profile_read()
+    pda.profile_enable(False)
+    split_us = split_ms / max(n, 1) * 1e3
+    merge_us = merge_ms / max(n, 1) * 1e3
+    nbytes = w.algorithmic_bytes()
+    achieved = nbytes / (split_us * 1e-6) / 1e9
+    res = {
+        "us_per_call": round(us, 2),
+        "gbs_per_call": round(nbytes / (us * 1e-6) / 1e9, 1),
+        "frac_of_peak_per_call": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+        "kernels_us": {"split": round(split_us, 2), "merge": round(merge_us, 2)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "frac_of_stream_read": round(achieved / stream_gbs, 4)},
+        "config": {"batch": w.batch, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
+                   "head_dim": w.head_dim, "page_size": w.page_size,
+                   "total_context_tokens": int(w.context_lens.astype(np.int64).sum()), "algorithmic_bytes": nbytes},
+    }
+    del q, k, v, bt, lens, out
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
 
 
 def prelude_main(args):
