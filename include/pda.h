@@ -292,7 +292,8 @@ int paged_decode_attention_noalloc(const void* q, const void* k_cache, const voi
  * batch is spread over waves (the paper's split across CTAs, sized here to
  * fill the given number of compute units).  No HIP call.
  *   num_cus      compute units of the target device (256 on MI355X).
- *   grid_blocks  out: workgroups of the split kernel.
+ *   grid_blocks  out: workgroups of the split kernel (one query token per
+ *                sequence, the plan paged_decode_attention makes).
  *   waves        out: waves (workers) in that grid.
  *   workspace_bytes out: device workspace a call with this shape may need,
  *                for any num_queries of paged_decode_attention_ext.
@@ -365,6 +366,20 @@ int32_t pda_version(void);
  *                          head; other shapes fail with PDA_ERR_UNSUPPORTED
  *                          while it is selected.  Outputs of the two paths
  *                          agree within the attention tolerance, not bitwise.
+ *   PDA_OPT_FUSED_MERGE    0 (default, env PDA_FUSED_MERGE): split
+ *                          sequences are merged by a second kernel.
+ *                          1: plans with little partial data per sequence
+ *                          (small batches, single requests) merge inside
+ *                          the attention kernel, by the last workgroup to
+ *                          finish each sequence, with one kv head per
+ *                          workgroup if that is what it takes (measured
+ *                          slower than the merge kernel on MI355X: the
+ *                          in-kernel hand-off costs more than a launch);
+ *                          2: every plan with several workgroups merges in
+ *                          the attention kernel, with the default kv-head
+ *                          grouping (for tests: slow for long contexts).
+ *                          All are deterministic for a fixed plan; they
+ *                          round differently.
  * Options are process-wide and apply to later calls.  pda_set_option
  * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
  * returns the current value or -1 for an unknown option.
@@ -372,6 +387,7 @@ int32_t pda_version(void);
 #define PDA_OPT_BLOCKS_PER_CU 1
 #define PDA_OPT_MIN_STEPS 2
 #define PDA_OPT_COMPUTE_PATH 3
+#define PDA_OPT_FUSED_MERGE 4
 int pda_set_option(int32_t option, int32_t value);
 int32_t pda_get_option(int32_t option);
 

@@ -437,6 +437,7 @@ def release_workspaces() -> None:
 OPT_BLOCKS_PER_CU = 1
 OPT_MIN_STEPS = 2
 OPT_COMPUTE_PATH = 3  # 0 = matrix cores (default), 1 = vector ALU (the measured alternative)
+OPT_FUSED_MERGE = 4   # 0 = merge kernel (default), 1 = fused merge for small plans, 2 = every multi-workgroup plan
 
 
 def set_option(option: int, value: int) -> None:

@@ -3,6 +3,7 @@
 // and optional event timing.  The kernels live in pda_kernels.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <climits>
 #include <cmath>
@@ -55,6 +56,7 @@ constexpr int kMaxMinSteps = 1 << 30;
 std::atomic<int> g_blocks_per_cu{-1};
 std::atomic<int> g_min_steps{-1};
 std::atomic<int> g_compute_path{-1};
+std::atomic<int> g_fused_merge{-1};
 
 int blocks_per_cu() {
   int v = g_blocks_per_cu.load();
@@ -78,6 +80,15 @@ int compute_path() {
   if (v < 0) {
     v = env_int("PDA_COMPUTE_PATH", 0, 0, 1);
     g_compute_path.store(v);
+  }
+  return v;
+}
+
+int fused_merge() {
+  int v = g_fused_merge.load();
+  if (v < 0) {
+    v = env_int("PDA_FUSED_MERGE", 0, 0, 2);
+    g_fused_merge.store(v);
   }
   return v;
 }
@@ -139,6 +150,7 @@ struct Plan {
   int grid = 0;
   int waves = 0;   // per workgroup
   int hgs = 0;     // kv heads per workgroup
+  bool fused = false;  // split sequences merged by their last workgroup
   int64_t slots = 0;
   int64_t off_acc = 0, off_ml = 0, off_pref = 0, bytes = 0;
 };
@@ -153,16 +165,16 @@ int heads_per_group(int hkv, int max_waves) {
   return 1;
 }
 
-// Workgroups: one wave per kv head of a group, times step phases up to
-// max_waves(d) waves (8; 4 at D = 256); as many workgroups as fill the device (blocks_per_cu per CU), but
-// none with fewer than min_steps 32-token steps per wave at the largest
-// context the page table allows.  Partial slots: one per (workgroup,
-// sequence piece), at most grid + batch * kv-head groups, each holding `cols`
-// (query token, head) rows per kv head.
-Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
+// Workgroups: one wave per kv head of a group of hgs, times step phases up
+// to max_waves(d) waves (8; 4 at D = 256); as many workgroups as fill the
+// device (blocks_per_cu per CU), but none with fewer than min_steps 32-token
+// steps per wave at the largest context the page table allows.  Partial
+// slots: one per (workgroup, sequence piece), at most grid + batch * kv-head
+// groups, each holding `cols` (query token, head) rows per kv head.
+Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
   Plan pl;
   const int max_waves = pda::max_waves(d);
-  pl.hgs = heads_per_group(hkv, max_waves);
+  pl.hgs = hgs;
   const int phases = max_waves / pl.hgs;
   pl.waves = pl.hgs * phases;
   const int64_t ngroups = hkv / pl.hgs;
@@ -182,6 +194,46 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   // steps prefix [batch + 1], then the split list [grid] (see the kernels)
   pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1 + pl.grid) * 4);
   return pl;
+}
+
+// The plan of a call.  The default reads all kv heads of a group of up to 8
+// together (the faster access order for long streams) and merges split
+// sequences in a separate kernel.  With PDA_OPT_FUSED_MERGE = 1, a grid of
+// several workgroups with little partial data per sequence merges inside
+// the attention kernel instead: with the largest kv-head group for which
+// the most partial data one sequence can have, grid x hgs x cols x d fp32,
+// fits pda::kFusedMergeBytes (a single request then takes one kv head per
+// workgroup).  On MI355X the in-kernel hand-off (write-through stores, their
+// acknowledgement, the arrival atomic, coherent reloads) costs more than
+// the merge kernel's launch, so the option is off by default.
+Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
+  const Plan dflt = plan_for(heads_per_group(hkv, pda::max_waves(d)), batch, hkv, d, p, maxp, num_cus, cols);
+  // (the vector-ALU variant, a measurement aid, keeps the merge kernel)
+  if (dflt.grid == 1 || !fused_merge() || compute_path() != 0) return dflt;
+  if (fused_merge() == 2) {  // every plan that has something to merge (tests)
+    Plan c = dflt;
+    c.fused = c.grid <= pda::kMaxFusedGrid && c.bytes < (int64_t{1} << 31);
+    return c;
+  }
+  for (int h = dflt.hgs; h >= 1; --h) {
+    if (hkv % h) continue;
+    Plan c = plan_for(h, batch, hkv, d, p, maxp, num_cus, cols);
+    const int64_t most = static_cast<int64_t>(c.grid) * h * cols * d * 4;
+    if (c.grid > 1 && c.grid <= pda::kMaxFusedGrid && most <= pda::kFusedMergeBytes && c.bytes < (int64_t{1} << 31)) {
+      c.fused = true;
+      return c;
+    }
+  }
+  return dflt;
+}
+
+// Workspace that any call of this shape may need: the largest plan over
+// every kv-head group size make_plan can pick, at 16 columns per kv head.
+int64_t reserve_bytes(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus) {
+  int64_t most = 0;
+  for (int h = 1; h <= pda::max_waves(d); ++h)
+    if (hkv % h == 0) most = std::max(most, plan_for(h, batch, hkv, d, p, maxp, num_cus, pda::kMaxCols).bytes);
+  return most;
 }
 
 int device_cus(int dev, int* cus) {
@@ -206,6 +258,7 @@ int device_cus(int dev, int* cus) {
 struct Workspace {
   void* ptr = nullptr;
   int64_t bytes = 0;
+  int32_t* cnt = nullptr;  // arrival counters of the fused merge, zero between calls
 };
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
@@ -237,6 +290,32 @@ int workspace_for(int dev, hipStream_t st, int64_t need, void** out) {
   }
   ws.bytes = grow;
   *out = ws.ptr;
+  return PDA_OK;
+}
+
+// The fused merge's arrival counters of (device, stream): a buffer of their
+// own (the GEMV calls share the workspace), cleared once when allocated;
+// every call leaves them at zero.
+int counters_for(int dev, hipStream_t st, int32_t** out) {
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  Workspace& ws = g_ws[{dev, st}];
+  if (!ws.cnt) {
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(st, &cap);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+    if (cap != hipStreamCaptureStatusNone)
+      return fail(PDA_ERR_HIP, "the merge counters must be allocated while the stream is being captured; "
+                  "call pda_workspace_reserve before capture");
+    void* p = nullptr;
+    const size_t bytes = static_cast<size_t>(pda::kMaxFusedGrid) * sizeof(int32_t);
+    if ((e = hipMalloc(&p, bytes)) != hipSuccess) return hip_fail(e, "hipMalloc(merge counters)");
+    if ((e = hipMemsetAsync(p, 0, bytes, st)) != hipSuccess) {
+      (void)hipFree(p);
+      return hip_fail(e, "hipMemsetAsync(merge counters)");
+    }
+    ws.cnt = static_cast<int32_t*>(p);
+  }
+  *out = ws.cnt;
   return PDA_OK;
 }
 
@@ -546,14 +625,19 @@ int attention_call(const void* q, const void* k_cache, const void* v_cache, cons
     return fail(PDA_ERR_UNSUPPORTED, "batch %d needs more LDS than a workgroup has", batch);
   hipStream_t st = static_cast<hipStream_t>(stream);
   void* ws = nullptr;
+  int32_t* cnt = nullptr;
   if (noalloc) {
-    if (pl.bytes > PDA_NOALLOC_SCRATCH_BYTES)
+    // the partials from the start of the scratch, the merge counters at its end
+    const int64_t counter_bytes = static_cast<int64_t>(pda::kMaxFusedGrid) * 4;
+    if (pl.bytes > PDA_NOALLOC_SCRATCH_BYTES - counter_bytes)
       return fail(PDA_ERR_UNSUPPORTED,
                   "this shape needs %lld bytes of workspace; the no-allocation entry point holds %lld",
-                  static_cast<long long>(pl.bytes), static_cast<long long>(PDA_NOALLOC_SCRATCH_BYTES));
+                  static_cast<long long>(pl.bytes), static_cast<long long>(PDA_NOALLOC_SCRATCH_BYTES - counter_bytes));
     if ((e = pda::noalloc_scratch(dev, &ws)) != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
-  } else if ((rc = workspace_for(dev, st, pl.bytes, &ws))) {
-    return rc;
+    cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + PDA_NOALLOC_SCRATCH_BYTES - counter_bytes);
+  } else {
+    if ((rc = workspace_for(dev, st, pl.bytes, &ws))) return rc;
+    if (pl.fused && (rc = counters_for(dev, st, &cnt))) return rc;
   }
 
   pda::LaunchArgs a;
@@ -582,14 +666,17 @@ int attention_call(const void* q, const void* k_cache, const void* v_cache, cons
   a.nq = num_queries;
   a.window = window;
   a.valu_cols = valu_cols;
+  a.ws_cnt = cnt;
+  a.fused = pl.fused;
 
   const Rec rec = noalloc ? Rec{nullptr, nullptr, nullptr, 0} : prof_begin(0);
   const bool prof = rec.a != nullptr;
   if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if ((e = pda::launch_attn_kernel(a, st)) != hipSuccess) return hip_fail(e, "attention kernel launch");
   if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  // with one workgroup every piece is a whole sequence: nothing to merge
-  if (pl.grid > 1 && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
+  // with one workgroup every piece is a whole sequence: nothing to merge;
+  // a fused plan merged in the attention kernel
+  if (pl.grid > 1 && !pl.fused && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
     return hip_fail(e, "merge kernel launch");
   if (prof) {
     if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
@@ -615,10 +702,11 @@ int pda_plan(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t h
   if (rc) return rc;
   if (num_cus <= 0) return fail(PDA_ERR_SHAPE, "num_cus must be positive");
   Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus,
-                      pda::kMaxCols);
+                      num_q_heads / num_kv_heads);
   *grid_blocks = batch ? pl.grid : 0;
   *waves = batch ? pl.grid * pl.waves : 0;
-  *workspace_bytes = batch ? pl.bytes : 0;
+  *workspace_bytes =
+      batch ? reserve_bytes(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_cus) : 0;
   return PDA_OK;
 }
 
@@ -634,10 +722,11 @@ int pda_workspace_reserve(int32_t batch, int32_t num_q_heads, int32_t num_kv_hea
   int cus = 0;
   if ((rc = device_cus(dev, &cus))) return rc;
   // sized for the most (query token, head) columns, so any num_queries fits
-  Plan pl = make_plan(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus,
-                      pda::kMaxCols);
   void* ptr = nullptr;
-  return workspace_for(dev, static_cast<hipStream_t>(stream), pl.bytes, &ptr);
+  const int64_t need = reserve_bytes(batch, num_kv_heads, head_dim, page_size, max_pages_per_seq, cus);
+  if ((rc = workspace_for(dev, static_cast<hipStream_t>(stream), need, &ptr))) return rc;
+  int32_t* cnt = nullptr;
+  return counters_for(dev, static_cast<hipStream_t>(stream), &cnt);
 }
 
 int pda_release_workspaces(void) {
@@ -645,12 +734,13 @@ int pda_release_workspaces(void) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   int rc = PDA_OK;
   for (auto& kv : g_ws) {
-    if (!kv.second.ptr) continue;
+    if (!kv.second.ptr && !kv.second.cnt) continue;
     int cur = 0;
     hipError_t e = hipGetDevice(&cur);
     if (e == hipSuccess) e = hipSetDevice(kv.first.first);
     if (e == hipSuccess) e = hipStreamSynchronize(kv.first.second);
-    if (e == hipSuccess) e = hipFree(kv.second.ptr);
+    if (e == hipSuccess && kv.second.ptr) e = hipFree(kv.second.ptr);
+    if (e == hipSuccess && kv.second.cnt) e = hipFree(kv.second.cnt);
     const hipError_t back = hipSetDevice(cur);
     if (e == hipSuccess) e = back;
     if (e != hipSuccess) rc = hip_fail(e, "releasing a workspace");
@@ -675,6 +765,10 @@ int pda_set_option(int32_t option, int32_t value) {
       if (value < 0 || value > 1) return fail(PDA_ERR_SHAPE, "compute path must be 0 or 1");
       g_compute_path.store(value);
       return PDA_OK;
+    case PDA_OPT_FUSED_MERGE:
+      if (value < 0 || value > 2) return fail(PDA_ERR_SHAPE, "fused merge must be 0, 1 or 2");
+      g_fused_merge.store(value);
+      return PDA_OK;
     default:
       return fail(PDA_ERR_UNSUPPORTED, "unknown option %d", option);
   }
@@ -685,6 +779,7 @@ int32_t pda_get_option(int32_t option) {
     case PDA_OPT_BLOCKS_PER_CU: return blocks_per_cu();
     case PDA_OPT_MIN_STEPS: return min_steps_per_wave();
     case PDA_OPT_COMPUTE_PATH: return compute_path();
+    case PDA_OPT_FUSED_MERGE: return fused_merge();
     default: return -1;
   }
 }

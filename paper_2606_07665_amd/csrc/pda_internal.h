@@ -28,6 +28,7 @@ struct LaunchArgs {
   float* ws_acc;      // [slots, hgs, nq * group, head_dim] partial accumulators
   float* ws_ml;       // [slots, hgs, nq * group, 2] partial (max in log2 units, sum)
   int32_t* ws_pref;   // [batch + 1] steps prefix, then [grid] split list, written by the attention kernel
+  int32_t* ws_cnt;    // [grid] arrival counters of the fused merge, zero between calls
   int batch, hq, hkv, group, head_dim, page_shift, num_pages, maxp;
   int hgs;            // kv heads per workgroup (a divisor of hkv, at most max_waves(head_dim))
   int waves;          // waves per workgroup: hgs x step phases
@@ -37,7 +38,14 @@ struct LaunchArgs {
   int nq;      // query tokens per sequence (causal among them)
   int window;  // sliding window in tokens, 0 = none
   int valu_cols = 0;  // 0: products on the matrix cores; 4 or 8: vector-ALU variant for that many columns
+  bool fused = false; // split sequences merged by their last workgroup (no merge kernel)
 };
+
+// The fused merge is planned when the most partial data one sequence can
+// have (grid x kv heads per workgroup x columns x head_dim fp32) is at most
+// this, so one workgroup reads it in about one memory round trip.
+constexpr int64_t kFusedMergeBytes = 128 * 1024;
+constexpr int kMaxFusedGrid = 4096;  // arrival counters a workspace holds
 
 hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st);
 // Device address of the fixed scratch of the no-allocation entry point on

@@ -149,6 +149,38 @@ __device__ __forceinline__ u32x4 ld16_stream(__amdgpu_buffer_rsrc_t r, int byte_
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kCachePolicyNT);
 }
 
+// Split partials that the last workgroup to finish a sequence merges (the
+// fused merge) cross workgroups on different XCDs, whose L2 caches are not
+// coherent with each other.  They are stored and loaded with the
+// device-coherent cache policy (sc1: stores write through, loads do not hit
+// a stale line), the form the memory model gives agent-scope atomic
+// accesses, so no cache-wide writeback or invalidate is needed around the
+// arrival counter.
+constexpr int kCachePolicyCoherent = 16;  // sc1
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t ws_rsrc(const float* base) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
+  void* ub = reinterpret_cast<void*>((static_cast<uint64_t>(hi) << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, 0, 0x7FFFFFFF, kBufferDword3);
+}
+__device__ __forceinline__ void store_coherent(__amdgpu_buffer_rsrc_t r, int64_t idx, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, static_cast<int>(idx * 4), 0,
+                                         kCachePolicyCoherent);
+}
+__device__ __forceinline__ void store_coherent(__amdgpu_buffer_rsrc_t r, int64_t idx, f32x2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, v), r, static_cast<int>(idx * 4), 0,
+                                        kCachePolicyCoherent);
+}
+__device__ __forceinline__ f32x4 load_coherent4(__amdgpu_buffer_rsrc_t r, int64_t idx) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(idx * 4), 0,
+                                                                          kCachePolicyCoherent));
+}
+__device__ __forceinline__ f32x2 load_coherent2(__amdgpu_buffer_rsrc_t r, int64_t idx) {
+  return __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(r, static_cast<int>(idx * 4), 0,
+                                                                         kCachePolicyCoherent));
+}
+
 // Workgroup that owns flattened step x of `total`, when `parts` workgroups
 // split [0, total) into ranges [w*total/parts, (w+1)*total/parts).
 __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t parts) {
@@ -176,19 +208,96 @@ __device__ __forceinline__ constexpr int valu_slot(int is) {
   return NC == 8 ? (((is & 1) << 2) | (is >> 1)) : (((is & 1) << 2) | (is & 2) | (is >> 2));
 }
 
+// The fused merge of one split sequence (kv-head group hg of sequence b,
+// pieces in workgroups w0 .. w1) by the workgroup that counted its last
+// piece: per (query row, float4 column) of the group,
+//   out = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j,  M = max_j m_j,
+// in slot order.  When the rows x columns leave threads over, each item's
+// pieces are dealt to PG groups (piece w to group (w - w0) mod PG) whose
+// results are folded in group order through LDS (the tiles, free by now).
+template <int D>
+__device__ void merge_in_workgroup(uint16_t* __restrict__ out, const float* __restrict__ ws_acc,
+                                   const float* __restrict__ ws_ml, unsigned char* smem, int b, int hg, int w0,
+                                   int w1, int ngroups, int hgs, int ncols, int group, int nq, int hq) {
+  constexpr int kC4 = D / 4;
+  const int nthreads = blockDim.x;
+  const int tid = threadIdx.x;
+  const int items = hgs * ncols * kC4;
+  int pgs = 1;
+  while (pgs < 8 && items * pgs * 2 <= nthreads) pgs *= 2;
+  const __amdgpu_buffer_rsrc_t ra = ws_rsrc(ws_acc), rm = ws_rsrc(ws_ml);
+  const int64_t base = static_cast<int64_t>(b) * ngroups + hg;
+  f32x4* s_num = reinterpret_cast<f32x4*>(smem);        // [pg][item]
+  f32x2* s_ml = reinterpret_cast<f32x2*>(s_num + items * pgs);
+  for (int it0 = 0; it0 < items * pgs; it0 += nthreads) {
+    const int it = it0 + tid;
+    const bool active = it < items * pgs;
+    const int item = it % items, pg = it / items;
+    const int r = item / kC4, col = item - r * kC4;
+    const int hi_w = r / ncols, cc = r - hi_w * ncols;
+    float mm = -__builtin_inff(), ll = 0.f;
+    f32x4 nn = {0.f, 0.f, 0.f, 0.f};
+    if (active) {
+#pragma unroll 4
+      for (int w = w0 + pg; w <= w1; w += pgs) {
+        const int64_t row = ((w + base) * hgs + hi_w) * ncols + cc;
+        const f32x2 mlv = load_coherent2(rm, row * 2);
+        const f32x4 av = load_coherent4(ra, row * D + 4 * col);
+        const float m2 = fmaxf(mm, mlv[0]);
+        const float mref = m2 == -__builtin_inff() ? 0.f : m2;  // pieces that saw no key
+        const float fo = __builtin_amdgcn_exp2f(mm - mref);
+        const float fn = __builtin_amdgcn_exp2f(mlv[0] - mref);
+        nn = nn * fo + av * fn;
+        ll = ll * fo + mlv[1] * fn;
+        mm = m2;
+      }
+    }
+    if (pgs > 1) {  // then items * pgs <= nthreads: one pass
+      if (active) {
+        s_num[it] = nn;
+        s_ml[it] = f32x2{mm, ll};
+      }
+      __syncthreads();
+      if (!active || pg != 0) continue;
+      float big_m = -__builtin_inff();
+      for (int p = 0; p < pgs; ++p) big_m = fmaxf(big_m, s_ml[p * items + item][0]);
+      nn = f32x4{0.f, 0.f, 0.f, 0.f};
+      ll = 0.f;
+      for (int p = 0; p < pgs; ++p) {
+        const f32x2 mlp = s_ml[p * items + item];
+        const float f = mlp[0] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(mlp[0] - big_m);
+        nn += f * s_num[p * items + item];
+        ll += f * mlp[1];
+      }
+    }
+    if (!active) continue;
+    const float inv = ll > 0.f ? 1.0f / ll : 0.f;  // a query that sees no key: zero row
+    bf16x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(nn[i] * inv);
+    const int j = cc / group;
+    const int h = (hg * hgs + hi_w) * group + (cc - j * group);
+    *reinterpret_cast<u32x2*>(out + ((static_cast<int64_t>(b) * nq + j) * hq + h) * D + 4 * col) =
+        __builtin_bit_cast(u32x2, o);
+  }
+}
+
+// kFused: split sequences are merged by the last workgroup to finish each
+// (plans with little partial data per sequence); otherwise merge_kernel
+// runs after this kernel.
 // kNC = 0: QK^T and P.V on the matrix cores (the path every entry point
 // uses).  kNC = 4 or 8: the same pass with both products on the vector ALU
 // (bf16 dot2 for QK^T, fp32 FMA for P.V) for up to kNC (query token, head)
 // columns at D = 128 -- the measured alternative to the matrix cores,
 // selected with PDA_OPT_COMPUTE_PATH.
-template <int D, bool kLanePages, int kNC = 0>
+template <int D, bool kLanePages, int kNC = 0, bool kFused = false>
 __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
     const int32_t* __restrict__ lens, uint16_t* __restrict__ out,
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_pref,
-    int batch, int hq, int hkv, int group, int hgs, int page_shift, int num_pages, int maxp,
-    int min_steps, float scale_log2, int nq, int window) {
+    int32_t* __restrict__ ws_cnt, int batch, int hq, int hkv, int group, int hgs, int page_shift,
+    int num_pages, int maxp, int min_steps, float scale_log2, int nq, int window) {
   constexpr bool kValu = kNC > 0;
   static_assert(!kValu || (D == 128 && !kLanePages && (kNC == 4 || kNC == 8)), "vector-ALU variant shapes");
   using S = Shape<D, kValu>;
@@ -860,8 +969,8 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
         }
       }
     }
+    const bool whole = (s0 == 0) && (s1 == nb);  // workgroup-uniform
     if (ph == 0 && c < ncols) {
-      const bool whole = (s0 == 0) && (s1 == nb);
       if (whole) {
         const float inv = den > 0.f ? 1.0f / den : 0.f;  // a query that sees no key: zero row
         uint16_t* orow = out + ((static_cast<int64_t>(b) * nq + qj) * hq + g * group + qh) * D + 4 * g4;
@@ -876,13 +985,44 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
         // slot (workgroup + sequence group) is unique: workgroup ranges are contiguous
         const int64_t slot = static_cast<int64_t>(blk) + static_cast<int64_t>(b) * ngroups + hg;
         const int64_t row = (slot * hgs + hi_w) * ncols + c;
-        float* arow = ws_acc + row * D + 4 * g4;
+        if constexpr (kFused) {
+          const __amdgpu_buffer_rsrc_t ra = ws_rsrc(ws_acc), rm = ws_rsrc(ws_ml);
 #pragma unroll
-        for (int dt = 0; dt < S::kDT; ++dt) *reinterpret_cast<f32x4*>(arow + 16 * dt) = acc[dt];
-        if (g4 == 0) *reinterpret_cast<f32x2*>(ws_ml + row * 2) = f32x2{big_m, den};
+          for (int dt = 0; dt < S::kDT; ++dt) store_coherent(ra, row * D + 4 * g4 + 16 * dt, acc[dt]);
+          if (g4 == 0) store_coherent(rm, row * 2, f32x2{big_m, den});
+        } else {
+          float* arow = ws_acc + row * D + 4 * g4;
+#pragma unroll
+          for (int dt = 0; dt < S::kDT; ++dt) *reinterpret_cast<f32x4*>(arow + 16 * dt) = acc[dt];
+          if (g4 == 0) *reinterpret_cast<f32x2*>(ws_ml + row * 2) = f32x2{big_m, den};
+        }
       }
     }
-    if (phases > 1) __syncthreads();  // the exchange area is a tile again
+    if (kFused && !whole) {
+      // Fused merge: every store of this piece is acknowledged (so visible
+      // device-wide) before the piece is counted; the workgroup that counts
+      // the sequence's last piece merges all of them in slot order, so the
+      // result does not depend on the order of arrival, and resets the
+      // counter for the next call (or graph replay).  The counter of a split
+      // sequence is indexed by the workgroup holding its first step, which
+      // no other split sequence starts in.
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      int32_t* flag = reinterpret_cast<int32_t*>(ml_x);
+      const int64_t x0 = static_cast<int64_t>(pref[b]) * ngroups + static_cast<int64_t>(hg) * nb;
+      const int w0 = static_cast<int>(owner_of(x0, total, beff));
+      const int w1 = static_cast<int>(owner_of(x0 + nb - 1, total, beff));
+      if (tid == 0)
+        *flag = __hip_atomic_fetch_add(ws_cnt + w0, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == w1 - w0;
+      __syncthreads();
+      if (uniform(*flag)) {
+        merge_in_workgroup<D>(out, ws_acc, ws_ml, smem, b, hg, w0, w1, ngroups, hgs, ncols, group, nq, hq);
+        if (tid == 0) __hip_atomic_store(ws_cnt + w0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      __syncthreads();  // the flag and the tiles are reused by the next piece
+    } else if (phases > 1) {
+      __syncthreads();  // the exchange area is a tile again
+    }
 
     x += s1 - s0;
     if (x >= xend) break;
@@ -1008,7 +1148,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
       __builtin_bit_cast(u32x2, o);
 }
 
-template <int D, bool kLanePages, int kNC = 0>
+template <int D, bool kLanePages, int kNC = 0, bool kFused = false>
 static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   const size_t lds = attn_lds_bytes(D, a.batch, a.waves, kNC > 0);
   // the dynamic-LDS limit is raised once per device (bit = device ordinal)
@@ -1018,14 +1158,15 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
   if (!bit || !(attr_set.load() & bit)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages, kNC>),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages, kNC, kFused>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
     if (e != hipSuccess) return e;
     attr_set.fetch_or(bit);
   }
-  hipLaunchKernelGGL((attn_kernel<D, kLanePages, kNC>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
-                     a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.batch, a.hq, a.hkv, a.group,
-                     a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e, a.nq, a.window);
+  hipLaunchKernelGGL((attn_kernel<D, kLanePages, kNC, kFused>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
+                     a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.ws_cnt, a.batch, a.hq, a.hkv,
+                     a.group, a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e, a.nq,
+                     a.window);
   return hipGetLastError();
 }
 
@@ -1033,9 +1174,16 @@ hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
   const bool lane_pages = a.page_shift < 4;
   if (a.waves > max_waves(a.head_dim)) return hipErrorInvalidValue;
   if (a.valu_cols) {
-    // vector-ALU variant: D = 128, pages of 16 tokens or more, at most 8 columns
-    if (a.head_dim != 128 || lane_pages || a.group * a.nq > a.valu_cols) return hipErrorInvalidValue;
+    // vector-ALU variant: D = 128, pages of 16 tokens or more, at most 8 columns, merge kernel
+    if (a.head_dim != 128 || lane_pages || a.group * a.nq > a.valu_cols || a.fused) return hipErrorInvalidValue;
     return a.valu_cols == 4 ? launch_attn<128, false, 4>(a, st) : launch_attn<128, false, 8>(a, st);
+  }
+  if (a.fused) {
+    if (a.head_dim == 128)
+      return lane_pages ? launch_attn<128, true, 0, true>(a, st) : launch_attn<128, false, 0, true>(a, st);
+    if (a.head_dim == 256)
+      return lane_pages ? launch_attn<256, true, 0, true>(a, st) : launch_attn<256, false, 0, true>(a, st);
+    return lane_pages ? launch_attn<64, true, 0, true>(a, st) : launch_attn<64, false, 0, true>(a, st);
   }
   if (a.head_dim == 128) return lane_pages ? launch_attn<128, true>(a, st) : launch_attn<128, false>(a, st);
   if (a.head_dim == 256) return lane_pages ? launch_attn<256, true>(a, st) : launch_attn<256, false>(a, st);

@@ -514,3 +514,19 @@ def test_o_proj_and_kv_append_binding_checks():
         oproj()
     with pytest.raises(ValueError, match=re.escape("v_new must be [B, Hkv, D] with Hkv = 2")):
         B.kv_append(_t(2, 2, 64), _t(2, 1, 64), _t(10, 16, 2, 64), _t(10, 16, 2, 64), _i32(2, 5), _i32(2))
+
+
+def test_fused_merge_option(lib):
+    assert B.get_option(B.OPT_FUSED_MERGE) == 0
+    with pytest.raises(B.PdaError):
+        B.set_option(B.OPT_FUSED_MERGE, 3)
+    try:
+        for v in (1, 2, 0):
+            B.set_option(B.OPT_FUSED_MERGE, v)
+            assert B.get_option(B.OPT_FUSED_MERGE) == v
+        # the reserve bound covers every kv-head grouping the planner may pick
+        # (a single request takes one kv head per workgroup with the fused merge)
+        _, _, ws = B.plan(1, 32, 8, 128, 16, 256, num_cus=256)
+        assert ws >= (64 + 8) * 1 * 16 * (128 + 2) * 4
+    finally:
+        B.set_option(B.OPT_FUSED_MERGE, 0)
