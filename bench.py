@@ -38,12 +38,16 @@ def parse():
                     choices=["tiny", "llama8b", "batched", "long70b", "ragged", "window", "multiq", "gqa16",
                              "falcon3", "tokenpage", "prelude_qwen3_4b", "prelude_llama8b", "prelude_70b", "prelude_glm4",
                              "prelude_falcon3", "oproj_qwen3_4b", "oproj_llama8b", "oproj_70b",
-                             "oproj_falcon3", "layer70b", "layer8b", "layer_falcon3"])
+                             "oproj_falcon3", "prelude_ragged", "oproj_ragged", "layer70b", "layer8b",
+                             "layer_falcon3", "layer_ragged"])
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="budget of each oracle cpu_baseline sample (all cores, then one thread)")
     ap.add_argument("--compute-path", default="mfma", choices=["mfma", "valu"],
                     help="attention products on the matrix cores (default) or the vector-ALU variant "
                          "(the measured alternative; head_dim 128 and <= 8 columns per kv head)")
+    ap.add_argument("--seed", type=int, default=None,
+                    help="draw the attention workload with this seed instead of its own (same shapes; the "
+                         "lengths come first, so two workloads of one length recipe then share lengths)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extra", default="batched,ragged",
                     help="comma-separated workloads timed in the same run after the headline one and reported "
@@ -228,7 +232,7 @@ def main():
     from paper_2606_07665_amd import binding as pda
 
     t_gen = time.perf_counter()
-    w = W.make(args.workload, poison=False)
+    w = W.make(args.workload, poison=False, seed=args.seed)
     print(f"[bench] generated {args.workload} in {time.perf_counter() - t_gen:.1f}s", file=sys.stderr, flush=True)
     cpu = None
     if not args.no_cpu_baseline:
@@ -420,6 +424,7 @@ def main():
             "total_context_tokens": int(w.context_lens.astype(np.int64).sum()),
             "algorithmic_bytes": nbytes, "parallelism": "single GPU", "device": gpu_name,
             "compute_path": args.compute_path,
+            "seed": args.seed if args.seed is not None else W.CONFIGS[args.workload].seed,
         },
         "kernels_ms": {"split": round(split_ms, 5), "merge": round(merge_ms, 5)},
         "graph_us_per_call": None if graph_us is None else round(graph_us, 2),
@@ -756,6 +761,7 @@ LAYERS = {
     "layer70b": ("long70b", "prelude_70b", "oproj_70b"),
     "layer8b": ("batched", "prelude_llama8b", "oproj_llama8b"),
     "layer_falcon3": ("falcon3", "prelude_falcon3", "oproj_falcon3"),
+    "layer_ragged": ("ragged", "prelude_ragged", "oproj_ragged"),
 }
 
 

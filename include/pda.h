@@ -380,6 +380,12 @@ int32_t pda_version(void);
  *                          grouping (for tests: slow for long contexts).
  *                          All are deterministic for a fixed plan; they
  *                          round differently.
+ *   PDA_OPT_KV_GROUP       most kv heads a workgroup reads together, 0..8
+ *                          (default 0 = the planner's choice, env
+ *                          PDA_KV_GROUP): the largest divisor of
+ *                          num_kv_heads not above it.  Fewer heads per
+ *                          workgroup mean smaller partials per split piece
+ *                          and shorter token rows read at a time.
  * Options are process-wide and apply to later calls.  pda_set_option
  * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
  * returns the current value or -1 for an unknown option.
@@ -388,6 +394,7 @@ int32_t pda_version(void);
 #define PDA_OPT_MIN_STEPS 2
 #define PDA_OPT_COMPUTE_PATH 3
 #define PDA_OPT_FUSED_MERGE 4
+#define PDA_OPT_KV_GROUP 5
 int pda_set_option(int32_t option, int32_t value);
 int32_t pda_get_option(int32_t option);
 
@@ -442,7 +449,8 @@ int pda_stream_read(const void* buf, int64_t bytes, uint32_t* sink, int32_t unro
  * ---------------------------------------------------------------------------
  */
 typedef struct {
-  int32_t batch;         /* sequences, 0 .. 64                                  */
+  int32_t batch;         /* sequences, 0 .. 256; above 64, (num_q_heads +
+                            2 num_kv_heads) * head_dim a multiple of 128       */
   int32_t hidden;        /* H: a positive multiple of 32, at most 65536         */
   int32_t num_q_heads;   /* Hq, a multiple of num_kv_heads                      */
   int32_t num_kv_heads;  /* Hkv                                                 */
@@ -516,8 +524,9 @@ int pda_prelude_workspace_reserve(const pda_prelude_dims* dims, void* stream);
  *   residual_out  bf16 [batch, hidden]: z rounded once (may be residual itself,
  *                 updated in place); normed_out bf16 [batch, hidden]: h, from
  *                 the unrounded z; must not be residual_out.
- *   batch 0..64; in_features a multiple of 32 up to 65536; hidden a multiple
- *   of 16 up to 32768; eps finite and >= 0.
+ *   batch 0..256 (above 64, hidden a multiple of 128); in_features a
+ *   multiple of 32 up to 65536; hidden a multiple of 16 up to 32768; eps
+ *   finite and >= 0.
  * Uses the (device, stream) workspace (pda_o_proj_workspace_reserve before
  * graph capture).  Asynchronous.  Errors as for pda_attention_prelude.
  * ---------------------------------------------------------------------------

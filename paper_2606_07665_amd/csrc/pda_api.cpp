@@ -57,6 +57,7 @@ std::atomic<int> g_blocks_per_cu{-1};
 std::atomic<int> g_min_steps{-1};
 std::atomic<int> g_compute_path{-1};
 std::atomic<int> g_fused_merge{-1};
+std::atomic<int> g_kv_group{-1};
 
 int blocks_per_cu() {
   int v = g_blocks_per_cu.load();
@@ -89,6 +90,16 @@ int fused_merge() {
   if (v < 0) {
     v = env_int("PDA_FUSED_MERGE", 0, 0, 2);
     g_fused_merge.store(v);
+  }
+  return v;
+}
+
+// Most kv heads one attention workgroup reads together (0 = the plan's own choice).
+int kv_group_cap() {
+  int v = g_kv_group.load();
+  if (v < 0) {
+    v = env_int("PDA_KV_GROUP", 0, 0, pda::kMaxWaves);
+    g_kv_group.store(v);
   }
   return v;
 }
@@ -207,7 +218,15 @@ Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t
 // acknowledgement, the arrival atomic, coherent reloads) costs more than
 // the merge kernel's launch, so the option is off by default.
 Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
-  const Plan dflt = plan_for(heads_per_group(hkv, pda::max_waves(d)), batch, hkv, d, p, maxp, num_cus, cols);
+  const int cap = kv_group_cap();
+  // A split piece leaves a partial of cols x head_dim fp32 per kv head it
+  // covers; with more than 8 columns (several query tokens) those writes
+  // cost more than the longer token rows save, so at most 4 kv heads go
+  // together (multiq: 191.4 -> 188.3 us per call; long70b and ragged, at 8
+  // columns or fewer, run slower with 4).
+  const int dflt_most = cols > 8 ? std::min(4, pda::max_waves(d)) : pda::max_waves(d);
+  const int most = cap > 0 && cap < pda::max_waves(d) ? cap : dflt_most;
+  const Plan dflt = plan_for(heads_per_group(hkv, most), batch, hkv, d, p, maxp, num_cus, cols);
   // (the vector-ALU variant, a measurement aid, keeps the merge kernel)
   if (dflt.grid == 1 || !fused_merge() || compute_path() != 0) return dflt;
   if (fused_merge() == 2) {  // every plan that has something to merge (tests)
@@ -490,6 +509,10 @@ int check_prelude(const pda_prelude_dims* dm) {
                 d.num_kv_heads);
   if (d.head_dim != 64 && d.head_dim != 128 && d.head_dim != 256)
     return fail(PDA_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128, 256)", d.head_dim);
+  if (d.batch > pda::kMaxGemvBatchAnyRows &&
+      (static_cast<int64_t>(d.num_q_heads + 2 * d.num_kv_heads) * d.head_dim) % 128)
+    return fail(PDA_ERR_UNSUPPORTED, "prelude batch %d above %d needs (num_q_heads + 2 num_kv_heads) * head_dim "
+                "a multiple of 128", d.batch, pda::kMaxGemvBatchAnyRows);
   if (d.num_kv_heads > PDA_MAX_KV_HEADS || d.num_q_heads > 8 * PDA_MAX_KV_HEADS)
     return fail(PDA_ERR_UNSUPPORTED, "too many heads (q %d, kv %d)", d.num_q_heads, d.num_kv_heads);
   if (d.rotary_dim < 0 || d.rotary_dim > d.head_dim || (d.rotary_dim & 1))
@@ -769,6 +792,10 @@ int pda_set_option(int32_t option, int32_t value) {
       if (value < 0 || value > 2) return fail(PDA_ERR_SHAPE, "fused merge must be 0, 1 or 2");
       g_fused_merge.store(value);
       return PDA_OK;
+    case PDA_OPT_KV_GROUP:
+      if (value < 0 || value > pda::kMaxWaves) return fail(PDA_ERR_SHAPE, "kv group must be in [0, %d]", pda::kMaxWaves);
+      g_kv_group.store(value);
+      return PDA_OK;
     default:
       return fail(PDA_ERR_UNSUPPORTED, "unknown option %d", option);
   }
@@ -780,6 +807,7 @@ int32_t pda_get_option(int32_t option) {
     case PDA_OPT_MIN_STEPS: return min_steps_per_wave();
     case PDA_OPT_COMPUTE_PATH: return compute_path();
     case PDA_OPT_FUSED_MERGE: return fused_merge();
+    case PDA_OPT_KV_GROUP: return kv_group_cap();
     default: return -1;
   }
 }
@@ -1041,6 +1069,9 @@ int pda_o_proj_residual_norm(const void* attn, const void* w_packed, const void*
   if (hidden % pda::kTileRows || hidden > pda::kMaxOProjHidden)
     return fail(PDA_ERR_UNSUPPORTED, "hidden %d (supported: multiples of 16 up to %d)", hidden,
                 pda::kMaxOProjHidden);
+  if (batch > pda::kMaxGemvBatchAnyRows && hidden % 128)
+    return fail(PDA_ERR_UNSUPPORTED, "o_proj batch %d above %d needs hidden a multiple of 128", batch,
+                pda::kMaxGemvBatchAnyRows);
   if (!std::isfinite(eps) || eps < 0.f) return fail(PDA_ERR_SCALE, "eps must be finite and >= 0");
   if (batch == 0) return PDA_OK;
   if (!attn || !w_packed || !residual || !norm_w || !residual_out || !normed_out)
@@ -1096,7 +1127,8 @@ int pda_o_proj_residual_norm(const void* attn, const void* w_packed, const void*
 int pda_o_proj_workspace_reserve(int32_t batch, int32_t in_features, int32_t hidden, void* stream) {
   g_err.clear();
   if (batch < 0 || batch > pda::kMaxGemvBatch || in_features <= 0 || in_features % pda::kTileK ||
-      hidden <= 0 || hidden % pda::kTileRows || hidden > pda::kMaxOProjHidden)
+      hidden <= 0 || hidden % pda::kTileRows || hidden > pda::kMaxOProjHidden ||
+      (batch > pda::kMaxGemvBatchAnyRows && hidden % 128))
     return fail(PDA_ERR_SHAPE, "o_proj shape out of range");
   if (batch == 0) return PDA_OK;
   int dev = 0;

@@ -41,7 +41,10 @@ __host__ __device__ constexpr int gemv_xlds_lds_bytes(int nbt) { return kXRing *
 constexpr int kGemvMaxSlots = 16;               // most workgroups sharing one row group
 constexpr int kTileRows = 16;                   // rows of W per MFMA tile
 constexpr int kTileK = 32;                      // k per MFMA tile
-constexpr int kMaxGemvBatch = 64;               // sequences: four 16-column tiles
+constexpr int kMaxGemvBatch = 256;              // sequences: sixteen 16-column tiles
+// Batches above this run only in the thin-GEMM form (gemv_xlds_kernel with
+// 8 or 16 column tiles), which needs the rows in groups of kXWaves tiles.
+constexpr int kMaxGemvBatchAnyRows = 64;
 constexpr int kPackThreads = 256;
 
 // y[b, n] = sum_k x[b, k] W[n, k] over a packed W (see launch_pack), as
@@ -108,6 +111,18 @@ struct OProjArgs {
 };
 
 __host__ __device__ inline int oproj_chunks(int hidden) { return (hidden + kOProjChunk - 1) / kOProjChunk; }
+
+// The o_proj epilogue runs as one kernel when the hidden size allows: one
+// workgroup of kOProjOneThreads per sequence holds all of its z in
+// registers (at most kOProjOneFeatures per thread), so the norm needs no
+// second pass.  Measured faster than or as fast as the two passes at
+// batches 1, 4, 16, 64 and 256; larger hidden sizes keep the two passes.
+constexpr int kOProjOneThreads = 1024;
+constexpr int kOProjOneFeatures = 8;
+constexpr int kOProjOneMaxBatch = 256;
+__host__ __device__ inline bool oproj_one_kernel(int batch, int hidden) {
+  return batch <= kOProjOneMaxBatch && hidden <= kOProjOneThreads * kOProjOneFeatures;
+}
 
 hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_t st);
 hipError_t launch_oproj_epilogue(const OProjArgs& a, hipStream_t st);

@@ -14,9 +14,10 @@
 //    8 (l / 16) .. +7 of it.  Every weight load of the GEMV is then one
 //    contiguous 1 KB wave access that feeds v_mfma_f32_16x16x32_bf16
 //    directly, with no LDS staging and no lane shuffles.
-//  * The batch (up to 64 sequences) forms the MFMA's B columns, in up to four
-//    16-column tiles; x rows past the batch read as zeros through the buffer
-//    descriptor's size.
+//  * The batch forms the MFMA's B columns in 16-column tiles (up to four in
+//    gemv_kernel, up to sixteen -- 256 sequences -- in the thin-GEMM form);
+//    x rows past the batch read as zeros through the buffer descriptor's
+//    size.
 //  * Stream-K over (row group, 32-k tile) units: every workgroup of a grid
 //    sized to the device streams the same number of packed weight tiles,
 //    whatever the shape, so no half-empty last round of workgroups.  The
@@ -372,6 +373,42 @@ __device__ __forceinline__ void gemv_rows(const float* __restrict__ part, const 
   }
 }
 
+// y[b][n .. n+3] for four consecutive rows n (n a multiple of 4, so one
+// 16-byte piece of one tile's partial row in every slot): the sum in
+// workgroup order of their group's partials, loaded as 16-byte pieces,
+// every slot's load issued before any is added.
+template <int kSlots>
+__device__ __forceinline__ float4 gemv_rows4(const float* __restrict__ part, const GemvPlan& p, int batch, int b,
+                                             int n) {
+  const int g = (n >> 4) / p.group;
+  int cnt;
+  if (((p.units * p.blocks) >> 32) == 0) {
+    const uint32_t nb = static_cast<uint32_t>(p.blocks), nu = static_cast<uint32_t>(p.units);
+    const uint32_t x0 = static_cast<uint32_t>(g) * p.kt_count;
+    cnt = static_cast<int>(((x0 + p.kt_count) * nb - 1) / nu - ((x0 + 1) * nb - 1) / nu + 1);
+  } else {
+    const int64_t x0 = static_cast<int64_t>(g) * p.kt_count;
+    cnt = static_cast<int>(((x0 + p.kt_count) * p.blocks - 1) / p.units - ((x0 + 1) * p.blocks - 1) / p.units + 1);
+  }
+  const int64_t slot_floats = static_cast<int64_t>(p.group) * batch * kTileRows;
+  const int i = (n >> 4) - g * p.group;
+  const float* q = part + static_cast<int64_t>(g) * p.slots * slot_floats +
+                   (static_cast<int64_t>(i) * batch + b) * kTileRows + (n & 15);
+  float4 v[kSlots];
+#pragma unroll
+  for (int j = 0; j < kSlots; ++j) v[j] = *reinterpret_cast<const float4*>(q + (j < cnt ? j : cnt - 1) * slot_floats);
+  float4 y = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < kSlots; ++j)
+    if (j < cnt) {
+      y.x += v[j].x;
+      y.y += v[j].y;
+      y.z += v[j].z;
+      y.w += v[j].w;
+    }
+  return y;
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __builtin_bit_cast(float, static_cast<uint32_t>(h) << 16);
 }
@@ -547,6 +584,59 @@ __global__ __launch_bounds__(kOProjChunk) void oproj_norm_kernel(OProjArgs a) {
   a.normed_out[at] = f32_to_bf16(z * inv * w);
 }
 
+// The o_proj epilogue in one kernel for small batches, one workgroup per
+// sequence b; thread t takes the four consecutive features 4 (t + 1024 j):
+// z = y + residual kept in registers (fp32; bf16 to residual_out), the
+// sequence's sum of z^2 reduced across the workgroup in a fixed order,
+// then h = z / sqrt(mean + eps) * w.  Partials are read as 16-byte pieces.
+template <int kSlots>
+__global__ __launch_bounds__(kOProjOneThreads) void oproj_one_kernel(OProjArgs a) {
+  constexpr int kGroups = kOProjOneFeatures / 4;  // groups of four features per thread, at most
+  __shared__ float wsum[kOProjOneThreads / 64];
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int64_t base = static_cast<int64_t>(b) * a.hidden;
+  float4 z[kGroups];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kGroups; ++j) {
+    const int n = 4 * (tid + kOProjOneThreads * j);
+    z[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (n < a.hidden) {
+      const uint2 r = *reinterpret_cast<const uint2*>(a.residual + base + n);
+      const float4 y = gemv_rows4<kSlots>(a.part, a.plan, a.batch, b, n);
+      z[j] = make_float4(y.x + bf16_to_f32(static_cast<uint16_t>(r.x)), y.y + bf16_to_f32(static_cast<uint16_t>(r.x >> 16)),
+                         y.z + bf16_to_f32(static_cast<uint16_t>(r.y)), y.w + bf16_to_f32(static_cast<uint16_t>(r.y >> 16)));
+      ss += z[j].x * z[j].x + z[j].y * z[j].y + z[j].z * z[j].z + z[j].w * z[j].w;
+      uint2 o;
+      o.x = f32_to_bf16(z[j].x) | (static_cast<uint32_t>(f32_to_bf16(z[j].y)) << 16);
+      o.y = f32_to_bf16(z[j].z) | (static_cast<uint32_t>(f32_to_bf16(z[j].w)) << 16);
+      *reinterpret_cast<uint2*>(a.residual_out + base + n) = o;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) ss += __shfl_xor(ss, off);
+  if ((tid & 63) == 0) wsum[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < kOProjOneThreads / 64; ++i) tot += wsum[i];
+  const float inv = rsqrtf(tot / a.hidden + a.eps);
+#pragma unroll
+  for (int j = 0; j < kGroups; ++j) {
+    const int n = 4 * (tid + kOProjOneThreads * j);
+    if (n < a.hidden) {
+      const uint2 w = *reinterpret_cast<const uint2*>(a.norm_w + n);
+      uint2 o;
+      o.x = f32_to_bf16(z[j].x * inv * bf16_to_f32(static_cast<uint16_t>(w.x))) |
+            (static_cast<uint32_t>(f32_to_bf16(z[j].y * inv * bf16_to_f32(static_cast<uint16_t>(w.x >> 16)))) << 16);
+      o.y = f32_to_bf16(z[j].z * inv * bf16_to_f32(static_cast<uint16_t>(w.y))) |
+            (static_cast<uint32_t>(f32_to_bf16(z[j].w * inv * bf16_to_f32(static_cast<uint16_t>(w.y >> 16)))) << 16);
+      *reinterpret_cast<uint2*>(a.normed_out + base + n) = o;
+    }
+  }
+}
+
 }  // namespace
 
 // Instantiations of the epilogues by the plan's partial slots per group.
@@ -571,7 +661,28 @@ hipError_t launch_prelude(const PreludeArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int kSlots>
+hipError_t launch_oproj_one(const OProjArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((oproj_one_kernel<kSlots>), dim3(a.batch), dim3(kOProjOneThreads), 0, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_oproj_epilogue(const OProjArgs& a, hipStream_t st) {
+  // PDA_OPROJ_ONE=0 in the environment keeps the two passes at every batch (for measurement)
+  static const bool one_ok = [] {
+    const char* e = std::getenv("PDA_OPROJ_ONE");
+    return !(e && e[0] == '0');
+  }();
+  // (the one-kernel form moves four bf16 features at a time: 8-byte aligned rows)
+  const bool aligned8 = ((reinterpret_cast<uintptr_t>(a.residual) | reinterpret_cast<uintptr_t>(a.norm_w) |
+                          reinterpret_cast<uintptr_t>(a.residual_out) | reinterpret_cast<uintptr_t>(a.normed_out)) &
+                         7) == 0;
+  if (one_ok && aligned8 && oproj_one_kernel(a.batch, a.hidden)) {
+    return a.plan.slots <= 4   ? launch_oproj_one<4>(a, st)
+           : a.plan.slots <= 8  ? launch_oproj_one<8>(a, st)
+           : a.plan.slots <= 12 ? launch_oproj_one<12>(a, st)
+                                : launch_oproj_one<kGemvMaxSlots>(a, st);
+  }
   const dim3 grid(a.batch * oproj_chunks(a.hidden));
   const hipError_t e = a.plan.slots <= 4   ? launch_oproj_residual<4>(a, st)
                        : a.plan.slots <= 8  ? launch_oproj_residual<8>(a, st)
@@ -606,12 +717,13 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
   p.group = 1;
   // batches of more than 16: the thin-GEMM form when the row tiles split
   // into groups of kXWaves (PDA_GEMV_THIN=0 in the environment selects
-  // gemv_kernel instead, for measurement)
+  // gemv_kernel instead, for measurement, up to 64 sequences; above that
+  // only the thin-GEMM form exists, and the callers check the rows)
   static const bool thin_ok = [] {
     const char* e = std::getenv("PDA_GEMV_THIN");
     return !(e && e[0] == '0');
   }();
-  if (thin_ok && nbt > 1 && tiles % kXWaves == 0) {
+  if ((thin_ok || nbt > 4) && nbt > 1 && tiles % kXWaves == 0) {
     p.xlds = true;
     p.group = kXWaves;
     p.units = static_cast<int64_t>(tiles / kXWaves) * p.kt_count;
@@ -688,8 +800,11 @@ hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
   if (a.plan.xlds) {
     if (nbt == 2) return launch_xlds<2>(a, st);
     if (nbt == 3) return launch_xlds<3>(a, st);
-    return launch_xlds<4>(a, st);
+    if (nbt == 4) return launch_xlds<4>(a, st);
+    if (nbt <= 8) return launch_xlds<8>(a, st);  // column tiles past the batch read zeros
+    return launch_xlds<16>(a, st);
   }
+  if (nbt > 4) return hipErrorInvalidValue;  // above 64 sequences only the thin-GEMM form
   const bool grouped = a.plan.group > 1;
 #define PDA_GEMV(NBT, R) \
   hipLaunchKernelGGL((gemv_kernel<NBT, R>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl)

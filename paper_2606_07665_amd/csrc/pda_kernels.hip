@@ -64,10 +64,11 @@ struct Shape {
   static constexpr int kChunks = D / 8;         // 16-byte chunks per key/value row
   static constexpr int kRowsPerLoad = 64 / kChunks;      // rows per wave load
   static constexpr int kLoads = kStep / kRowsPerLoad;    // loads per step (K and V each)
-  // One LDS tile per wave for the K and V rows of a step.  K rows have
-  // stride 2D+16 bytes (the A-operand read, lane = row, starts rows 4 banks
-  // apart); V rows stride 2D+32 (the transposed reads start rows 8 banks apart).
-  static constexpr int kKRowBytes = 2 * D + 16;
+  // One LDS tile per wave for the K and V rows of a step, rows padded by 32
+  // bytes.  Measured with SQ_LDS_BANK_CONFLICT on long70b: K rows padded by
+  // 16 bytes cost 32 conflict cycles per wave step (4.2 M per call), by 32
+  // none; V rows padded by 16 double them, unpadded K rows give 29 M.
+  static constexpr int kKRowBytes = 2 * D + 32;
   static constexpr int kVRowBytes = 2 * D + 32;
   // D = 256 keeps one register buffer of K/V per wave (a step is 32 KB): a
   // step's K and V rows go to separate regions of the tile as soon as they

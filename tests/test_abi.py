@@ -245,7 +245,8 @@ def prelude_call(ptrs=None, **kw):
 
 @pytest.mark.parametrize("kwargs,code,text", [
     (dict(batch=-1), SHAPE, "batch"),
-    (dict(batch=65), UNSUPPORTED, "batch"),
+    (dict(batch=257), UNSUPPORTED, "batch"),
+    (dict(batch=65, hq=5, hkv=1, d=64, rotary_dim=64), UNSUPPORTED, "multiple of 128"),   # 7 x 64 rows
     (dict(hidden=300), UNSUPPORTED, "hidden"),
     (dict(hidden=0), SHAPE, "positive"),
     (dict(hkv=3), SHAPE, "multiple"),
@@ -299,7 +300,8 @@ def oproj_call(ptrs=None, batch=2, k=256, h=512, eps=1e-5):
 
 @pytest.mark.parametrize("kwargs,code,text", [
     (dict(batch=-1), SHAPE, "batch"),
-    (dict(batch=65), UNSUPPORTED, "batch"),
+    (dict(batch=257), UNSUPPORTED, "batch"),
+    (dict(batch=65, h=1040), UNSUPPORTED, "multiple of 128"),
     (dict(k=0), SHAPE, "positive"),
     (dict(k=100), UNSUPPORTED, "in_features"),
     (dict(h=24), UNSUPPORTED, "hidden"),

@@ -54,7 +54,9 @@ SMALL = [(1, 32, 16), (3, 96, 48), (17, 4096, 2560), (64, 512, 1024), (5, 64, 32
          # more than 16 sequences: the thin-GEMM form when the row tiles divide
          # by 8, otherwise the per-wave form with 2, 3 or 4 row tiles per unit
          # (1056 rows: 66 tiles; 1088: 68) or one (1040: 65)
-         (32, 256, 1056), (48, 512, 1056), (64, 512, 1088), (40, 1024, 1040), (64, 4096, 4096)]
+         (32, 256, 1056), (48, 512, 1056), (64, 512, 1088), (40, 1024, 1040), (64, 4096, 4096),
+         # above 64 sequences: the thin-GEMM form with 8 or 16 column tiles
+         (65, 1024, 1024), (128, 512, 2048), (200, 256, 384), (256, 2048, 1280)]
 
 
 @pytest.mark.parametrize("b,k,h", SMALL, ids=[f"B{c[0]}-K{c[1]}-H{c[2]}" for c in SMALL])
@@ -105,3 +107,24 @@ def test_oproj_graph_replay(lib):
         torch.cuda.synchronize()
         check_ulps(host(z), rz, f"replay {rep} z")
         check_ulps(host(h), rh, f"replay {rep} h")
+
+
+def test_oproj_rows_not_8_byte_aligned(lib):
+    # the one-kernel epilogue (batch <= 16) moves four bf16 features at a
+    # time; rows offset by one element take the two passes, same results
+    import torch
+    w = W.build_oproj(5, 1024, 2048, seed=11)
+    attn, nw = dev_bf16(w.attn), dev_bf16(w.norm_w)
+    wp = lib.pack_weights(dev_bf16(w.w_o))
+    buf = torch.empty(3 * 5 * 2048 + 8, dtype=torch.bfloat16, device="cuda")
+    res = buf[1:1 + 5 * 2048].view(5, 2048)
+    res.copy_(dev_bf16(w.residual))
+    z = buf[2 + 5 * 2048:2 + 10 * 2048].view(5, 2048)
+    h = buf[3 + 10 * 2048:3 + 15 * 2048].view(5, 2048)
+    lib.o_proj_residual_norm(attn, wp, res, nw, z, h, eps=float(w.eps))
+    torch.cuda.synchronize()
+    rz, rh = ref(w)
+    check_ulps(host(z), rz, "z, unaligned rows")
+    check_ulps(host(h), rh, "h, unaligned rows")
+    aligned = run(lib, w)
+    assert np.array_equal(host(z), aligned[0]) and np.array_equal(host(h), aligned[1])

@@ -93,6 +93,10 @@ SMALL = [
     (33, 512, 6, 2, 64, dict(qk_norm=True, rotary_dim=32)),
     (64, 1024, 8, 1, 128, dict(qk_norm=True, bias=True)),
     (3, 256, 4, 2, 128, dict(rotary_dim=0)),
+    # above 64 sequences (the thin-GEMM form with 8 or 16 column tiles)
+    (100, 512, 4, 2, 128, dict(qk_norm=True)),
+    (256, 768, 12, 2, 64, dict(bias=True, rotary_dim=32, interleaved=True)),
+    (129, 256, 2, 1, 256, dict()),
 ]
 
 

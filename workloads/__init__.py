@@ -400,6 +400,10 @@ PRELUDE_CONFIGS: Dict[str, PreludeConfig] = {
         "prelude_falcon3", 16, 3072, 12, 4, 256, 14, "uniform:16:32768", 1000042.0,
         description="Falcon3-7B-shaped prelude, batch 16, hidden 3072, 12:4 heads, D=256, "
                     "theta 1000042"),
+    "prelude_ragged": PreludeConfig(
+        "prelude_ragged", 256, 5120, 40, 8, 128, 15, "zipf:1.2:16:32768", 1.0e6,
+        description="prelude of the ragged serving batch, batch 256, hidden 5120, 40:8 heads, "
+                    "D=128, positions Zipf(1.2) in [16, 32768], theta 1e6"),
 }
 
 
@@ -503,6 +507,8 @@ OPROJ_CONFIGS: Dict[str, OProjConfig] = {
     "oproj_70b": OProjConfig("oproj_70b", 4, 8192, 8192, 22, "70B-shaped o_proj, batch 4, 8192 -> 8192"),
     "oproj_falcon3": OProjConfig("oproj_falcon3", 16, 3072, 3072, 23,
                                  "Falcon3-7B-shaped o_proj, batch 16, 12 x 256 -> 3072"),
+    "oproj_ragged": OProjConfig("oproj_ragged", 256, 5120, 5120, 24,
+                                "o_proj of the ragged serving batch, batch 256, 40 x 128 -> 5120"),
 }
 
 
