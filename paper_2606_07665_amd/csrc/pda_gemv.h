@@ -42,8 +42,9 @@ constexpr int kGemvMaxSlots = 16;               // most workgroups sharing one r
 constexpr int kTileRows = 16;                   // rows of W per MFMA tile
 constexpr int kTileK = 32;                      // k per MFMA tile
 constexpr int kMaxGemvBatch = 256;              // sequences: sixteen 16-column tiles
-// Batches above this run only in the thin-GEMM form (gemv_xlds_kernel with
-// 8 or 16 column tiles), which needs the rows in groups of kXWaves tiles.
+// Batches above this run only in the thin-GEMM forms (gemv_xlds_kernel with
+// 8 column tiles, gemv_thin_kernel with 16, both with row groups of 8
+// tiles), which need the rows in groups of 128.
 constexpr int kMaxGemvBatchAnyRows = 64;
 constexpr int kPackThreads = 256;
 

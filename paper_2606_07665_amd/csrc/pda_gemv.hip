@@ -324,6 +324,173 @@ __global__ __launch_bounds__(kXWaves * 64, 1) void gemv_xlds_kernel(
   }
 }
 
+// Thin-GEMM form for the largest batches, with the activations copied
+// straight into LDS.  The B fragments of a chunk (kC k tiles x kNBT column
+// tiles, 1 KB each) are fetched by the workgroup's waves with buffer loads
+// that write LDS directly (no registers, no LDS store instructions): lane l
+// of such a load fetches x[16 bt + l % 16][32 kt + 8 (l / 16) .. +7], so each
+// fragment lands in LDS in exactly the order the matrix cores read it and
+// every LDS read of a fragment is one contiguous, conflict-free 1 KB wave
+// access.  Weights come from the packed tiles into registers, kR row tiles
+// per wave, so each B fragment read from LDS feeds kR MFMAs: at 256
+// sequences a wave of gemv_xlds_kernel reads 16 KB of fragments from LDS per
+// 1 KB weight tile, this form 8 KB.  Activations and weights are both kD
+// chunks ahead through a ring of kD + 1 stages, with one barrier per chunk.
+// The workgroup's range of (row group, k tile) units is walked as one
+// stream: where it passes into the next row group the accumulators are
+// written out as that group's partial and cleared, while the loads keep
+// flowing.  Partials and their layout are gemv_kernel's (group = kW kR row
+// tiles).
+template <int kNBT, int kW, int kR, int kC, int kD>
+__global__ __launch_bounds__(kW * 64, 1) void gemv_thin_kernel(const uint16_t* __restrict__ x,
+                                                               const uint16_t* __restrict__ wp,
+                                                               float* __restrict__ part, int batch, int n, int k,
+                                                               int slots) {
+  extern __shared__ __align__(1024) unsigned char xs[];  // [kD + 1][kC][kNBT] fragments of 1 KB
+  constexpr int kGroup = kW * kR;
+  constexpr int kFrags = kC * kNBT;
+  static_assert(kFrags % kW == 0, "every wave copies the same number of fragments");
+  constexpr int kDma = kFrags / kW;
+  constexpr int kStages = kD + 1;
+  constexpr int kLoads = kDma + kC * kR;  // vector memory instructions per wave and chunk
+  constexpr int kAhead = (kD - 1) * kLoads;
+  static_assert(kAhead < 64, "vmcnt holds at most 63");
+  constexpr int kWaitChunk = 0x0F70 | (kAhead & 15) | ((kAhead >> 4) << 14);
+  constexpr uint32_t kOutside = 0x80000000u;  // past any descriptor of x: reads zero
+  const int lane = threadIdx.x & 63;
+  const int wv = uniform(threadIdx.x >> 6);
+  const int64_t blocks = gridDim.x;
+  const int64_t blk = blockIdx.x;
+  const int kt_count = k / kTileK;
+  const int64_t units = static_cast<int64_t>(n / (kTileRows * kGroup)) * kt_count;
+  const int64_t u0 = blk * units / blocks;
+  const int64_t u1 = (blk + 1) * units / blocks;
+  const int nch = static_cast<int>((u1 - u0 + kC - 1) / kC);
+  // x rows at or past the batch fall outside the descriptor and read as zeros
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, static_cast<uint32_t>(batch) * k * 2u);
+  const uint32_t xlane = static_cast<uint32_t>(((lane & 15) * k + 8 * (lane >> 4)) * 2);
+
+  // load stream: the (group, k tile) of the next unit to fetch
+  int lg = static_cast<int>(u0 / kt_count);
+  int lkt = static_cast<int>(u0 - static_cast<int64_t>(lg) * kt_count);
+  int64_t lu = u0;
+  u32x4 wa[kStages][kC][kR];
+  auto issue = [&](int stage) __attribute__((always_inline)) {
+    int gj[kC], ktj[kC];
+    bool live[kC];
+#pragma unroll
+    for (int j = 0; j < kC; ++j) {
+      gj[j] = lg;
+      ktj[j] = lkt;
+      live[j] = lu < u1;
+      ++lu;
+      if (++lkt == kt_count) {
+        lkt = 0;
+        ++lg;
+      }
+    }
+#pragma unroll
+    for (int d = 0; d < kDma; ++d) {
+      const int f = wv * kDma + d;  // fragment (j, bt) of the chunk
+      const int j = f / kNBT;
+      const int bt = f - j * kNBT;
+      const uint32_t off = live[j] ? xlane + static_cast<uint32_t>((16 * bt * k + ktj[j] * kTileK) * 2) : kOutside;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rx, (__attribute__((address_space(3))) void*)(xs + (stage * kFrags + f) * 1024),
+                                               16, off, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kC; ++j) {
+#pragma unroll
+      for (int r = 0; r < kR; ++r) {
+        const int64_t tile = static_cast<int64_t>(gj[j]) * kGroup + wv * kR + r;
+        const __amdgpu_buffer_rsrc_t rw =
+            make_rsrc(wp + (tile * kt_count + ktj[j]) * (kTileRows * kTileK), live[j] ? 1024u : 0u);
+        wa[stage][j][r] = __builtin_amdgcn_raw_buffer_load_b128(rw, 16 * lane, 0, kCachePolicyNT);
+      }
+    }
+  };
+
+  f32x4 acc[kR][kNBT];
+#pragma unroll
+  for (int r = 0; r < kR; ++r)
+#pragma unroll
+    for (int bt = 0; bt < kNBT; ++bt) acc[r][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int r16 = lane & 15;
+  const int g4 = lane >> 4;
+  // this wave's rows of group g as the workgroup's partial of g, then cleared
+  auto flush = [&](int g) __attribute__((always_inline)) {
+    const int64_t first = (static_cast<int64_t>(g) * kt_count * blocks + blocks - 1) / units;  // first block of g
+    float* slot = part + (static_cast<int64_t>(g) * slots + (blk - first)) * kGroup * batch * kTileRows;
+#pragma unroll
+    for (int r = 0; r < kR; ++r)
+#pragma unroll
+      for (int bt = 0; bt < kNBT; ++bt) {
+        const int b = 16 * bt + r16;
+        if (b < batch) *reinterpret_cast<f32x4*>(slot + ((wv * kR + r) * batch + b) * kTileRows + 4 * g4) = acc[r][bt];
+        acc[r][bt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+  };
+  // compute stream: the (group, k tile) of the next unit to accumulate
+  int mg = lg;
+  int mkt = lkt;
+  int64_t mu = u0;
+  // A unit's partial flush comes before its B fragments are read: every
+  // fragment is requested before the first MFMA, and each MFMA waits only
+  // for its own.
+  auto mma = [&](int stage) __attribute__((always_inline)) {
+#pragma unroll
+    for (int j = 0; j < kC; ++j) {
+      if (mu < u1 && mkt == 0 && mu != u0) flush(mg - 1);
+      u32x4 b[kNBT];
+#pragma unroll
+      for (int bt = 0; bt < kNBT; ++bt)
+        b[bt] = *reinterpret_cast<const u32x4*>(xs + ((stage * kC + j) * kNBT + bt) * 1024 + 16 * lane);
+      __builtin_amdgcn_sched_barrier(0);  // keeps the reads ahead of the MFMAs
+      if (mu < u1) {
+#pragma unroll
+        for (int bt = 0; bt < kNBT; ++bt)
+#pragma unroll
+          for (int r = 0; r < kR; ++r)
+            acc[r][bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[stage][j][r]),
+                                                                 __builtin_bit_cast(bf16x8, b[bt]), acc[r][bt], 0, 0, 0);
+      }
+      ++mu;
+      if (++mkt == kt_count) {
+        mkt = 0;
+        ++mg;
+      }
+    }
+  };
+
+  // chunks past the range load nothing (zero-size reads), so every chunk
+  // issues the same loads and the wait for chunk c is one count
+#pragma unroll
+  for (int s = 0; s < kD; ++s) issue(s);
+  for (int c0 = 0; c0 < nch; c0 += kStages) {
+#pragma unroll
+    for (int s = 0; s < kStages; ++s) {
+      if (c0 + s < nch) {
+        // this wave's copies and weights of chunk c0 + s; after the barrier,
+        // every wave's copies, and stage s - 1 has been read by all.  A bare
+        // s_barrier, fenced for the compiler only: a workgroup fence would
+        // also wait for the copies still in flight into the later stages.
+        __builtin_amdgcn_s_waitcnt(kWaitChunk);
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        issue((s + kD) % kStages);
+        mma(s);
+      }
+    }
+  }
+  if (u1 > u0) {
+    // the group of the range's last unit
+    const int64_t last = u1 - 1;
+    flush(static_cast<int>(last / kt_count));
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // copies into LDS still in flight end before the workgroup does
+}
+
 // y[b][rows[r]] for kRows rows: for each, the sum in workgroup order of the
 // partials of its row group (kSlots >= the plan's slots, the most
 // workgroups that touch one group).  All partial counts are worked out
@@ -597,12 +764,15 @@ __global__ __launch_bounds__(kOProjOneThreads) void oproj_one_kernel(OProjArgs a
   const int tid = threadIdx.x;
   const int64_t base = static_cast<int64_t>(b) * a.hidden;
   float4 z[kGroups];
+  uint2 w[kGroups];  // norm weights, requested with everything else before the reduction
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < kGroups; ++j) {
     const int n = 4 * (tid + kOProjOneThreads * j);
     z[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    w[j] = make_uint2(0u, 0u);
     if (n < a.hidden) {
+      w[j] = *reinterpret_cast<const uint2*>(a.norm_w + n);
       const uint2 r = *reinterpret_cast<const uint2*>(a.residual + base + n);
       const float4 y = gemv_rows4<kSlots>(a.part, a.plan, a.batch, b, n);
       z[j] = make_float4(y.x + bf16_to_f32(static_cast<uint16_t>(r.x)), y.y + bf16_to_f32(static_cast<uint16_t>(r.x >> 16)),
@@ -626,12 +796,11 @@ __global__ __launch_bounds__(kOProjOneThreads) void oproj_one_kernel(OProjArgs a
   for (int j = 0; j < kGroups; ++j) {
     const int n = 4 * (tid + kOProjOneThreads * j);
     if (n < a.hidden) {
-      const uint2 w = *reinterpret_cast<const uint2*>(a.norm_w + n);
       uint2 o;
-      o.x = f32_to_bf16(z[j].x * inv * bf16_to_f32(static_cast<uint16_t>(w.x))) |
-            (static_cast<uint32_t>(f32_to_bf16(z[j].y * inv * bf16_to_f32(static_cast<uint16_t>(w.x >> 16)))) << 16);
-      o.y = f32_to_bf16(z[j].z * inv * bf16_to_f32(static_cast<uint16_t>(w.y))) |
-            (static_cast<uint32_t>(f32_to_bf16(z[j].w * inv * bf16_to_f32(static_cast<uint16_t>(w.y >> 16)))) << 16);
+      o.x = f32_to_bf16(z[j].x * inv * bf16_to_f32(static_cast<uint16_t>(w[j].x))) |
+            (static_cast<uint32_t>(f32_to_bf16(z[j].y * inv * bf16_to_f32(static_cast<uint16_t>(w[j].x >> 16)))) << 16);
+      o.y = f32_to_bf16(z[j].z * inv * bf16_to_f32(static_cast<uint16_t>(w[j].y))) |
+            (static_cast<uint32_t>(f32_to_bf16(z[j].w * inv * bf16_to_f32(static_cast<uint16_t>(w[j].y >> 16)))) << 16);
       *reinterpret_cast<uint2*>(a.normed_out + base + n) = o;
     }
   }
@@ -793,16 +962,41 @@ hipError_t launch_xlds(const GemvArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int kNBT, int kW, int kR, int kC, int kD>
+hipError_t launch_thin(const GemvArgs& a, hipStream_t st) {
+  constexpr int lds = (kD + 1) * kC * kNBT * 1024;
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
+  if (!bit || !(attr_set.load() & bit)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemv_thin_kernel<kNBT, kW, kR, kC, kD>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+    attr_set.fetch_or(bit);
+  }
+  hipLaunchKernelGGL((gemv_thin_kernel<kNBT, kW, kR, kC, kD>), dim3(a.plan.grid), dim3(kW * 64), lds, st, a.x, a.wp,
+                     a.part, a.batch, a.n, a.k, a.plan.slots);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
   const dim3 grid(a.plan.grid);
   const int nbt = (a.batch + 15) / 16;
   const int sl = a.plan.slots;
+  // Above 128 sequences the LDS-copy form with two row tiles per wave: on
+  // the 256-sequence prelude (5120 -> 7168) it ran 40.8 against 46.2 us for
+  // gemv_xlds_kernel<16>, on the o_proj (5120 -> 5120) 31.4 against 33.0.
+  // Up to 128 sequences gemv_xlds_kernel is the faster form (batch 64,
+  // 4096 -> 6144: 15.1 us against 17.1 for the LDS-copy form at its best
+  // depth).
   if (a.plan.xlds) {
     if (nbt == 2) return launch_xlds<2>(a, st);
     if (nbt == 3) return launch_xlds<3>(a, st);
     if (nbt == 4) return launch_xlds<4>(a, st);
     if (nbt <= 8) return launch_xlds<8>(a, st);  // column tiles past the batch read zeros
-    return launch_xlds<16>(a, st);
+    return launch_thin<16, 4, 2, 1, 3>(a, st);
   }
   if (nbt > 4) return hipErrorInvalidValue;  // above 64 sequences only the thin-GEMM form
   const bool grouped = a.plan.group > 1;
