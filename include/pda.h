@@ -353,8 +353,12 @@ int32_t pda_version(void);
  * steps / (min_steps * step phases))) workgroups of up to 8 waves.
  *   PDA_OPT_BLOCKS_PER_CU  workgroups per compute unit, 1..8
  *                          (default 1, env PDA_BLOCKS_PER_CU).
- *   PDA_OPT_MIN_STEPS      fewest 32-token steps a wave is given, >= 1
- *                          (default 2, env PDA_MIN_STEPS); a large value
+ *   PDA_OPT_MIN_STEPS      fewest 32-token steps a wave is given, >= 1,
+ *                          or 0 = the planner's choice (default, env
+ *                          PDA_MIN_STEPS): 2, or 1 for a call whose K and V
+ *                          (bounded by the page table) fit in 128 MB and
+ *                          whose 2-step plan has several workgroups but
+ *                          fewer than the device's CUs.  A large value
  *                          forces fewer splits, 1 the most.
  *   PDA_OPT_COMPUTE_PATH   where the attention kernel forms QK^T and P.V:
  *                          0 = matrix cores (default, env PDA_COMPUTE_PATH),
@@ -385,7 +389,11 @@ int32_t pda_version(void);
  *                          PDA_KV_GROUP): the largest divisor of
  *                          num_kv_heads not above it.  Fewer heads per
  *                          workgroup mean smaller partials per split piece
- *                          and shorter token rows read at a time.
+ *                          and shorter token rows read at a time.  The
+ *                          planner takes 8 (4 above 8 columns per kv head),
+ *                          and for a call whose K and V fit in 128 MB the
+ *                          largest group that cuts no (sequence, kv-head
+ *                          group) into more than 32 pieces.
  * Options are process-wide and apply to later calls.  pda_set_option
  * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
  * returns the current value or -1 for an unknown option.

@@ -67,10 +67,11 @@ int blocks_per_cu() {
   }
   return v;
 }
-int min_steps_per_wave() {
+// Fewest 32-token steps per wave the caller fixed (0 = the planner's choice).
+int min_steps_option() {
   int v = g_min_steps.load();
   if (v < 0) {
-    v = env_int("PDA_MIN_STEPS", 2, 1, kMaxMinSteps);
+    v = env_int("PDA_MIN_STEPS", 0, 0, kMaxMinSteps);
     g_min_steps.store(v);
   }
   return v;
@@ -161,6 +162,7 @@ struct Plan {
   int grid = 0;
   int waves = 0;   // per workgroup
   int hgs = 0;     // kv heads per workgroup
+  int min_steps = 0;   // fewest 32-token steps per wave
   bool fused = false;  // split sequences merged by their last workgroup
   int64_t slots = 0;
   int64_t off_acc = 0, off_ml = 0, off_pref = 0, bytes = 0;
@@ -182,16 +184,18 @@ int heads_per_group(int hkv, int max_waves) {
 // steps per wave at the largest context the page table allows.  Partial
 // slots: one per (workgroup, sequence piece), at most grid + batch * kv-head
 // groups, each holding `cols` (query token, head) rows per kv head.
-Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
+Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols,
+              int min_steps) {
   Plan pl;
   const int max_waves = pda::max_waves(d);
   pl.hgs = hgs;
+  pl.min_steps = min_steps;
   const int phases = max_waves / pl.hgs;
   pl.waves = pl.hgs * phases;
   const int64_t ngroups = hkv / pl.hgs;
   const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
   const int64_t steps_max = static_cast<int64_t>(batch) * ngroups * ((max_ctx + pda::kStep - 1) / pda::kStep);
-  const int64_t per_block = static_cast<int64_t>(min_steps_per_wave()) * phases;
+  const int64_t per_block = static_cast<int64_t>(min_steps) * phases;
   int64_t blocks = (steps_max + per_block - 1) / per_block;
   const int64_t target = static_cast<int64_t>(num_cus) * blocks_per_cu();
   if (blocks > target) blocks = target;
@@ -217,8 +221,16 @@ Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t
 // workgroup).  On MI355X the in-kernel hand-off (write-through stores, their
 // acknowledgement, the arrival atomic, coherent reloads) costs more than
 // the merge kernel's launch, so the option is off by default.
+// Calls whose K and V (bounded by the page table) fit in this many bytes are
+// latency-bound: they take the small-call rules of make_plan.
+constexpr int64_t kSmallCallBytes = int64_t{128} << 20;
+// Most pieces a small call cuts one (sequence, kv-head group) into.
+constexpr int64_t kSmallCallPieces = 32;
+constexpr int kDefaultMinSteps = 2;
+
 Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus, int cols) {
   const int cap = kv_group_cap();
+  const int ms_opt = min_steps_option();
   // A split piece leaves a partial of cols x head_dim fp32 per kv head it
   // covers; with more than 8 columns (several query tokens) those writes
   // cost more than the longer token rows save, so at most 4 kv heads go
@@ -226,7 +238,36 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   // columns or fewer, run slower with 4).
   const int dflt_most = cols > 8 ? std::min(4, pda::max_waves(d)) : pda::max_waves(d);
   const int most = cap > 0 && cap < pda::max_waves(d) ? cap : dflt_most;
-  const Plan dflt = plan_for(heads_per_group(hkv, most), batch, hkv, d, p, maxp, num_cus, cols);
+  Plan dflt = plan_for(heads_per_group(hkv, most), batch, hkv, d, p, maxp, num_cus, cols,
+                       ms_opt > 0 ? ms_opt : kDefaultMinSteps);
+  // Small calls (each 32-token step's K and V is a few KB; the whole call
+  // is a chain of latencies):
+  //  - a plan that splits the work but leaves CUs idle gives each wave one
+  //    step instead of two, doubling the workgroups (graph replay of 20
+  //    calls over cold K/V: 1 x 1024 tokens 15.1 -> 12.5 us, 4 x 1024
+  //    15.9 -> 13.6, 8 x 512 15.7 -> 13.8);
+  //  - fewer kv heads per workgroup when a sequence's heads would be cut
+  //    into more than kSmallCallPieces pieces: the same workgroups then take
+  //    longer runs of fewer heads, so less partial data and a lighter merge
+  //    (1 x 4096 tokens, 32:8 heads, 15.6 -> 14.4 us with 2 heads per
+  //    workgroup; 1 x 16384 25.1 -> 21.9 with 1; 1 x 8192, 64:8 heads,
+  //    20.7 -> 16.8 with 1).  Large calls keep 8 heads, whose 2 KB token
+  //    rows stream faster (long70b: 319.8 us per call with 8, 321.2 with 4,
+  //    329.6 with 2, 351.8 with 1).
+  const int64_t kv_bytes = static_cast<int64_t>(batch) * maxp * p * hkv * d * 4;
+  if (kv_bytes <= kSmallCallBytes) {
+    if (ms_opt == 0 && dflt.grid > 1 && dflt.grid < static_cast<int64_t>(num_cus) * blocks_per_cu())
+      dflt = plan_for(dflt.hgs, batch, hkv, d, p, maxp, num_cus, cols, 1);
+    if (cap == 0) {
+      for (int h = dflt.hgs; h >= 1; --h) {
+        if (hkv % h) continue;
+        if (h == 1 || static_cast<int64_t>(dflt.grid) * h <= kSmallCallPieces * batch * hkv) {
+          if (h != dflt.hgs) dflt = plan_for(h, batch, hkv, d, p, maxp, num_cus, cols, dflt.min_steps);
+          break;
+        }
+      }
+    }
+  }
   // (the vector-ALU variant, a measurement aid, keeps the merge kernel)
   if (dflt.grid == 1 || !fused_merge() || compute_path() != 0) return dflt;
   if (fused_merge() == 2) {  // every plan that has something to merge (tests)
@@ -236,9 +277,10 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   }
   for (int h = dflt.hgs; h >= 1; --h) {
     if (hkv % h) continue;
-    Plan c = plan_for(h, batch, hkv, d, p, maxp, num_cus, cols);
-    const int64_t most = static_cast<int64_t>(c.grid) * h * cols * d * 4;
-    if (c.grid > 1 && c.grid <= pda::kMaxFusedGrid && most <= pda::kFusedMergeBytes && c.bytes < (int64_t{1} << 31)) {
+    Plan c = plan_for(h, batch, hkv, d, p, maxp, num_cus, cols, dflt.min_steps);
+    const int64_t most_bytes = static_cast<int64_t>(c.grid) * h * cols * d * 4;
+    if (c.grid > 1 && c.grid <= pda::kMaxFusedGrid && most_bytes <= pda::kFusedMergeBytes &&
+        c.bytes < (int64_t{1} << 31)) {
       c.fused = true;
       return c;
     }
@@ -247,11 +289,14 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
 }
 
 // Workspace that any call of this shape may need: the largest plan over
-// every kv-head group size make_plan can pick, at 16 columns per kv head.
+// every kv-head group size and step count make_plan can pick, at 16 columns
+// per kv head.
 int64_t reserve_bytes(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus) {
+  const int ms_opt = min_steps_option();
   int64_t most = 0;
-  for (int h = 1; h <= pda::max_waves(d); ++h)
-    if (hkv % h == 0) most = std::max(most, plan_for(h, batch, hkv, d, p, maxp, num_cus, pda::kMaxCols).bytes);
+  for (int ms : {ms_opt > 0 ? ms_opt : kDefaultMinSteps, ms_opt > 0 ? ms_opt : 1})
+    for (int h = 1; h <= pda::max_waves(d); ++h)
+      if (hkv % h == 0) most = std::max(most, plan_for(h, batch, hkv, d, p, maxp, num_cus, pda::kMaxCols, ms).bytes);
   return most;
 }
 
@@ -684,7 +729,7 @@ int attention_call(const void* q, const void* k_cache, const void* v_cache, cons
   a.grid = pl.grid;
   a.waves = pl.waves;
   a.hgs = pl.hgs;
-  a.min_steps = min_steps_per_wave();
+  a.min_steps = pl.min_steps;
   a.scale = scale;
   a.nq = num_queries;
   a.window = window;
@@ -781,7 +826,7 @@ int pda_set_option(int32_t option, int32_t value) {
       g_blocks_per_cu.store(value);
       return PDA_OK;
     case PDA_OPT_MIN_STEPS:
-      if (value < 1) return fail(PDA_ERR_SHAPE, "min steps per wave must be >= 1");
+      if (value < 0) return fail(PDA_ERR_SHAPE, "min steps per wave must be >= 0 (0 = the planner's choice)");
       g_min_steps.store(value);
       return PDA_OK;
     case PDA_OPT_COMPUTE_PATH:
@@ -804,7 +849,7 @@ int pda_set_option(int32_t option, int32_t value) {
 int32_t pda_get_option(int32_t option) {
   switch (option) {
     case PDA_OPT_BLOCKS_PER_CU: return blocks_per_cu();
-    case PDA_OPT_MIN_STEPS: return min_steps_per_wave();
+    case PDA_OPT_MIN_STEPS: return min_steps_option();
     case PDA_OPT_COMPUTE_PATH: return compute_path();
     case PDA_OPT_FUSED_MERGE: return fused_merge();
     case PDA_OPT_KV_GROUP: return kv_group_cap();

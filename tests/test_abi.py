@@ -93,6 +93,23 @@ def test_planner_fills_the_device_and_sizes_the_workspace(lib):
         B.plan(1, 8, 2, 64, 16, 16, num_cus=0)
 
 
+def test_small_calls_take_one_step_per_wave(lib):
+    """Planner's choice (min steps 0): a call whose K/V fit in 128 MB and
+    whose two-step plan splits the work but leaves CUs idle gets one step
+    per wave (twice the workgroups); a caller's fixed value is kept; large
+    calls and single-workgroup calls are unchanged."""
+    assert B.get_option(B.OPT_MIN_STEPS) == 0
+    assert B.plan(1, 32, 8, 128, 16, 256, num_cus=256)[0] == 128   # 1 x 4096 tokens
+    assert B.plan(4, 32, 8, 128, 16, 64, num_cus=256)[0] == 128    # 4 x 1024
+    assert B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)[0] == 256  # long70b
+    assert B.plan(1, 8, 2, 64, 16, 16, num_cus=256)[0] == 1        # one workgroup: no merge
+    try:
+        B.set_option(B.OPT_MIN_STEPS, 2)
+        assert B.plan(1, 32, 8, 128, 16, 256, num_cus=256)[0] == 64
+    finally:
+        B.set_option(B.OPT_MIN_STEPS, 0)
+
+
 def test_planner_grid_scales_with_options(lib):
     try:
         B.set_option(B.OPT_BLOCKS_PER_CU, 2)
@@ -102,8 +119,10 @@ def test_planner_grid_scales_with_options(lib):
         assert B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)[0] == 1
     finally:
         B.set_option(B.OPT_BLOCKS_PER_CU, 1)
-        B.set_option(B.OPT_MIN_STEPS, 2)
-    assert B.get_option(B.OPT_MIN_STEPS) == 2
+        B.set_option(B.OPT_MIN_STEPS, 0)
+    assert B.get_option(B.OPT_MIN_STEPS) == 0
+    with pytest.raises(B.PdaError):
+        B.set_option(B.OPT_MIN_STEPS, -1)
     with pytest.raises(B.PdaError):
         B.set_option(B.OPT_BLOCKS_PER_CU, 0)
     with pytest.raises(B.PdaError):

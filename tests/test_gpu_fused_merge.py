@@ -27,7 +27,7 @@ def default_options(gpu_lib):
     yield
     gpu_lib.set_option(gpu_lib.OPT_FUSED_MERGE, 0)
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
-    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
+    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
 
 
 def ref(w):

@@ -23,12 +23,12 @@ def lib(gpu_lib):
 @pytest.fixture(autouse=True)
 def valu_path(gpu_lib):
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
-    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
+    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
     gpu_lib.set_option(gpu_lib.OPT_COMPUTE_PATH, 1)
     yield
     gpu_lib.set_option(gpu_lib.OPT_COMPUTE_PATH, 0)
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
-    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
+    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
 
 
 def ref(w):

@@ -25,10 +25,10 @@ def lib(gpu_lib):
 @pytest.fixture(autouse=True)
 def default_options(gpu_lib):
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
-    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
+    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
     yield
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
-    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
+    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
 
 
 def ref(w):

@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(scope="module")
 def lib(gpu_lib):
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
-    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 2)
+    gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
     return gpu_lib
 
 
