@@ -435,7 +435,7 @@ def release_workspaces() -> None:
 
 
 OPT_BLOCKS_PER_CU = 1
-OPT_MIN_STEPS = 2
+OPT_MIN_STEPS = 2     # fewest 32-token steps per wave (0 = the planner's choice, the default)
 OPT_COMPUTE_PATH = 3  # 0 = matrix cores (default), 1 = vector ALU (the measured alternative)
 OPT_FUSED_MERGE = 4   # 0 = merge kernel (default), 1 = fused merge for small plans, 2 = every multi-workgroup plan
 OPT_KV_GROUP = 5      # most kv heads per attention workgroup (0 = the planner's choice)
