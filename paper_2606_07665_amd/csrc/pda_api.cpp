@@ -1133,7 +1133,7 @@ int pda_o_proj_residual_norm(const void* attn, const void* w_packed, const void*
   int rc = device_cus(dev, &cus);
   if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const pda::GemvPlan plan = pda::plan_gemv(batch, hidden, in_features, cus);
+  const pda::GemvPlan plan = pda::plan_gemv(batch, hidden, in_features, cus, /*seq_major=*/true);
   void* ws = nullptr;
   if ((rc = workspace_for(dev, st, oproj_ws_bytes(plan, batch, hidden), &ws))) return rc;
   pda::GemvArgs g;
@@ -1182,7 +1182,7 @@ int pda_o_proj_workspace_reserve(int32_t batch, int32_t in_features, int32_t hid
   int cus = 0;
   int rc = device_cus(dev, &cus);
   if (rc) return rc;
-  const pda::GemvPlan plan = pda::plan_gemv(batch, hidden, in_features, cus);
+  const pda::GemvPlan plan = pda::plan_gemv(batch, hidden, in_features, cus, /*seq_major=*/true);
   void* ptr = nullptr;
   return workspace_for(dev, static_cast<hipStream_t>(stream), oproj_ws_bytes(plan, batch, hidden), &ptr);
 }

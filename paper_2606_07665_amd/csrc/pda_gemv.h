@@ -50,11 +50,16 @@ constexpr int kPackThreads = 256;
 
 // y[b, n] = sum_k x[b, k] W[n, k] over a packed W (see launch_pack), as
 // fp32 partials: a work unit is one 32-k tile of a group of `group`
-// consecutive 16-row tiles; part[g][j][i][b][16] holds the contribution of
-// the j-th workgroup that touched row group g, for its tile i.  GemvPlan says how
-// the waves split the work.
+// consecutive 16-row tiles; part[g][j][i][b][16] (tile-major) or
+// part[g][j][b][i][16] (sequence-major) holds the contribution of the j-th
+// workgroup that touched row group g, for its tile i and sequence b.
+// Tile-major partials are written as contiguous 1 KB rows; sequence-major
+// ones keep a sequence's rows of a group together (group x 64 bytes), which
+// the o_proj epilogue, one workgroup per sequence, reads as whole lines.
+// GemvPlan says how the waves split the work.
 struct GemvPlan {
   bool xlds;    // thin-GEMM form (gemv_xlds_kernel, kXWaves waves) instead of gemv_kernel
+  bool seq_major = false;  // partial layout (see above)
   int grid;     // workgroups
   int slots;    // partial slots per row group (an upper bound)
   int group;    // 16-row tiles per work unit (x fragments are reused across them)
@@ -62,7 +67,10 @@ struct GemvPlan {
   int kt_count;
 };
 
-GemvPlan plan_gemv(int batch, int n, int k, int num_cus);
+// seq_major: the caller's epilogue reads sequence-major partials better; the
+// plan takes that layout except in gemv_thin_kernel, whose tile-major
+// stores it would spread out.
+GemvPlan plan_gemv(int batch, int n, int k, int num_cus, bool seq_major = false);
 int64_t gemv_partial_floats(const GemvPlan& p, int batch, int n);
 
 struct GemvArgs {

@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kPackThreads) void pack_kernel(const uint16_t* __re
 template <int kNBT, int kR>
 __global__ __launch_bounds__(kGemvThreads, gemv_min_waves_per_simd(kNBT, kR)) void gemv_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wp, float* __restrict__ part, int batch, int n,
-    int k, int slots) {
+    int k, int slots, int seq_major) {
   __shared__ f32x4 red[kGemvWaves][kR * kNBT][64];
   const int lane = threadIdx.x & 63;
   const int wv = uniform(threadIdx.x >> 6);
@@ -191,7 +191,8 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_waves_per_simd(kNBT, kR)) vo
 #pragma unroll
       for (int w2 = 1; w2 < kGemvWaves; ++w2) sum += red[w2][p][lane];
       const int b = 16 * bt + r;
-      if (b < batch) *reinterpret_cast<f32x4*>(slot + (i * batch + b) * kTileRows + 4 * g4) = sum;
+      const int row = seq_major ? b * kR + i : i * batch + b;
+      if (b < batch) *reinterpret_cast<f32x4*>(slot + row * kTileRows + 4 * g4) = sum;
     }
     __syncthreads();  // red is rewritten by the next segment
     u = seg_end;
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_waves_per_simd(kNBT, kR)) vo
 template <int kNBT>
 __global__ __launch_bounds__(kXWaves * 64, 1) void gemv_xlds_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ wp, float* __restrict__ part, int batch, int n,
-    int k, int slots) {
+    int k, int slots, int seq_major) {
   extern __shared__ __align__(16) unsigned char xs[];  // [kXRing][kNBT * 16 rows][kXRowBytes]
   constexpr int kRows = kNBT * kTileRows;
   constexpr int kBuf = kRows * kXRowBytes;
@@ -316,7 +317,8 @@ __global__ __launch_bounds__(kXWaves * 64, 1) void gemv_xlds_kernel(
 #pragma unroll
     for (int bt = 0; bt < kNBT; ++bt) {
       const int b = 16 * bt + r;
-      if (b < batch) *reinterpret_cast<f32x4*>(slot + (wv * batch + b) * kTileRows + 4 * g4) = acc[bt];
+      const int row = seq_major ? b * kXWaves + wv : wv * batch + b;
+      if (b < batch) *reinterpret_cast<f32x4*>(slot + row * kTileRows + 4 * g4) = acc[bt];
     }
     __builtin_amdgcn_s_waitcnt(0x0F70);  // the loads issued past the segment
     __syncthreads();                     // the LDS buffers are rewritten by the next segment
@@ -527,7 +529,9 @@ __device__ __forceinline__ void gemv_rows(const float* __restrict__ part, const 
   for (int r = 0; r < kRows; ++r) {
     const int i = (rows[r] >> 4) - g[r] * p.group;
     const float* q = part + static_cast<int64_t>(g[r]) * p.slots * slot_floats +
-                     (static_cast<int64_t>(i) * batch + b) * kTileRows + (rows[r] & 15);
+                     (p.seq_major ? static_cast<int64_t>(b) * p.group + i : static_cast<int64_t>(i) * batch + b) *
+                         kTileRows +
+                     (rows[r] & 15);
 #pragma unroll
     for (int j = 0; j < kSlots; ++j) v[r][j] = q[(j < cnt[r] ? j : cnt[r] - 1) * slot_floats];
   }
@@ -560,7 +564,9 @@ __device__ __forceinline__ float4 gemv_rows4(const float* __restrict__ part, con
   const int64_t slot_floats = static_cast<int64_t>(p.group) * batch * kTileRows;
   const int i = (n >> 4) - g * p.group;
   const float* q = part + static_cast<int64_t>(g) * p.slots * slot_floats +
-                   (static_cast<int64_t>(i) * batch + b) * kTileRows + (n & 15);
+                   (p.seq_major ? static_cast<int64_t>(b) * p.group + i : static_cast<int64_t>(i) * batch + b) *
+                       kTileRows +
+                   (n & 15);
   float4 v[kSlots];
 #pragma unroll
   for (int j = 0; j < kSlots; ++j) v[j] = *reinterpret_cast<const float4*>(q + (j < cnt ? j : cnt - 1) * slot_floats);
@@ -869,7 +875,7 @@ hipError_t launch_pack(const uint16_t* w, uint16_t* wp, int n, int k, hipStream_
   return hipGetLastError();
 }
 
-GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
+GemvPlan plan_gemv(int batch, int n, int k, int num_cus, bool seq_major) {
   GemvPlan p;
   const int nbt = (batch + 15) / 16;
   const int tiles = n / kTileRows;
@@ -905,6 +911,9 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
     p.grid = static_cast<int>(grid);
     p.blocks = grid;
     p.slots = static_cast<int>((static_cast<int64_t>(p.kt_count) * p.blocks + p.units - 1) / p.units + 1);
+    // above 8 column tiles (gemv_thin_kernel) the partials stay tile-major:
+    // sequence-major stores there made the 256-sequence GEMVs 15-20% slower
+    p.seq_major = seq_major && nbt <= 8;
     return p;
   }
   if (nbt > 1 && tiles % nbt == 0) {
@@ -935,6 +944,7 @@ GemvPlan plan_gemv(int batch, int n, int k, int num_cus) {
   p.blocks = grid;
   // workgroups touching one row group: its kt_count units span at most this many ranges
   p.slots = static_cast<int>((static_cast<int64_t>(p.kt_count) * p.blocks + p.units - 1) / p.units + 1);
+  p.seq_major = seq_major;
   return p;
 }
 
@@ -958,7 +968,7 @@ hipError_t launch_xlds(const GemvArgs& a, hipStream_t st) {
     attr_set.fetch_or(bit);
   }
   hipLaunchKernelGGL((gemv_xlds_kernel<kNBT>), dim3(a.plan.grid), dim3(kXWaves * 64), lds, st, a.x, a.wp, a.part,
-                     a.batch, a.n, a.k, a.plan.slots);
+                     a.batch, a.n, a.k, a.plan.slots, a.plan.seq_major ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -1001,7 +1011,8 @@ hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
   if (nbt > 4) return hipErrorInvalidValue;  // above 64 sequences only the thin-GEMM form
   const bool grouped = a.plan.group > 1;
 #define PDA_GEMV(NBT, R) \
-  hipLaunchKernelGGL((gemv_kernel<NBT, R>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl)
+  hipLaunchKernelGGL((gemv_kernel<NBT, R>), grid, dim3(kGemvThreads), 0, st, a.x, a.wp, a.part, a.batch, a.n, a.k, sl, \
+                     a.plan.seq_major ? 1 : 0)
   switch (nbt) {
     case 1: if (grouped) PDA_GEMV(1, 4); else PDA_GEMV(1, 1); break;
     case 2: if (grouped) PDA_GEMV(2, 2); else PDA_GEMV(2, 1); break;
