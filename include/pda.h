@@ -394,6 +394,19 @@ int32_t pda_version(void);
  *                          and for a call whose K and V fit in 128 MB the
  *                          largest group that cuts no (sequence, kv-head
  *                          group) into more than 32 pieces.
+ *   PDA_OPT_FIXED_SPLIT    1 (default, env PDA_FIXED_SPLIT): a call whose
+ *                          K and V fit in 128 MB, planned on several
+ *                          workgroups for at most half the device's
+ *                          workgroups' worth of (sequence, kv-head group)
+ *                          pairs, cuts every pair into the same number of
+ *                          chunks of whole 32-token steps sized by the page
+ *                          table's largest context, so that a workgroup
+ *                          knows its piece from its index (no steps prefix
+ *                          on the way to the first loads; the merge finds
+ *                          the pieces from the lengths).  0: every call is
+ *                          split stream-K over the actual lengths.  Both
+ *                          are deterministic for a fixed plan; they round
+ *                          differently.
  * Options are process-wide and apply to later calls.  pda_set_option
  * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
  * returns the current value or -1 for an unknown option.
@@ -403,6 +416,7 @@ int32_t pda_version(void);
 #define PDA_OPT_COMPUTE_PATH 3
 #define PDA_OPT_FUSED_MERGE 4
 #define PDA_OPT_KV_GROUP 5
+#define PDA_OPT_FIXED_SPLIT 6
 int pda_set_option(int32_t option, int32_t value);
 int32_t pda_get_option(int32_t option);
 

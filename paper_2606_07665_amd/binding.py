@@ -181,10 +181,14 @@ def raw_call(q_ptr, k_ptr, v_ptr, bt_ptr, lens_ptr, out_ptr, batch, hq, hkv, d, 
                                          page_size, num_pages, max_pages, ctypes.c_float(scale), stream_ptr)
 
 
-def _stream_ptr(stream):
+def _stream_ptr(stream, device=None):
+    """The HIP stream handle of ``stream``, or of torch's current stream on
+    ``device`` (default: the current device)."""
     import torch
     if stream is None:
-        stream = torch.cuda.current_stream()
+        # the raw handle without building a Stream object (~3 us a call)
+        return ctypes.c_void_p(torch._C._cuda_getCurrentRawStream(
+            torch.cuda.current_device() if device is None else device))
     return ctypes.c_void_p(stream.cuda_stream)
 
 
@@ -236,11 +240,25 @@ def _cache_specs(k_cache, v_cache, block_table, context_lens):
 
 def _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out):
     """Checks of a one-query attention call; returns (B, Hq, D, num_pages,
-    page_size, Hkv)."""
+    page_size, Hkv, device).  The usual case (every check passes) reads each
+    property once; otherwise _validate runs the full checks and raises the
+    specific error."""
     import torch
+    bf, i32 = torch.bfloat16, torch.int32
+    qs, ks = q.shape, k_cache.shape
+    if (len(qs) == 3 and len(ks) == 4 and out.shape == qs and v_cache.shape == ks and ks[3] == qs[2]
+            and block_table.dim() == 2 and block_table.shape[0] == qs[0] and context_lens.shape == (qs[0],)
+            and q.dtype is bf and out.dtype is bf and k_cache.dtype is bf and v_cache.dtype is bf
+            and block_table.dtype is i32 and context_lens.dtype is i32):
+        dev = q.get_device()
+        if (dev >= 0 and out.get_device() == dev and k_cache.get_device() == dev and v_cache.get_device() == dev
+                and block_table.get_device() == dev and context_lens.get_device() == dev
+                and q.is_contiguous() and out.is_contiguous() and k_cache.is_contiguous()
+                and v_cache.is_contiguous() and block_table.is_contiguous() and context_lens.is_contiguous()):
+            return qs[0], qs[1], qs[2], ks[0], ks[1], ks[2], dev
     sz = _validate([("q", q, torch.bfloat16, "B Hq D"), *_cache_specs(k_cache, v_cache, block_table, context_lens),
                     ("out", out, torch.bfloat16, "B Hq D")])
-    return sz["B"], sz["Hq"], sz["D"], sz["N"], sz["P"], sz["Hkv"]
+    return sz["B"], sz["Hq"], sz["D"], sz["N"], sz["P"], sz["Hkv"], q.get_device()
 
 
 def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, scale, stream=None):
@@ -250,10 +268,10 @@ def paged_decode_attention(q, k_cache, v_cache, block_table, context_lens, out, 
     block_table: int32 [B, maxp]; context_lens: int32 [B]; all contiguous on
     one GPU.  Launches on ``stream`` (default: torch's current stream).
     """
-    b, hq, d, n, p, hkv = _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out)
+    b, hq, d, n, p, hkv, dev = _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out)
     _check(raw_call(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
                     context_lens.data_ptr(), out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1],
-                    float(scale), _stream_ptr(stream)))
+                    float(scale), _stream_ptr(stream, dev)))
     return out
 
 
@@ -261,11 +279,11 @@ def paged_decode_attention_noalloc(q, k_cache, v_cache, block_table, context_len
     """:func:`paged_decode_attention` through the entry point that allocates
     nothing: its partials go to the library's fixed per-device scratch
     (NOALLOC_SCRATCH_BYTES).  Calls on one device must not overlap in time."""
-    b, hq, d, n, p, hkv = _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out)
+    b, hq, d, n, p, hkv, dev = _check_attention_args(q, k_cache, v_cache, block_table, context_lens, out)
     _check(load().paged_decode_attention_noalloc(
         q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(),
         out.data_ptr(), b, hq, hkv, d, p, n, block_table.shape[1], ctypes.c_float(float(scale)),
-        _stream_ptr(stream)))
+        _stream_ptr(stream, dev)))
     return out
 
 
@@ -439,6 +457,7 @@ OPT_MIN_STEPS = 2     # fewest 32-token steps per wave (0 = the planner's choice
 OPT_COMPUTE_PATH = 3  # 0 = matrix cores (default), 1 = vector ALU (the measured alternative)
 OPT_FUSED_MERGE = 4   # 0 = merge kernel (default), 1 = fused merge for small plans, 2 = every multi-workgroup plan
 OPT_KV_GROUP = 5      # most kv heads per attention workgroup (0 = the planner's choice)
+OPT_FIXED_SPLIT = 6   # 1 = fixed split for latency-bound calls (default), 0 = stream-K for every call
 
 
 def set_option(option: int, value: int) -> None:

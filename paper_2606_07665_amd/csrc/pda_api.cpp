@@ -58,6 +58,7 @@ std::atomic<int> g_min_steps{-1};
 std::atomic<int> g_compute_path{-1};
 std::atomic<int> g_fused_merge{-1};
 std::atomic<int> g_kv_group{-1};
+std::atomic<int> g_fixed_split{-1};
 
 int blocks_per_cu() {
   int v = g_blocks_per_cu.load();
@@ -101,6 +102,17 @@ int kv_group_cap() {
   if (v < 0) {
     v = env_int("PDA_KV_GROUP", 0, 0, pda::kMaxWaves);
     g_kv_group.store(v);
+  }
+  return v;
+}
+
+// 1 (default): latency-bound calls take the fixed split; 0: every call
+// takes the stream-K split.
+int fixed_split() {
+  int v = g_fixed_split.load();
+  if (v < 0) {
+    v = env_int("PDA_FIXED_SPLIT", 1, 0, 1);
+    g_fixed_split.store(v);
   }
   return v;
 }
@@ -164,6 +176,8 @@ struct Plan {
   int hgs = 0;     // kv heads per workgroup
   int min_steps = 0;   // fewest 32-token steps per wave
   bool fused = false;  // split sequences merged by their last workgroup
+  int chunks = 0;       // > 0: fixed split, chunks per (sequence, kv-head group)
+  int chunk_steps = 0;  // 32-token steps per chunk of the fixed split
   int64_t slots = 0;
   int64_t off_acc = 0, off_ml = 0, off_pref = 0, bytes = 0;
 };
@@ -211,6 +225,42 @@ Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t
   return pl;
 }
 
+// The fixed split of a latency-bound call with the kv-head grouping and
+// step count of `base`: every (sequence, kv-head group) is cut into the same
+// number of chunks of whole 32-token steps, as many as the stream-K plan
+// would give it at the page table's largest context (but at least 2 and
+// within the device's workgroups), so each workgroup knows its piece from
+// its index.  Returns a plan with grid 0 where it does not apply: one
+// workgroup, or more sequences than half the device's workgroups (the
+// stream-K split balances those better).  One partial slot per workgroup.
+Plan plan_fixed(const Plan& base, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus,
+                int cols) {
+  Plan pl = base;
+  pl.grid = 0;
+  const int phases = pl.waves / pl.hgs;
+  const int64_t seqs = static_cast<int64_t>(batch) * (hkv / pl.hgs);
+  const int64_t target = static_cast<int64_t>(num_cus) * blocks_per_cu();
+  const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
+  const int64_t steps_seq = (max_ctx + pda::kStep - 1) / pda::kStep;
+  const int64_t per_block = static_cast<int64_t>(pl.min_steps) * phases;
+  if (base.grid <= 1 || 2 * seqs > target) return pl;
+  int64_t chunks = std::min((steps_seq + per_block - 1) / per_block, target / seqs);
+  chunks = std::max<int64_t>(chunks, 1);
+  const int64_t chunk_steps = (steps_seq + chunks - 1) / chunks;
+  chunks = (steps_seq + chunk_steps - 1) / chunk_steps;  // no chunk wholly past the largest context
+  if (chunks < 2) return pl;
+  pl.grid = static_cast<int>(seqs * chunks);
+  pl.chunks = static_cast<int>(chunks);
+  pl.chunk_steps = static_cast<int>(chunk_steps);
+  pl.slots = pl.grid;
+  const int64_t rows = pl.slots * pl.hgs * cols;
+  pl.off_acc = 0;
+  pl.off_ml = align256(rows * d * 4);
+  pl.off_pref = pl.off_ml + align256(rows * 2 * 4);
+  pl.bytes = pl.off_pref + align256((static_cast<int64_t>(batch) + 1 + pl.grid) * 4);
+  return pl;
+}
+
 // The plan of a call.  The default reads all kv heads of a group of up to 8
 // together (the faster access order for long streams) and merges split
 // sequences in a separate kernel.  With PDA_OPT_FUSED_MERGE = 1, a grid of
@@ -254,8 +304,12 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   //    20.7 -> 16.8 with 1).  Large calls keep 8 heads, whose 2 KB token
   //    rows stream faster (long70b: 319.8 us per call with 8, 321.2 with 4,
   //    329.6 with 2, 351.8 with 1).
+  //  - the fixed split (plan_fixed) unless PDA_OPT_FIXED_SPLIT is 0: the
+  //    first K/V loads leave ~3 us earlier and the merge needs no prefix
+  //    (1 x 4096 tokens, 32:8 heads: ...).
   const int64_t kv_bytes = static_cast<int64_t>(batch) * maxp * p * hkv * d * 4;
-  if (kv_bytes <= kSmallCallBytes) {
+  const bool small = kv_bytes <= kSmallCallBytes;
+  if (small) {
     if (ms_opt == 0 && dflt.grid > 1 && dflt.grid < static_cast<int64_t>(num_cus) * blocks_per_cu())
       dflt = plan_for(dflt.hgs, batch, hkv, d, p, maxp, num_cus, cols, 1);
     if (cap == 0) {
@@ -269,7 +323,13 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
     }
   }
   // (the vector-ALU variant, a measurement aid, keeps the merge kernel)
-  if (dflt.grid == 1 || !fused_merge() || compute_path() != 0) return dflt;
+  if (dflt.grid == 1 || !fused_merge() || compute_path() != 0) {
+    if (small && dflt.grid > 1 && fixed_split() && compute_path() == 0) {
+      const Plan f = plan_fixed(dflt, batch, hkv, d, p, maxp, num_cus, cols);
+      if (f.grid > 1) return f;
+    }
+    return dflt;
+  }
   if (fused_merge() == 2) {  // every plan that has something to merge (tests)
     Plan c = dflt;
     c.fused = c.grid <= pda::kMaxFusedGrid && c.bytes < (int64_t{1} << 31);
@@ -296,7 +356,11 @@ int64_t reserve_bytes(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t 
   int64_t most = 0;
   for (int ms : {ms_opt > 0 ? ms_opt : kDefaultMinSteps, ms_opt > 0 ? ms_opt : 1})
     for (int h = 1; h <= pda::max_waves(d); ++h)
-      if (hkv % h == 0) most = std::max(most, plan_for(h, batch, hkv, d, p, maxp, num_cus, pda::kMaxCols, ms).bytes);
+      if (hkv % h == 0) {
+        const Plan pl = plan_for(h, batch, hkv, d, p, maxp, num_cus, pda::kMaxCols, ms);
+        most = std::max(most, pl.bytes);
+        most = std::max(most, plan_fixed(pl, batch, hkv, d, p, maxp, num_cus, pda::kMaxCols).bytes);
+      }
   return most;
 }
 
@@ -736,6 +800,8 @@ int attention_call(const void* q, const void* k_cache, const void* v_cache, cons
   a.valu_cols = valu_cols;
   a.ws_cnt = cnt;
   a.fused = pl.fused;
+  a.chunks = pl.chunks;
+  a.chunk_steps = pl.chunk_steps;
 
   const Rec rec = noalloc ? Rec{nullptr, nullptr, nullptr, 0} : prof_begin(0);
   const bool prof = rec.a != nullptr;
@@ -841,6 +907,10 @@ int pda_set_option(int32_t option, int32_t value) {
       if (value < 0 || value > pda::kMaxWaves) return fail(PDA_ERR_SHAPE, "kv group must be in [0, %d]", pda::kMaxWaves);
       g_kv_group.store(value);
       return PDA_OK;
+    case PDA_OPT_FIXED_SPLIT:
+      if (value < 0 || value > 1) return fail(PDA_ERR_SHAPE, "fixed split must be 0 or 1");
+      g_fixed_split.store(value);
+      return PDA_OK;
     default:
       return fail(PDA_ERR_UNSUPPORTED, "unknown option %d", option);
   }
@@ -853,6 +923,7 @@ int32_t pda_get_option(int32_t option) {
     case PDA_OPT_COMPUTE_PATH: return compute_path();
     case PDA_OPT_FUSED_MERGE: return fused_merge();
     case PDA_OPT_KV_GROUP: return kv_group_cap();
+    case PDA_OPT_FIXED_SPLIT: return fixed_split();
     default: return -1;
   }
 }

@@ -39,6 +39,11 @@ struct LaunchArgs {
   int window;  // sliding window in tokens, 0 = none
   int valu_cols = 0;  // 0: products on the matrix cores; 4 or 8: vector-ALU variant for that many columns
   bool fused = false; // split sequences merged by their last workgroup (no merge kernel)
+  // > 0: the fixed split of small calls -- workgroup w takes chunk w % chunks
+  // (chunk_steps 32-token steps) of (sequence, kv-head group) w / chunks;
+  // grid = batch x (hkv / hgs) x chunks and merge_fixed_kernel merges
+  int chunks = 0;
+  int chunk_steps = 0;
 };
 
 // The fused merge is planned when the most partial data one sequence can

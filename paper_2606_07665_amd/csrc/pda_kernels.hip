@@ -182,10 +182,35 @@ __device__ __forceinline__ f32x2 load_coherent2(__amdgpu_buffer_rsrc_t r, int64_
                                                                          kCachePolicyCoherent));
 }
 
+// Integer quotients on the way to the first loads.  The compiler expands a
+// 64-bit integer division into ~120 dependent instructions (a 32-bit one
+// into ~25); the chain of them between the steps prefix and the first
+// page-id load took ~2.5 us of every call on MI355X.  Both helpers divide
+// in fp64 instead:
+//  * div_small (0 <= a < 2^31, 0 < b < 2^31): both operands convert
+//    exactly and the quotient a/b, correctly rounded, cannot reach the next
+//    integer (it is at least 1/b below it, more than the rounding error of a
+//    quotient below 2^31), so truncation gives floor(a / b);
+//  * div_floor (0 <= a < 2^62, 0 < b, quotient < 2^50): three roundings
+//    leave the fp64 quotient within 3/8 of a/b, so its truncation is within
+//    one of floor(a / b), which one integer remainder test corrects.
+__device__ __forceinline__ int div_small(int a, int b) {
+  return static_cast<int>(static_cast<double>(a) / static_cast<double>(b));
+}
+__device__ __forceinline__ int64_t div_floor(int64_t a, int64_t b) {
+  int64_t q = static_cast<int64_t>(static_cast<double>(a) / static_cast<double>(b));
+  const int64_t r = a - q * b;
+  if (r < 0)
+    --q;
+  else if (r >= b)
+    ++q;
+  return q;
+}
+
 // Workgroup that owns flattened step x of `total`, when `parts` workgroups
 // split [0, total) into ranges [w*total/parts, (w+1)*total/parts).
 __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t parts) {
-  return ((x + 1) * parts - 1) / total;
+  return div_floor((x + 1) * parts - 1, total);
 }
 
 // Value of a partner lane in the same 16-lane row (DPP), for the vector-ALU
@@ -291,22 +316,42 @@ __device__ void merge_in_workgroup(uint16_t* __restrict__ out, const float* __re
 // (bf16 dot2 for QK^T, fp32 FMA for P.V) for up to kNC (query token, head)
 // columns at D = 128 -- the measured alternative to the matrix cores,
 // selected with PDA_OPT_COMPUTE_PATH.
-template <int D, bool kLanePages, int kNC = 0, bool kFused = false>
+// kFixed: the fixed split of small calls.  Workgroup w takes chunk
+// w % chunks (chunk_steps steps) of the (sequence, kv-head group)
+// w / chunks, known from its index alone: no steps prefix, and the length,
+// q and the first page ids are requested together at entry (a small call
+// is a chain of memory latencies; the prefix and the stream-K range put
+// ~3 us of them before the first K/V load on MI355X).  The pieces are
+// merged by merge_fixed_kernel.
+template <int D, bool kLanePages, int kNC = 0, bool kFused = false, bool kFixed = false>
 __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kc,
     const uint16_t* __restrict__ vc, const int32_t* __restrict__ bt,
     const int32_t* __restrict__ lens, uint16_t* __restrict__ out,
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_pref,
     int32_t* __restrict__ ws_cnt, int batch, int hq, int hkv, int group, int hgs, int page_shift,
-    int num_pages, int maxp, int min_steps, float scale_log2, int nq, int window) {
+    int num_pages, int maxp, int min_steps, float scale_log2, int nq, int window, int chunks,
+    int chunk_steps) {
   constexpr bool kValu = kNC > 0;
   static_assert(!kValu || (D == 128 && !kLanePages && (kNC == 4 || kNC == 8)), "vector-ALU variant shapes");
+  static_assert(!kFixed || (!kValu && !kFused), "the fixed split runs on the matrix cores with the merge kernel");
+  // Every argument in SGPRs before anything waits on one: the compiler
+  // otherwise requests them in two groups with a wait between (the second
+  // group only where the first pointer is used), and since scalar loads
+  // complete out of order, a wait for one of them is a wait for all, so the
+  // length, page-id and q loads queued behind another round trip.  Later
+  // uses of the integer arguments depend on this statement; the pointers
+  // are inputs only, so their loads stay global loads.
+  asm volatile(""
+               : "+s"(batch), "+s"(hq), "+s"(hkv), "+s"(group), "+s"(hgs), "+s"(page_shift), "+s"(num_pages),
+                 "+s"(maxp), "+s"(min_steps), "+s"(nq), "+s"(window), "+s"(chunks), "+s"(chunk_steps)
+               : "s"(q), "s"(kc), "s"(vc), "s"(bt), "s"(lens), "s"(out), "s"(ws_acc), "s"(ws_ml), "s"(ws_pref));
   using S = Shape<D, kValu>;
   extern __shared__ __align__(16) unsigned char smem[];
   const int nthreads = blockDim.x;
   const int nwaves = nthreads >> 6;
-  const int phases = nwaves / hgs;  // waves per kv head, interleaving steps
-  const int ngroups = hkv / hgs;    // kv-head groups per sequence
+  const int phases = div_small(nwaves, hgs);  // waves per kv head, interleaving steps
+  const int ngroups = div_small(hkv, hgs);    // kv-head groups per sequence
   const int ncols = group * nq;     // MFMA columns in use: (query token, head of the group)
   int32_t* pref = reinterpret_cast<int32_t*>(smem + pref_offset<D, kValu>(nwaves));
   int32_t* lens_s = pref + batch + 1;  // clamped lengths (kLensInLds)
@@ -317,73 +362,75 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   const int page = 1 << page_shift;
   const int max_ctx = maxp << page_shift;
 
-  // ---- per-block prefix over the batch of 32-token steps per sequence ----
-  // Each thread sums a run of sequences; a shuffle scan inside each wave and
-  // one exchange of wave totals through LDS make the prefix with two
-  // barriers (a tree over the workgroup took ~2 us of barriers).
-  {
-    if constexpr (S::kLensInLds) {
-      // the lengths go to LDS first, read by consecutive threads with
-      // several loads in flight each (a run of them read one after another
-      // by its owner cost ~0.5 us per load at a batch of 8192)
-#pragma unroll 8
-      for (int b = tid; b < batch; b += nthreads) lens_s[b] = clamp_len(lens[b], max_ctx);
+  if constexpr (!kFixed) {
+    // ---- per-block prefix over the batch of 32-token steps per sequence ----
+    // Each thread sums a run of sequences; a shuffle scan inside each wave and
+    // one exchange of wave totals through LDS make the prefix with two
+    // barriers (a tree over the workgroup took ~2 us of barriers).
+    {
+      if constexpr (S::kLensInLds) {
+        // the lengths go to LDS first, read by consecutive threads with
+        // several loads in flight each (a run of them read one after another
+        // by its owner cost ~0.5 us per load at a batch of 8192)
+  #pragma unroll 8
+        for (int b = tid; b < batch; b += nthreads) lens_s[b] = clamp_len(lens[b], max_ctx);
+        __syncthreads();
+      }
+      const int per = (batch + nthreads - 1) / nthreads;
+      const int lo = tid * per;
+      const int hi = min(batch, lo + per);
+      int sum = 0;
+      for (int b = lo; b < hi; ++b) sum += seq_steps(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx), nq, window);
+      int incl = sum;  // inclusive prefix within the wave
+  #pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off, 64);
+        if ((tid & 63) >= off) incl += v;
+      }
+      if ((tid & 63) == 63) scan[tid >> 6] = incl;  // wave totals
+      __syncthreads();
+      int before = 0;
+      for (int w = 0; w < (tid >> 6); ++w) before += scan[w];
+      int run = before + incl - sum;
+      for (int b = lo; b < hi; ++b) {
+        pref[b] = run;
+        run += seq_steps(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx), nq, window);
+      }
+      if (tid == nthreads - 1) pref[batch] = before + incl;
       __syncthreads();
     }
-    const int per = (batch + nthreads - 1) / nthreads;
-    const int lo = tid * per;
-    const int hi = min(batch, lo + per);
-    int sum = 0;
-    for (int b = lo; b < hi; ++b) sum += seq_steps(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx), nq, window);
-    int incl = sum;  // inclusive prefix within the wave
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_up(incl, off, 64);
-      if ((tid & 63) >= off) incl += v;
-    }
-    if ((tid & 63) == 63) scan[tid >> 6] = incl;  // wave totals
-    __syncthreads();
-    int before = 0;
-    for (int w = 0; w < (tid >> 6); ++w) before += scan[w];
-    int run = before + incl - sum;
-    for (int b = lo; b < hi; ++b) {
-      pref[b] = run;
-      run += seq_steps(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx), nq, window);
-    }
-    if (tid == nthreads - 1) pref[batch] = before + incl;
-    __syncthreads();
-  }
-  if (blockIdx.x == 0) {
-    // the merge kernel reads the same prefix; empty sequences get zero rows
-    // here: each wave tests 64 sequences at a time and clears the rows of the
-    // empty ones together (testing one sequence after another cost ~65 ns
-    // each, half a millisecond at a batch of 8192, on this workgroup alone)
-    for (int b = tid; b <= batch; b += nthreads) ws_pref[b] = pref[b];
-    const int row16 = nq * hq * D / 8;  // 16-byte stores per sequence
-    const int ln = tid & 63;
-    for (int c = (tid >> 6) * 64; c < batch; c += nwaves * 64) {
-      const int bb = c + ln;
-      uint64_t empty = __ballot(bb < batch && pref[bb + 1] == pref[bb]);
-      while (empty) {
-        const int j = __builtin_ctzll(empty);
-        empty &= empty - 1;
-        u32x4* orow = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(c + j) * nq * hq * D);
-        for (int i = ln; i < row16; i += 64) orow[i] = u32x4{0u, 0u, 0u, 0u};
+    if (blockIdx.x == 0) {
+      // the merge kernel reads the same prefix; empty sequences get zero rows
+      // here: each wave tests 64 sequences at a time and clears the rows of the
+      // empty ones together (testing one sequence after another cost ~65 ns
+      // each, half a millisecond at a batch of 8192, on this workgroup alone)
+      for (int b = tid; b <= batch; b += nthreads) ws_pref[b] = pref[b];
+      const int row16 = nq * hq * D / 8;  // 16-byte stores per sequence
+      const int ln = tid & 63;
+      for (int c = (tid >> 6) * 64; c < batch; c += nwaves * 64) {
+        const int bb = c + ln;
+        uint64_t empty = __ballot(bb < batch && pref[bb + 1] == pref[bb]);
+        while (empty) {
+          const int j = __builtin_ctzll(empty);
+          empty &= empty - 1;
+          u32x4* orow = reinterpret_cast<u32x4*>(out + static_cast<int64_t>(c + j) * nq * hq * D);
+          for (int i = ln; i < row16; i += 64) orow[i] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
+    __syncthreads();  // the scan area becomes the tiles
   }
-  __syncthreads();  // the scan area becomes the tiles
 
   const int lane = tid & 63;
   const int wid = uniform(tid >> 6);  // wave-uniform: lets the compiler keep per-wave values in SGPRs
-  const int hi_w = wid % hgs;         // kv head of this wave within the group
-  const int ph = wid / hgs;           // step phase of this wave
+  const int ph = div_small(wid, hgs);  // step phase of this wave
+  const int hi_w = wid - ph * hgs;     // kv head of this wave within the group
   const int g4 = lane >> 4;           // lane group: MFMA k block / C row block
   const int c = lane & 15;            // MFMA row (A) / column (B, C)
   // column c = query token qj, head qh of the group (padding columns c >= ncols
   // take the last token's key range and a zero query)
-  const int qj = c < ncols ? c / group : nq - 1;
-  const int qh = c - (c / group) * group;
+  const int qj = c < ncols ? div_small(c, group) : nq - 1;
+  const int qh = c - div_small(c, group) * group;
   // Vector-ALU variant: lane (vr, vq) = (lane / 16, lane % 16) holds
   // d = 8 vq .. 8 vq + 7 of token rows 4 i + vr of a step.  Its partial QK^T
   // sums over those 8 d are added across the 16 lanes of the row by a
@@ -399,43 +446,88 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   const int vMi = kNC == 8 ? vd4 : (vd3 | vd4 << 1);
   const int qjv = vMh < ncols ? vMh / group : nq - 1;  // query token of the lane's column
 
-  // ws_split[blk]: the (sequence, kv-head group) whose first split point
-  // is this workgroup's start, else -1 -- the list of pieces to merge when
-  // the batch has more sequences than workgroups (merge_kernel<.., true>)
-  int32_t* ws_split = ws_pref + batch + 1;
   const int blk = blockIdx.x;
-  const int64_t total = static_cast<int64_t>(pref[batch]) * ngroups;
-  if (total == 0) {
-    if (tid == 0) ws_split[blk] = -1;
-    return;
-  }
-  const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
-  int64_t beff = (total + per_block_min - 1) / per_block_min;
-  beff = beff < gridDim.x ? beff : gridDim.x;
-  if (blk >= beff) {
-    if (tid == 0) ws_split[blk] = -1;
-    return;
-  }
-  int64_t x = (static_cast<int64_t>(blk) * total) / beff;
-  const int64_t xend = (static_cast<int64_t>(blk + 1) * total) / beff;
-
-  // sequence containing step x: largest b with pref[b] * ngroups <= x
-  int b;
-  {
-    const int y = static_cast<int>(x / ngroups);
-    int lo = 0, hi = batch - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (uniform(pref[mid]) <= y) lo = mid; else hi = mid - 1;
+  int b, nb, hg, s0;
+  int64_t x, xend;
+  int64_t total = 0, beff = 1;  // stream-K: flattened steps and workgroups that take some
+  // fixed split: the raw q rows of the columns and the page ids of the
+  // wave's first two steps (without a window they do not depend on the
+  // length), requested before the length is waited for
+  int fx_L = 0;
+  u32x4 fx_q[S::kQK];
+  int fx_pa0 = 0, fx_pb0 = 0, fx_pa1 = 0, fx_pb1 = 0;
+  if constexpr (kFixed) {
+    const int e = div_small(blk, chunks);  // (sequence, kv-head group)
+    b = div_small(e, ngroups);
+    hg = e - b * ngroups;
+    s0 = (blk - e * chunks) * chunk_steps;
+    fx_L = lens[b];
+    // a padding column (c >= ncols) reads a row inside q (token nq - 1,
+    // head qh < group) and is zeroed where the operand is formed
+    const uint16_t* qrow = q + ((static_cast<int64_t>(b) * nq + qj) * hq + (hg * hgs + hi_w) * group + qh) * D + 8 * g4;
+#pragma unroll
+    for (int kk = 0; kk < S::kQK; ++kk) fx_q[kk] = ld16(qrow + 32 * kk);
+    if (window == 0) {
+      const int32_t* bt_row = bt + static_cast<int64_t>(b) * maxp;
+      auto first_pids = [&](int step, int& pa, int& pb) {
+        const int t0 = step * kStep;
+        if constexpr (!kLanePages) {
+          int ja = t0 >> page_shift, jb = (t0 + 16) >> page_shift;
+          ja = ja < maxp ? ja : maxp - 1;
+          jb = jb < maxp ? jb : maxp - 1;
+          pa = bt_row[ja];
+          pb = bt_row[jb];
+        } else {
+          int j = (t0 >> page_shift) + (lane & ((kStep >> page_shift) - 1));
+          j = j < maxp ? j : maxp - 1;
+          pa = bt_row[j];
+          pb = 0;
+        }
+      };
+      first_pids(s0 + ph, fx_pa0, fx_pb0);
+      first_pids(s0 + ph + phases, fx_pa1, fx_pb1);
     }
-    b = lo;
+    nb = seq_steps(clamp_len(uniform(fx_L), max_ctx), nq, window);
+    if (s0 >= nb) return;  // a chunk past the sequence's end
+    x = 0;
+    xend = nb - s0 < chunk_steps ? nb - s0 : chunk_steps;
+  } else {
+    // ws_split[blk]: the (sequence, kv-head group) whose first split point
+    // is this workgroup's start, else -1 -- the list of pieces to merge when
+    // the batch has more sequences than workgroups (merge_kernel<.., true>)
+    int32_t* ws_split = ws_pref + batch + 1;
+    total = static_cast<int64_t>(pref[batch]) * ngroups;
+    if (total == 0) {
+      if (tid == 0) ws_split[blk] = -1;
+      return;
+    }
+    const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
+    beff = div_floor(total + per_block_min - 1, per_block_min);
+    beff = beff < gridDim.x ? beff : gridDim.x;
+    if (blk >= beff) {
+      if (tid == 0) ws_split[blk] = -1;
+      return;
+    }
+    x = div_floor(static_cast<int64_t>(blk) * total, beff);
+    xend = div_floor(static_cast<int64_t>(blk + 1) * total, beff);
+
+    // sequence containing step x: largest b with pref[b] * ngroups <= x
+    {
+      const int y = static_cast<int>(div_floor(x, ngroups));
+      int lo = 0, hi = batch - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (uniform(pref[mid]) <= y) lo = mid; else hi = mid - 1;
+      }
+      b = lo;
+    }
+    nb = uniform(pref[b + 1]) - uniform(pref[b]);
+    const int rel = static_cast<int>(x - static_cast<int64_t>(uniform(pref[b])) * ngroups);
+    hg = div_small(rel, nb);
+    s0 = rel - hg * nb;
+    // a sequence split across workgroups w0 .. w1 is listed once, by w0 + 1
+    if (tid == 0) ws_split[blk] = (s0 > 0 && owner_of(x - s0, total, beff) == blk - 1) ? b * ngroups + hg : -1;
   }
-  int nb = uniform(pref[b + 1]) - uniform(pref[b]);
-  int rel = static_cast<int>(x - static_cast<int64_t>(uniform(pref[b])) * ngroups);
-  int hg = rel / nb;
-  int s0 = rel - hg * nb;
-  // a sequence split across workgroups w0 .. w1 is listed once, by w0 + 1
-  if (tid == 0) ws_split[blk] = (s0 > 0 && owner_of(x - s0, total, beff) == blk - 1) ? b * ngroups + hg : -1;
 
   unsigned char* tile = smem + wid * S::kTileBytes;
   const int vr = lane / S::kChunks;   // row within one wave load (K and V alike)
@@ -452,7 +544,8 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   while (true) {
     const int64_t remaining = xend - x;
     const int s1 = remaining < nb - s0 ? s0 + static_cast<int>(remaining) : nb;
-    const int L = uniform(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx));
+    const int L = kFixed ? clamp_len(uniform(fx_L), max_ctx)
+                         : uniform(S::kLensInLds ? lens_s[b] : clamp_len(lens[b], max_ctx));
     const int npages = (L + page - 1) >> page_shift;
     const int lo_seq = uniform(seq_start(L, nq, window));
     const int sb = lo_seq / kStep;                  // first step of the sequence
@@ -466,7 +559,11 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
 
     // query operand (B of QK^T): column c, d = 32*kk + 8*g4 + e
     bf16x8 qop[S::kQK];
-    if constexpr (!kValu) {
+    if constexpr (kFixed) {
+#pragma unroll
+      for (int kk = 0; kk < S::kQK; ++kk)
+        qop[kk] = __builtin_bit_cast(bf16x8, c < ncols ? fx_q[kk] : u32x4{0u, 0u, 0u, 0u});
+    } else if constexpr (!kValu) {
       const uint16_t* qrow = q + ((static_cast<int64_t>(b) * nq + qj) * hq + g * group + qh) * D + 8 * g4;
 #pragma unroll
       for (int kk = 0; kk < S::kQK; ++kk) {
@@ -512,7 +609,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     // arrived: one step in flight per wave while the previous one computes
     // streams ~1% faster on MI355X than letting two steps overlap.
     const int sw = s0 + ph;  // this wave's first step; it takes sw, sw + phases, ...
-    const int nsteps = sw < s1 ? (s1 - sw + phases - 1) / phases : 0;
+    const int nsteps = sw < s1 ? div_small(s1 - sw + phases - 1, phases) : 0;
     auto step_of = [&](int k) {  // k-th step of this wave (absolute), clamped to its last one
       k = k < nsteps ? k : nsteps - 1;
       return sb + sw + k * phases;
@@ -836,8 +933,12 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       if (nsteps > 0) {
         u32x4 kA[S::kLoads], vA[S::kLoads];
         int pa0, pb0, pa1, pb1;
-        load_pids(0, pa0, pb0);
-        load_pids(1, pa1, pb1);
+        if (kFixed && window == 0) {
+          pa0 = fx_pa0, pb0 = fx_pb0, pa1 = fx_pa1, pb1 = fx_pb1;
+        } else {
+          load_pids(0, pa0, pb0);
+          load_pids(1, pa1, pb1);
+        }
         issue(0, pa0, pb0, kA, vA, kIssueK);
         issue(0, pa0, pb0, kA, vA, kIssueV);
         // A step's K rows are staged as soon as they arrive and the next
@@ -866,8 +967,12 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     } else if (nsteps > 0) {
       u32x4 kA[S::kLoads], vA[S::kLoads], kB[S::kLoads], vB[S::kLoads];
       int pa0, pb0, pa1, pb1;
-      load_pids(0, pa0, pb0);
-      load_pids(1, pa1, pb1);
+      if (kFixed && window == 0) {
+        pa0 = fx_pa0, pb0 = fx_pb0, pa1 = fx_pa1, pb1 = fx_pb1;
+      } else {
+        load_pids(0, pa0, pb0);
+        load_pids(1, pa1, pb1);
+      }
       issue(0, pa0, pb0, kA, vA);
       int k = 0;
       // The waves of a workgroup meet at a barrier once per step, after
@@ -879,7 +984,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       // barrier, so each wave passes the same number of them.  (The
       // small-page path runs ~3% slower with it: its waves already wait on
       // their page-id shuffles at every issue.)
-      const int nmin = kLanePages ? 0 : (s1 - s0) / phases;
+      const int nmin = kLanePages ? 0 : div_small(s1 - s0, phases);
       // (Small pages read their page ids with vector loads, which the wait
       // for all vector loads would also wait for: they are issued after it.)
       for (; k + 2 < nsteps; k += 2) {
@@ -983,8 +1088,9 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
           *reinterpret_cast<u32x2*>(orow + 16 * dt) = __builtin_bit_cast(u32x2, o);
         }
       } else {
-        // slot (workgroup + sequence group) is unique: workgroup ranges are contiguous
-        const int64_t slot = static_cast<int64_t>(blk) + static_cast<int64_t>(b) * ngroups + hg;
+        // slot (workgroup + sequence group) is unique: workgroup ranges are
+        // contiguous; a fixed-split workgroup has one piece, in slot blk
+        const int64_t slot = kFixed ? static_cast<int64_t>(blk) : static_cast<int64_t>(blk) + static_cast<int64_t>(b) * ngroups + hg;
         const int64_t row = (slot * hgs + hi_w) * ncols + c;
         if constexpr (kFused) {
           const __amdgpu_buffer_rsrc_t ra = ws_rsrc(ws_acc), rm = ws_rsrc(ws_ml);
@@ -1060,17 +1166,17 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   __shared__ f32x4 s_num[kHPB][kPG][kCols];
   __shared__ float s_m[kHPB][kPG], s_l[kHPB][kPG];
 
-  const int ngroups = hkv / hgs;
+  const int ngroups = div_small(hkv, hgs);
   const int ncols = group * nq;   // (query token, head) columns per kv head
   const int heads = hgs * ncols;  // query rows of one kv-head group
   const int chunks = (heads + kHPB - 1) / kHPB;
-  int e = blockIdx.x / chunks;
+  int e = div_small(static_cast<int>(blockIdx.x), chunks);
   const int chunk = blockIdx.x - e * chunks;
   if constexpr (kBySplit) {
     e = ws_pref[batch + 1 + e];  // ws_split
     if (e < 0) return;
   }
-  const int b = e / ngroups;
+  const int b = div_small(e, ngroups);
   const int hg = e - b * ngroups;
   // The three prefix entries are requested together and the one early
   // return needs all of them (with a return on nb == 0 first, the total
@@ -1080,7 +1186,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   int64_t total = static_cast<int64_t>(pbt) * ngroups;
   total = total > 0 ? total : 1;  // an all-empty batch returns below (nb == 0)
   const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
-  int64_t beff = (total + per_block_min - 1) / per_block_min;
+  int64_t beff = div_floor(total + per_block_min - 1, per_block_min);
   beff = beff < grid_blocks ? beff : grid_blocks;
   const int64_t x0 = static_cast<int64_t>(pb0) * ngroups + static_cast<int64_t>(hg) * nb;
   const int64_t w0 = owner_of(x0, total, beff);
@@ -1149,7 +1255,119 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
       __builtin_bit_cast(u32x2, o);
 }
 
-template <int D, bool kLanePages, int kNC = 0, bool kFused = false>
+// Merge of the fixed split: the pieces of (sequence b, kv-head group hg) are
+// the slots e * chunks + w, w < n, with e = b * groups + hg and n the number
+// of chunk_steps-step chunks the sequence's steps fill.  n follows from the
+// length alone, so the partials of every chunk are requested together with
+// the length and those of chunks past n (stale data of other calls) are
+// selected away.  n = 1: the attention kernel wrote the sequence itself;
+// n = 0: the row is zero.  Same layout and slot order as merge_kernel.
+template <int D, int kPG>
+__global__ __launch_bounds__(kMergeThreads) void merge_fixed_kernel(
+    uint16_t* __restrict__ out, const float* __restrict__ ws_acc, const float* __restrict__ ws_ml,
+    const int32_t* __restrict__ lens, int hq, int hkv, int group, int hgs, int nq, int window, int max_ctx,
+    int chunks, int chunk_steps) {
+  constexpr int kCols = D / 4;
+  constexpr int kHPB = kMergeThreads / (kPG * kCols);  // query heads per workgroup
+  static_assert(kHPB >= 1 && kHPB * kPG * kCols == kMergeThreads, "merge layout");
+  __shared__ f32x4 s_num[kHPB][kPG][kCols];
+  __shared__ float s_m[kHPB][kPG], s_l[kHPB][kPG];
+
+  // one round trip for the arguments: this statement needs all of them in
+  // SGPRs and every later use of an integer argument depends on it
+  // (pointers are inputs only, so their loads stay global loads)
+  asm volatile(""
+               : "+s"(hq), "+s"(hkv), "+s"(group), "+s"(hgs), "+s"(nq), "+s"(window), "+s"(max_ctx), "+s"(chunks),
+                 "+s"(chunk_steps)
+               : "s"(out), "s"(ws_acc), "s"(ws_ml), "s"(lens));
+  const int ngroups = div_small(hkv, hgs);
+  const int ncols = group * nq;
+  const int heads = hgs * ncols;
+  const int hchunks = (heads + kHPB - 1) / kHPB;
+  const int e = div_small(static_cast<int>(blockIdx.x), hchunks);
+  const int chunk = blockIdx.x - e * hchunks;
+  const int b = div_small(e, ngroups);
+  const int hg = e - b * ngroups;
+  const int len = lens[b];
+
+  const int tid = threadIdx.x;
+  const int hs = tid / (kPG * kCols);
+  const int pg = (tid / kCols) % kPG;
+  const int col = tid % kCols;
+  const int hh = chunk * kHPB + hs;  // query head within the kv-head group
+  const bool active = hh < heads;
+  const int hhc = active ? hh : 0;    // (a thread past the heads reads a valid row and writes nothing)
+  const int hi_w = div_small(hhc, ncols), c = hhc - hi_w * ncols;
+  auto row_of = [&](int w) { return ((static_cast<int64_t>(e) * chunks + w) * hgs + hi_w) * ncols + c; };
+  // the first kAhead pieces of this thread's piece group, requested before
+  // the length is waited for (clamped into the sequence's own slots)
+  constexpr int kAhead = 4;
+  f32x2 mla[kAhead];
+  f32x4 aca[kAhead];
+#pragma unroll
+  for (int i = 0; i < kAhead; ++i) {
+    const int w = pg + i * kPG < chunks ? pg + i * kPG : chunks - 1;
+    mla[i] = *reinterpret_cast<const f32x2*>(ws_ml + row_of(w) * 2);
+    aca[i] = *reinterpret_cast<const f32x4*>(ws_acc + row_of(w) * D + 4 * col);
+  }
+  __builtin_amdgcn_sched_barrier(0);  // every load above issues before the length is used
+  const int nb = seq_steps(clamp_len(len, max_ctx), nq, window);
+  const int n = div_small(nb + chunk_steps - 1, chunk_steps);  // pieces: slots e * chunks + [0, n)
+  float mm = -__builtin_inff(), ll = 0.f;
+  f32x4 nn = {0.f, 0.f, 0.f, 0.f};
+  auto take = [&](float mj, float lj, f32x4 aj) {
+    const float m2 = fmaxf(mm, mj);
+    const float mref = m2 == -__builtin_inff() ? 0.f : m2;  // no piece yet, or one that saw no key
+    const float fo = __builtin_amdgcn_exp2f(mm - mref);
+    const float fn = __builtin_amdgcn_exp2f(mj - mref);
+    nn = nn * fo + aj * fn;
+    ll = ll * fo + lj * fn;
+    mm = m2;
+  };
+#pragma unroll
+  for (int i = 0; i < kAhead; ++i) {
+    const bool use = pg + i * kPG < n;  // a piece of this call (else stale data, selected away)
+    take(use ? mla[i][0] : -__builtin_inff(), use ? mla[i][1] : 0.f, use ? aca[i] : f32x4{0.f, 0.f, 0.f, 0.f});
+  }
+  for (int w = pg + kAhead * kPG; w < n; w += kPG) {
+    const f32x2 mlv = *reinterpret_cast<const f32x2*>(ws_ml + row_of(w) * 2);
+    take(mlv[0], mlv[1], *reinterpret_cast<const f32x4*>(ws_acc + row_of(w) * D + 4 * col));
+  }
+  if (n == 1) return;  // whole: written by the attention kernel (uniform per workgroup)
+  if (kPG > 1) {
+    s_num[hs][pg][col] = nn;
+    if (col == 0) {
+      s_m[hs][pg] = mm;
+      s_l[hs][pg] = ll;
+    }
+    __syncthreads();
+    if (pg != 0) return;
+    float big_m = -__builtin_inff();
+#pragma unroll
+    for (int p = 0; p < kPG; ++p) big_m = fmaxf(big_m, s_m[hs][p]);
+    float den = 0.f;
+    f32x4 num = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < kPG; ++p) {
+      const float f = s_m[hs][p] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(s_m[hs][p] - big_m);
+      den += f * s_l[hs][p];
+      num += f * s_num[hs][p][col];
+    }
+    nn = num;
+    ll = den;
+  }
+  if (!active) return;
+  const float inv = ll > 0.f ? 1.0f / ll : 0.f;  // an empty sequence, or a query that sees no key: zero row
+  bf16x4 o;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = static_cast<__bf16>(nn[i] * inv);
+  const int j = div_small(c, group);
+  const int h = (hg * hgs + hi_w) * group + (c - j * group);
+  *reinterpret_cast<u32x2*>(out + ((static_cast<int64_t>(b) * nq + j) * hq + h) * D + 4 * col) =
+      __builtin_bit_cast(u32x2, o);
+}
+
+template <int D, bool kLanePages, int kNC = 0, bool kFused = false, bool kFixed = false>
 static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   const size_t lds = attn_lds_bytes(D, a.batch, a.waves, kNC > 0);
   // the dynamic-LDS limit is raised once per device (bit = device ordinal)
@@ -1159,15 +1377,15 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   if (e != hipSuccess) return e;
   const uint64_t bit = dev < 64 ? uint64_t{1} << dev : 0;
   if (!bit || !(attr_set.load() & bit)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages, kNC, kFused>),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, kLanePages, kNC, kFused, kFixed>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLdsBytes);
     if (e != hipSuccess) return e;
     attr_set.fetch_or(bit);
   }
-  hipLaunchKernelGGL((attn_kernel<D, kLanePages, kNC, kFused>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q, a.k,
-                     a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.ws_cnt, a.batch, a.hq, a.hkv,
+  hipLaunchKernelGGL((attn_kernel<D, kLanePages, kNC, kFused, kFixed>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q,
+                     a.k, a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.ws_cnt, a.batch, a.hq, a.hkv,
                      a.group, a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e, a.nq,
-                     a.window);
+                     a.window, a.chunks, a.chunk_steps);
   return hipGetLastError();
 }
 
@@ -1176,8 +1394,17 @@ hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
   if (a.waves > max_waves(a.head_dim)) return hipErrorInvalidValue;
   if (a.valu_cols) {
     // vector-ALU variant: D = 128, pages of 16 tokens or more, at most 8 columns, merge kernel
-    if (a.head_dim != 128 || lane_pages || a.group * a.nq > a.valu_cols || a.fused) return hipErrorInvalidValue;
+    if (a.head_dim != 128 || lane_pages || a.group * a.nq > a.valu_cols || a.fused || a.chunks > 0)
+      return hipErrorInvalidValue;
     return a.valu_cols == 4 ? launch_attn<128, false, 4>(a, st) : launch_attn<128, false, 8>(a, st);
+  }
+  if (a.chunks > 0) {
+    if (a.fused) return hipErrorInvalidValue;
+    if (a.head_dim == 128)
+      return lane_pages ? launch_attn<128, true, 0, false, true>(a, st) : launch_attn<128, false, 0, false, true>(a, st);
+    if (a.head_dim == 256)
+      return lane_pages ? launch_attn<256, true, 0, false, true>(a, st) : launch_attn<256, false, 0, false, true>(a, st);
+    return lane_pages ? launch_attn<64, true, 0, false, true>(a, st) : launch_attn<64, false, 0, false, true>(a, st);
   }
   if (a.fused) {
     if (a.head_dim == 128)
@@ -1203,7 +1430,25 @@ static hipError_t launch_merge(const LaunchArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int D, int kPG>
+static hipError_t launch_merge_fixed(const LaunchArgs& a, hipStream_t st) {
+  constexpr int kHPB = kMergeThreads / (kPG * (D / 4));
+  const int heads = a.hgs * a.group * a.nq;
+  const int hchunks = (heads + kHPB - 1) / kHPB;
+  const dim3 grid(a.batch * (a.hkv / a.hgs) * hchunks);
+  hipLaunchKernelGGL((merge_fixed_kernel<D, kPG>), grid, dim3(kMergeThreads), 0, st, a.out, a.ws_acc, a.ws_ml, a.lens,
+                     a.hq, a.hkv, a.group, a.hgs, a.nq, a.window, a.maxp << a.page_shift, a.chunks, a.chunk_steps);
+  return hipGetLastError();
+}
+
 hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
+  if (a.chunks > 0) {
+    // several pieces per sequence: piece groups folded through LDS
+    const bool many = a.chunks >= 8;
+    if (a.head_dim == 128) return many ? launch_merge_fixed<128, 8>(a, st) : launch_merge_fixed<128, 1>(a, st);
+    if (a.head_dim == 256) return many ? launch_merge_fixed<256, 4>(a, st) : launch_merge_fixed<256, 1>(a, st);
+    return many ? launch_merge_fixed<64, 8>(a, st) : launch_merge_fixed<64, 1>(a, st);
+  }
   // expected pieces per split sequence: workgroups per kv-head-group sequence
   const int64_t seqs = static_cast<int64_t>(a.batch) * (a.hkv / a.hgs);
   const bool many = a.grid >= 8 * seqs;

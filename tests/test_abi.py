@@ -110,6 +110,28 @@ def test_small_calls_take_one_step_per_wave(lib):
         B.set_option(B.OPT_MIN_STEPS, 0)
 
 
+def test_fixed_split_option(lib):
+    """Latency-bound calls take the fixed split by default: every
+    (sequence, kv-head group) is cut into the same number of whole-step
+    chunks (2 x 3000 tokens at D = 256: 2 sequences x 4 groups x 24 chunks
+    of 4 steps = 192 workgroups, against 188 for the stream-K split over
+    the same step count); large calls, and calls with more sequences than
+    half the device's workgroups, keep the stream-K split."""
+    assert B.get_option(B.OPT_FIXED_SPLIT) == 1
+    assert B.plan(2, 16, 4, 256, 32, 94, num_cus=256)[0] == 192
+    assert B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)[0] == 256  # long70b: stream-K
+    try:
+        B.set_option(B.OPT_FIXED_SPLIT, 0)
+        assert B.get_option(B.OPT_FIXED_SPLIT) == 0
+        assert B.plan(2, 16, 4, 256, 32, 94, num_cus=256)[0] == 188
+        with pytest.raises(B.PdaError):
+            B.set_option(B.OPT_FIXED_SPLIT, 2)
+        with pytest.raises(B.PdaError):
+            B.set_option(B.OPT_FIXED_SPLIT, -1)
+    finally:
+        B.set_option(B.OPT_FIXED_SPLIT, 1)
+
+
 def test_planner_grid_scales_with_options(lib):
     try:
         B.set_option(B.OPT_BLOCKS_PER_CU, 2)

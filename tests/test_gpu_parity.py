@@ -254,33 +254,38 @@ def test_two_streams(lib):
 
 # ------------------------------------------------------------- named workloads
 # Calls the planner treats as small (K and V within 128 MB): one 32-token
-# step per wave when the two-step plan leaves CUs idle, and fewer kv heads
-# per workgroup when a (sequence, kv-head group) would be cut into more than
-# 32 pieces.  (lengths, Hq, Hkv, D, P, grid with the planner's choice, grid
-# with two steps per wave fixed by the caller)
+# step per wave when the two-step plan leaves CUs idle, fewer kv heads per
+# workgroup when a (sequence, kv-head group) would be cut into more than 32
+# pieces, and the fixed split (every pair cut into the same chunks, the
+# merge finding the pieces from the lengths).  (lengths, Hq, Hkv, D, P, then
+# the grid of the fixed split with the planner's step count and with two
+# steps per wave fixed by the caller, then the same two for the stream-K
+# split over the actual lengths)
 SMALL_CALLS = [
-    ([4096], 32, 8, 128, 16, 128, 64),       # single request: 2 kv heads per workgroup
-    ([8192], 64, 8, 128, 16, 256, 128),      # one kv head per workgroup, 8 columns
-    ([16384], 32, 8, 128, 16, 256, 256),     # one kv head per workgroup
-    ([1024] * 4, 32, 8, 128, 16, 128, 64),   # one step per wave, 8 kv heads
-    ([3000, 17], 16, 4, 256, 32, 188, 94),   # D = 256: one kv head of 4-wave workgroups
-    ([700, 5, 1900], 40, 8, 128, 1, 180, 90),  # one-token pages
+    ([4096], 32, 8, 128, 16, 128, 64, 128, 64),       # single request: 2 kv heads per workgroup
+    ([8192], 64, 8, 128, 16, 256, 128, 256, 128),     # one kv head per workgroup, 8 columns
+    ([16384], 32, 8, 128, 16, 256, 256, 256, 256),    # one kv head per workgroup
+    ([1024] * 4, 32, 8, 128, 16, 128, 64, 128, 64),   # one step per wave, 8 kv heads
+    ([3000, 17], 16, 4, 256, 32, 192, 96, 188, 94),   # D = 256: one kv head of 4-wave workgroups
+    ([700, 5, 1900], 40, 8, 128, 1, 180, 90, 180, 90),  # one-token pages
 ]
 
 
-@pytest.mark.parametrize("lens,hq,hkv,d,p,grid,grid2", SMALL_CALLS,
+@pytest.mark.parametrize("lens,hq,hkv,d,p,gf,gf2,gs,gs2", SMALL_CALLS,
                          ids=[f"{len(c[0])}x{max(c[0])}-{c[1]}:{c[2]}-D{c[3]}-P{c[4]}" for c in SMALL_CALLS])
-def test_small_call_plans_match_oracle(lib, lens, hq, hkv, d, p, grid, grid2):
+def test_small_call_plans_match_oracle(lib, lens, hq, hkv, d, p, gf, gf2, gs, gs2):
     w = W.build(lens, hq, hkv, d, p, seed=sum(lens) + hq, pool="holes:0.1")
     maxp = w.block_table.shape[1]
-    assert lib.plan(len(lens), hq, hkv, d, p, maxp)[0] == grid
-    log(f"case {len(lens)} x {max(lens)} {hq}:{hkv} D={d} P={p} grid {grid}")
-    check(run(lib, w), ref(w), "small call")
+    r = ref(w)
     try:
-        lib.set_option(lib.OPT_MIN_STEPS, 2)
-        assert lib.plan(len(lens), hq, hkv, d, p, maxp)[0] == grid2
-        check(run(lib, w), ref(w), "small call, two steps per wave")
+        for fixed, steps, grid in ((1, 0, gf), (1, 2, gf2), (0, 0, gs), (0, 2, gs2)):
+            lib.set_option(lib.OPT_FIXED_SPLIT, fixed)
+            lib.set_option(lib.OPT_MIN_STEPS, steps)
+            assert lib.plan(len(lens), hq, hkv, d, p, maxp)[0] == grid
+            log(f"case {len(lens)} x {max(lens)} {hq}:{hkv} D={d} P={p} fixed split {fixed} steps {steps} grid {grid}")
+            check(run(lib, w), r, f"small call, fixed split {fixed}, steps {steps}")
     finally:
+        lib.set_option(lib.OPT_FIXED_SPLIT, 1)
         lib.set_option(lib.OPT_MIN_STEPS, 0)
 
 
