@@ -305,8 +305,9 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   //    rows stream faster (long70b: 319.8 us per call with 8, 321.2 with 4,
   //    329.6 with 2, 351.8 with 1).
   //  - the fixed split (plan_fixed) unless PDA_OPT_FIXED_SPLIT is 0: the
-  //    first K/V loads leave ~3 us earlier and the merge needs no prefix
-  //    (1 x 4096 tokens, 32:8 heads: ...).
+  //    first K/V loads leave ~2 us earlier and the merge needs no prefix
+  //    (1 x 4096 tokens, 32:8 heads, cold K/V: attention kernel 14.8 ->
+  //    11.4 us by events, 16.7 -> 11.9 us per call replayed from a graph).
   const int64_t kv_bytes = static_cast<int64_t>(batch) * maxp * p * hkv * d * 4;
   const bool small = kv_bytes <= kSmallCallBytes;
   if (small) {

@@ -182,35 +182,27 @@ __device__ __forceinline__ f32x2 load_coherent2(__amdgpu_buffer_rsrc_t r, int64_
                                                                          kCachePolicyCoherent));
 }
 
-// Integer quotients on the way to the first loads.  The compiler expands a
-// 64-bit integer division into ~120 dependent instructions (a 32-bit one
-// into ~25); the chain of them between the steps prefix and the first
-// page-id load took ~2.5 us of every call on MI355X.  Both helpers divide
-// in fp64 instead:
-//  * div_small (0 <= a < 2^31, 0 < b < 2^31): both operands convert
-//    exactly and the quotient a/b, correctly rounded, cannot reach the next
-//    integer (it is at least 1/b below it, more than the rounding error of a
-//    quotient below 2^31), so truncation gives floor(a / b);
-//  * div_floor (0 <= a < 2^62, 0 < b, quotient < 2^50): three roundings
-//    leave the fp64 quotient within 3/8 of a/b, so its truncation is within
-//    one of floor(a / b), which one integer remainder test corrects.
+// Quotients on the way to the first loads of the fixed split and its
+// merge.  The compiler expands a 32-bit integer division into ~25 dependent
+// instructions; these divide in fp64 instead: both operands (0 <= a < 2^31,
+// 0 < b < 2^31) convert exactly and the quotient a/b, correctly rounded,
+// cannot reach the next integer (it is at least 1/b below it, more than the
+// rounding error of a quotient below 2^31), so truncation gives
+// floor(a / b).  div_small_u is the same for wave-uniform operands: the
+// quotient is computed in vector registers (the scalar unit has no fp64)
+// and readfirstlane returns it to scalar registers, so that nothing derived
+// from it takes vector registers.  (The stream-K prologue keeps the
+// compiler's integer division: there the fp64 form measured no faster and
+// cost the main loop vector registers.)
 __device__ __forceinline__ int div_small(int a, int b) {
   return static_cast<int>(static_cast<double>(a) / static_cast<double>(b));
 }
-__device__ __forceinline__ int64_t div_floor(int64_t a, int64_t b) {
-  int64_t q = static_cast<int64_t>(static_cast<double>(a) / static_cast<double>(b));
-  const int64_t r = a - q * b;
-  if (r < 0)
-    --q;
-  else if (r >= b)
-    ++q;
-  return q;
-}
+__device__ __forceinline__ int div_small_u(int a, int b) { return uniform(div_small(a, b)); }
 
 // Workgroup that owns flattened step x of `total`, when `parts` workgroups
 // split [0, total) into ranges [w*total/parts, (w+1)*total/parts).
 __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t parts) {
-  return div_floor((x + 1) * parts - 1, total);
+  return ((x + 1) * parts - 1) / total;
 }
 
 // Value of a partner lane in the same 16-lane row (DPP), for the vector-ALU
@@ -350,8 +342,8 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   extern __shared__ __align__(16) unsigned char smem[];
   const int nthreads = blockDim.x;
   const int nwaves = nthreads >> 6;
-  const int phases = div_small(nwaves, hgs);  // waves per kv head, interleaving steps
-  const int ngroups = div_small(hkv, hgs);    // kv-head groups per sequence
+  const int phases = nwaves / hgs;  // waves per kv head, interleaving steps
+  const int ngroups = hkv / hgs;    // kv-head groups per sequence
   const int ncols = group * nq;     // MFMA columns in use: (query token, head of the group)
   int32_t* pref = reinterpret_cast<int32_t*>(smem + pref_offset<D, kValu>(nwaves));
   int32_t* lens_s = pref + batch + 1;  // clamped lengths (kLensInLds)
@@ -423,14 +415,14 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
 
   const int lane = tid & 63;
   const int wid = uniform(tid >> 6);  // wave-uniform: lets the compiler keep per-wave values in SGPRs
-  const int ph = div_small(wid, hgs);  // step phase of this wave
-  const int hi_w = wid - ph * hgs;     // kv head of this wave within the group
+  const int hi_w = wid % hgs;         // kv head of this wave within the group
+  const int ph = wid / hgs;           // step phase of this wave
   const int g4 = lane >> 4;           // lane group: MFMA k block / C row block
   const int c = lane & 15;            // MFMA row (A) / column (B, C)
   // column c = query token qj, head qh of the group (padding columns c >= ncols
   // take the last token's key range and a zero query)
-  const int qj = c < ncols ? div_small(c, group) : nq - 1;
-  const int qh = c - div_small(c, group) * group;
+  const int qj = c < ncols ? c / group : nq - 1;
+  const int qh = c - (c / group) * group;
   // Vector-ALU variant: lane (vr, vq) = (lane / 16, lane % 16) holds
   // d = 8 vq .. 8 vq + 7 of token rows 4 i + vr of a step.  Its partial QK^T
   // sums over those 8 d are added across the 16 lanes of the row by a
@@ -447,28 +439,27 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   const int qjv = vMh < ncols ? vMh / group : nq - 1;  // query token of the lane's column
 
   const int blk = blockIdx.x;
-  int b, nb, hg, s0;
-  int64_t x, xend;
-  int64_t total = 0, beff = 1;  // stream-K: flattened steps and workgroups that take some
-  // fixed split: the raw q rows of the columns and the page ids of the
-  // wave's first two steps (without a window they do not depend on the
-  // length), requested before the length is waited for
-  int fx_L = 0;
+  // fixed split: the piece from the workgroup index; the raw q rows of the
+  // columns and the page ids of the wave's first two steps (without a
+  // window they do not depend on the length) are requested before the
+  // length is waited for
+  int fx_b = 0, fx_hg = 0, fx_s0 = 0, fx_L = 0, fx_nb = 0;
   u32x4 fx_q[S::kQK];
   int fx_pa0 = 0, fx_pb0 = 0, fx_pa1 = 0, fx_pb1 = 0;
   if constexpr (kFixed) {
-    const int e = div_small(blk, chunks);  // (sequence, kv-head group)
-    b = div_small(e, ngroups);
-    hg = e - b * ngroups;
-    s0 = (blk - e * chunks) * chunk_steps;
-    fx_L = lens[b];
+    const int e = div_small_u(blk, chunks);  // (sequence, kv-head group)
+    fx_b = div_small_u(e, ngroups);
+    fx_hg = e - fx_b * ngroups;
+    fx_s0 = (blk - e * chunks) * chunk_steps;
+    fx_L = lens[fx_b];
     // a padding column (c >= ncols) reads a row inside q (token nq - 1,
     // head qh < group) and is zeroed where the operand is formed
-    const uint16_t* qrow = q + ((static_cast<int64_t>(b) * nq + qj) * hq + (hg * hgs + hi_w) * group + qh) * D + 8 * g4;
+    const uint16_t* qrow =
+        q + ((static_cast<int64_t>(fx_b) * nq + qj) * hq + (fx_hg * hgs + hi_w) * group + qh) * D + 8 * g4;
 #pragma unroll
     for (int kk = 0; kk < S::kQK; ++kk) fx_q[kk] = ld16(qrow + 32 * kk);
     if (window == 0) {
-      const int32_t* bt_row = bt + static_cast<int64_t>(b) * maxp;
+      const int32_t* bt_row = bt + static_cast<int64_t>(fx_b) * maxp;
       auto first_pids = [&](int step, int& pa, int& pb) {
         const int t0 = step * kStep;
         if constexpr (!kLanePages) {
@@ -484,50 +475,52 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
           pb = 0;
         }
       };
-      first_pids(s0 + ph, fx_pa0, fx_pb0);
-      first_pids(s0 + ph + phases, fx_pa1, fx_pb1);
+      first_pids(fx_s0 + ph, fx_pa0, fx_pb0);
+      first_pids(fx_s0 + ph + phases, fx_pa1, fx_pb1);
     }
-    nb = seq_steps(clamp_len(uniform(fx_L), max_ctx), nq, window);
-    if (s0 >= nb) return;  // a chunk past the sequence's end
-    x = 0;
-    xend = nb - s0 < chunk_steps ? nb - s0 : chunk_steps;
-  } else {
-    // ws_split[blk]: the (sequence, kv-head group) whose first split point
-    // is this workgroup's start, else -1 -- the list of pieces to merge when
-    // the batch has more sequences than workgroups (merge_kernel<.., true>)
-    int32_t* ws_split = ws_pref + batch + 1;
-    total = static_cast<int64_t>(pref[batch]) * ngroups;
-    if (total == 0) {
-      if (tid == 0) ws_split[blk] = -1;
-      return;
-    }
-    const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
-    beff = div_floor(total + per_block_min - 1, per_block_min);
-    beff = beff < gridDim.x ? beff : gridDim.x;
-    if (blk >= beff) {
-      if (tid == 0) ws_split[blk] = -1;
-      return;
-    }
-    x = div_floor(static_cast<int64_t>(blk) * total, beff);
-    xend = div_floor(static_cast<int64_t>(blk + 1) * total, beff);
-
-    // sequence containing step x: largest b with pref[b] * ngroups <= x
-    {
-      const int y = static_cast<int>(div_floor(x, ngroups));
-      int lo = 0, hi = batch - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (uniform(pref[mid]) <= y) lo = mid; else hi = mid - 1;
-      }
-      b = lo;
-    }
-    nb = uniform(pref[b + 1]) - uniform(pref[b]);
-    const int rel = static_cast<int>(x - static_cast<int64_t>(uniform(pref[b])) * ngroups);
-    hg = div_small(rel, nb);
-    s0 = rel - hg * nb;
-    // a sequence split across workgroups w0 .. w1 is listed once, by w0 + 1
-    if (tid == 0) ws_split[blk] = (s0 > 0 && owner_of(x - s0, total, beff) == blk - 1) ? b * ngroups + hg : -1;
+    fx_nb = seq_steps(clamp_len(uniform(fx_L), max_ctx), nq, window);
+    if (fx_s0 >= fx_nb) return;  // a chunk past the sequence's end
   }
+
+  // ws_split[blk]: the (sequence, kv-head group) whose first split point
+  // is this workgroup's start, else -1 -- the list of pieces to merge when
+  // the batch has more sequences than workgroups (merge_kernel<.., true>)
+  int32_t* ws_split = ws_pref + batch + 1;
+  const int64_t total = kFixed ? 1 : static_cast<int64_t>(pref[batch]) * ngroups;
+  if (!kFixed && total == 0) {
+    if (tid == 0) ws_split[blk] = -1;
+    return;
+  }
+  const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
+  int64_t beff = kFixed ? 1 : (total + per_block_min - 1) / per_block_min;
+  beff = beff < gridDim.x ? beff : gridDim.x;
+  if (!kFixed && blk >= beff) {
+    if (tid == 0) ws_split[blk] = -1;
+    return;
+  }
+  // a fixed-split workgroup takes one piece: steps [0, xend) from x = 0
+  int64_t x = kFixed ? 0 : (static_cast<int64_t>(blk) * total) / beff;
+  const int64_t xend = kFixed ? (fx_nb - fx_s0 < chunk_steps ? fx_nb - fx_s0 : chunk_steps)
+                              : (static_cast<int64_t>(blk + 1) * total) / beff;
+
+  // sequence containing step x: largest b with pref[b] * ngroups <= x
+  int b = fx_b;
+  if constexpr (!kFixed) {
+    const int y = static_cast<int>(x / ngroups);
+    int lo = 0, hi = batch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (uniform(pref[mid]) <= y) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+  }
+  int nb = kFixed ? fx_nb : uniform(pref[b + 1]) - uniform(pref[b]);
+  int rel = kFixed ? 0 : static_cast<int>(x - static_cast<int64_t>(uniform(pref[b])) * ngroups);
+  int hg = kFixed ? fx_hg : rel / nb;
+  int s0 = kFixed ? fx_s0 : rel - hg * nb;
+  // a sequence split across workgroups w0 .. w1 is listed once, by w0 + 1
+  if (!kFixed && tid == 0)
+    ws_split[blk] = (s0 > 0 && owner_of(x - s0, total, beff) == blk - 1) ? b * ngroups + hg : -1;
 
   unsigned char* tile = smem + wid * S::kTileBytes;
   const int vr = lane / S::kChunks;   // row within one wave load (K and V alike)
@@ -609,7 +602,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     // arrived: one step in flight per wave while the previous one computes
     // streams ~1% faster on MI355X than letting two steps overlap.
     const int sw = s0 + ph;  // this wave's first step; it takes sw, sw + phases, ...
-    const int nsteps = sw < s1 ? div_small(s1 - sw + phases - 1, phases) : 0;
+    const int nsteps = sw < s1 ? (s1 - sw + phases - 1) / phases : 0;
     auto step_of = [&](int k) {  // k-th step of this wave (absolute), clamped to its last one
       k = k < nsteps ? k : nsteps - 1;
       return sb + sw + k * phases;
@@ -984,7 +977,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       // barrier, so each wave passes the same number of them.  (The
       // small-page path runs ~3% slower with it: its waves already wait on
       // their page-id shuffles at every issue.)
-      const int nmin = kLanePages ? 0 : div_small(s1 - s0, phases);
+      const int nmin = kLanePages ? 0 : (s1 - s0) / phases;
       // (Small pages read their page ids with vector loads, which the wait
       // for all vector loads would also wait for: they are issued after it.)
       for (; k + 2 < nsteps; k += 2) {
@@ -1166,17 +1159,17 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   __shared__ f32x4 s_num[kHPB][kPG][kCols];
   __shared__ float s_m[kHPB][kPG], s_l[kHPB][kPG];
 
-  const int ngroups = div_small(hkv, hgs);
+  const int ngroups = hkv / hgs;
   const int ncols = group * nq;   // (query token, head) columns per kv head
   const int heads = hgs * ncols;  // query rows of one kv-head group
   const int chunks = (heads + kHPB - 1) / kHPB;
-  int e = div_small(static_cast<int>(blockIdx.x), chunks);
+  int e = blockIdx.x / chunks;
   const int chunk = blockIdx.x - e * chunks;
   if constexpr (kBySplit) {
     e = ws_pref[batch + 1 + e];  // ws_split
     if (e < 0) return;
   }
-  const int b = div_small(e, ngroups);
+  const int b = e / ngroups;
   const int hg = e - b * ngroups;
   // The three prefix entries are requested together and the one early
   // return needs all of them (with a return on nb == 0 first, the total
@@ -1186,7 +1179,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
   int64_t total = static_cast<int64_t>(pbt) * ngroups;
   total = total > 0 ? total : 1;  // an all-empty batch returns below (nb == 0)
   const int64_t per_block_min = static_cast<int64_t>(min_steps) * phases;
-  int64_t beff = div_floor(total + per_block_min - 1, per_block_min);
+  int64_t beff = (total + per_block_min - 1) / per_block_min;
   beff = beff < grid_blocks ? beff : grid_blocks;
   const int64_t x0 = static_cast<int64_t>(pb0) * ngroups + static_cast<int64_t>(hg) * nb;
   const int64_t w0 = owner_of(x0, total, beff);
@@ -1280,13 +1273,13 @@ __global__ __launch_bounds__(kMergeThreads) void merge_fixed_kernel(
                : "+s"(hq), "+s"(hkv), "+s"(group), "+s"(hgs), "+s"(nq), "+s"(window), "+s"(max_ctx), "+s"(chunks),
                  "+s"(chunk_steps)
                : "s"(out), "s"(ws_acc), "s"(ws_ml), "s"(lens));
-  const int ngroups = div_small(hkv, hgs);
+  const int ngroups = div_small_u(hkv, hgs);
   const int ncols = group * nq;
   const int heads = hgs * ncols;
   const int hchunks = (heads + kHPB - 1) / kHPB;
-  const int e = div_small(static_cast<int>(blockIdx.x), hchunks);
+  const int e = div_small_u(static_cast<int>(blockIdx.x), hchunks);
   const int chunk = blockIdx.x - e * hchunks;
-  const int b = div_small(e, ngroups);
+  const int b = div_small_u(e, ngroups);
   const int hg = e - b * ngroups;
   const int len = lens[b];
 
@@ -1312,7 +1305,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_fixed_kernel(
   }
   __builtin_amdgcn_sched_barrier(0);  // every load above issues before the length is used
   const int nb = seq_steps(clamp_len(len, max_ctx), nq, window);
-  const int n = div_small(nb + chunk_steps - 1, chunk_steps);  // pieces: slots e * chunks + [0, n)
+  const int n = div_small_u(nb + chunk_steps - 1, chunk_steps);  // pieces: slots e * chunks + [0, n)
   float mm = -__builtin_inff(), ll = 0.f;
   f32x4 nn = {0.f, 0.f, 0.f, 0.f};
   auto take = [&](float mj, float lj, f32x4 aj) {

@@ -25,9 +25,11 @@ def lib(gpu_lib):
 def default_options(gpu_lib):
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
     gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
+    gpu_lib.set_option(gpu_lib.OPT_FIXED_SPLIT, 1)
     yield
     gpu_lib.set_option(gpu_lib.OPT_BLOCKS_PER_CU, 1)
     gpu_lib.set_option(gpu_lib.OPT_MIN_STEPS, 0)
+    gpu_lib.set_option(gpu_lib.OPT_FIXED_SPLIT, 1)
 
 
 def ref(w):
@@ -108,12 +110,15 @@ def test_golden_closed_forms(lib, name, w, expected, d):
 
 @pytest.mark.parametrize("min_steps", [1, 2, 7, 1 << 20])
 @pytest.mark.parametrize("blocks", [1, 2, 4])
-def test_split_count_sweep(lib, min_steps, blocks):
+@pytest.mark.parametrize("fixed", [1, 0])
+def test_split_count_sweep(lib, min_steps, blocks, fixed):
+    # both splits of a small call (fixed chunks, stream-K over the lengths)
     w = W.build([3000, 17, 700, 1], 32, 8, 128, 16, seed=3, pool="holes:0.1")
     lib.set_option(lib.OPT_MIN_STEPS, min_steps)
     lib.set_option(lib.OPT_BLOCKS_PER_CU, blocks)
-    log(f"case min_steps={min_steps} blocks={blocks}")
-    check(run(lib, w), ref(w), f"sweep {min_steps}/{blocks}")
+    lib.set_option(lib.OPT_FIXED_SPLIT, fixed)
+    log(f"case min_steps={min_steps} blocks={blocks} fixed={fixed}")
+    check(run(lib, w), ref(w), f"sweep {min_steps}/{blocks}/{fixed}")
 
 
 def test_length_one_is_v_exactly(lib):
@@ -420,9 +425,10 @@ def _plant_dominant(w, b, g, t, score):
     return key, u
 
 
+@pytest.mark.parametrize("fixed", [1, 0])
 @pytest.mark.parametrize("min_steps", [1, 2])
 @pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
-def test_dominant_key_returns_its_value(lib, d, p, min_steps):
+def test_dominant_key_returns_its_value(lib, d, p, min_steps, fixed):
     # one key per (sequence, kv head) scores ~1e3 against the group's query
     # (scale * q.k far beyond exp's fp32 range without the max shift): the
     # output is that token's v, bitwise (every other weight is below 2^-1400).
@@ -444,7 +450,8 @@ def test_dominant_key_returns_its_value(lib, d, p, min_steps):
                 w.k_cache[page, slot, g] = W.f32_to_bf16_bits((2.0 * oracle.bf16_to_f64(key)).astype(np.float32))
                 assert np.isnan(W.bf16_bits_to_f32(w.v_cache[page, slot, g])).all()
     lib.set_option(lib.OPT_MIN_STEPS, min_steps)
-    log(f"case dominant key D={d} P={p} min_steps={min_steps}")
+    lib.set_option(lib.OPT_FIXED_SPLIT, fixed)
+    log(f"case dominant key D={d} P={p} min_steps={min_steps} fixed={fixed}")
     got = run(lib, w)
     check(got, ref(w), "dominant key")
     for (b, g), t in planted.items():
@@ -452,9 +459,10 @@ def test_dominant_key_returns_its_value(lib, d, p, min_steps):
         assert np.array_equal(got[b, g * G:(g + 1) * G], np.broadcast_to(v, (G, d))), (b, g, t)
 
 
+@pytest.mark.parametrize("fixed", [1, 0])
 @pytest.mark.parametrize("min_steps", [1, 2])
 @pytest.mark.parametrize("d,p", EDGE_SHAPES, ids=EDGE_IDS)
-def test_two_dominant_keys_split_the_weight(lib, d, p, min_steps):
+def test_two_dominant_keys_split_the_weight(lib, d, p, min_steps, fixed):
     # two keys scoring ~1000 and ~1000 - ln 2, far apart in the sequence (in
     # different pieces of a split plan): the merge combines two pieces whose
     # maxima are in the thousands, weights ~2/3 and ~1/3
@@ -467,7 +475,8 @@ def test_two_dominant_keys_split_the_weight(lib, d, p, min_steps):
             page, slot = _token_slot(w, b, L - 40 - 9 * g)
             w.k_cache[page, slot, g] = second
     lib.set_option(lib.OPT_MIN_STEPS, min_steps)
-    log(f"case two dominant keys D={d} P={p} min_steps={min_steps}")
+    lib.set_option(lib.OPT_FIXED_SPLIT, fixed)
+    log(f"case two dominant keys D={d} P={p} min_steps={min_steps} fixed={fixed}")
     check(run(lib, w), ref(w), "two dominant keys")
 
 
