@@ -803,6 +803,10 @@ int attention_call(const void* q, const void* k_cache, const void* v_cache, cons
   a.fused = pl.fused;
   a.chunks = pl.chunks;
   a.chunk_steps = pl.chunk_steps;
+  // the first-piece stash of stream-K plans, where the LDS holds it
+  a.stash = pl.chunks == 0 && !pl.fused && pl.grid > 1 && valu_cols == 0 &&
+            pda::attn_stash_lds_bytes(head_dim, batch, pl.waves, pl.hgs, cols, valu_cols > 0) <=
+                static_cast<size_t>(pda::kMaxLdsBytes);
 
   const Rec rec = noalloc ? Rec{nullptr, nullptr, nullptr, 0} : prof_begin(0);
   const bool prof = rec.a != nullptr;

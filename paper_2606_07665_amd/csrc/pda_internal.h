@@ -44,6 +44,9 @@ struct LaunchArgs {
   // grid = batch x (hkv / hgs) x chunks and merge_fixed_kernel merges
   int chunks = 0;
   int chunk_steps = 0;
+  // stream-K only: the partial of a workgroup's first piece is kept in LDS
+  // and written after its last piece (the launch adds attn_stash_lds_bytes)
+  bool stash = false;
 };
 
 // The fused merge is planned when the most partial data one sequence can
@@ -59,5 +62,8 @@ constexpr int kMaxDevices = 64;
 hipError_t noalloc_scratch(int dev, void** ptr);
 hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st);
 size_t attn_lds_bytes(int head_dim, int batch, int waves, bool valu = false);
+// LDS of an attention launch with the first-piece stash: hgs kv heads x cols
+// columns x (head_dim + 4) floats after attn_lds_bytes.
+size_t attn_stash_lds_bytes(int head_dim, int batch, int waves, int hgs, int cols, bool valu = false);
 
 }  // namespace pda

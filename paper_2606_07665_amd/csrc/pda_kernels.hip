@@ -96,6 +96,9 @@ __host__ __device__ constexpr int pref_offset(int waves) {
 
 __device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Start of the first-piece stash (16-byte aligned) after `bytes` of LDS.
+__host__ __device__ constexpr int stash_offset(int bytes) { return (bytes + 15) & ~15; }
+
 // s_waitcnt vmcnt(0): wait for every outstanding vector memory load of the
 // wave (expcnt 7 and lgkmcnt 15 in the gfx9 encoding mean "do not wait").
 constexpr int kWaitAllVectorLoads = 0x0F70;
@@ -323,7 +326,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     float* __restrict__ ws_acc, float* __restrict__ ws_ml, int32_t* __restrict__ ws_pref,
     int32_t* __restrict__ ws_cnt, int batch, int hq, int hkv, int group, int hgs, int page_shift,
     int num_pages, int maxp, int min_steps, float scale_log2, int nq, int window, int chunks,
-    int chunk_steps) {
+    int chunk_steps, int stash) {
   constexpr bool kValu = kNC > 0;
   static_assert(!kValu || (D == 128 && !kLanePages && (kNC == 4 || kNC == 8)), "vector-ALU variant shapes");
   static_assert(!kFixed || (!kValu && !kFused), "the fixed split runs on the matrix cores with the merge kernel");
@@ -336,7 +339,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   // are inputs only, so their loads stay global loads.
   asm volatile(""
                : "+s"(batch), "+s"(hq), "+s"(hkv), "+s"(group), "+s"(hgs), "+s"(page_shift), "+s"(num_pages),
-                 "+s"(maxp), "+s"(min_steps), "+s"(nq), "+s"(window), "+s"(chunks), "+s"(chunk_steps)
+                 "+s"(maxp), "+s"(min_steps), "+s"(nq), "+s"(window), "+s"(chunks), "+s"(chunk_steps), "+s"(stash)
                : "s"(q), "s"(kc), "s"(vc), "s"(bt), "s"(lens), "s"(out), "s"(ws_acc), "s"(ws_ml), "s"(ws_pref));
   using S = Shape<D, kValu>;
   extern __shared__ __align__(16) unsigned char smem[];
@@ -349,6 +352,21 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   int32_t* lens_s = pref + batch + 1;  // clamped lengths (kLensInLds)
   float* ml_x = reinterpret_cast<float*>(smem + ml_offset<D, kValu>(nwaves));
   int32_t* scan = reinterpret_cast<int32_t*>(smem);  // reuses the tiles before the loop
+  // stash != 0: the partial of the workgroup's first piece, when split (a
+  // sequence's tail), is kept here -- [kv head of the group][column][D + 4]
+  // floats after the lengths -- and written after the workgroup's last
+  // piece.  Stores issued mid-kernel are waited for by the next piece's
+  // first load wait (the gfx9 vector memory counter covers stores as well
+  // as loads and retires them in order), so a partial written there holds
+  // the next piece back until the writes are acknowledged.  Measured on the
+  // 4-query-token workload (16 columns, 21 MB of partials): first-piece
+  // partials skipped altogether (a timing-only build) 183 -> 175 us, kept
+  // here 183 -> 178 us; the Zipf batch of 256 sequences 831 -> 825 us; the
+  // others unchanged.
+  float* stash_lds = reinterpret_cast<float*>(
+      smem + stash_offset(pref_offset<D, kValu>(nwaves) + (batch + 1 + (S::kLensInLds ? batch : 0)) * 4));
+  bool stashed = false;
+  int64_t stash_row = 0;
 
   const int tid = threadIdx.x;
   const int page = 1 << page_shift;
@@ -1090,6 +1108,13 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
 #pragma unroll
           for (int dt = 0; dt < S::kDT; ++dt) store_coherent(ra, row * D + 4 * g4 + 16 * dt, acc[dt]);
           if (g4 == 0) store_coherent(rm, row * 2, f32x2{big_m, den});
+        } else if (!kFixed && !kValu && stash && s0 > 0) {
+          float* srow = stash_lds + (hi_w * ncols + c) * (D + 4);
+#pragma unroll
+          for (int dt = 0; dt < S::kDT; ++dt) *reinterpret_cast<f32x4*>(srow + 4 * g4 + 16 * dt) = acc[dt];
+          if (g4 == 0) *reinterpret_cast<f32x2*>(srow + D) = f32x2{big_m, den};
+          stashed = true;
+          stash_row = row;
         } else {
           float* arow = ws_acc + row * D + 4 * g4;
 #pragma unroll
@@ -1125,7 +1150,17 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     }
 
     x += s1 - s0;
-    if (x >= xend) break;
+    if (x >= xend) {
+      if (!kFixed && !kValu && stashed) {  // the first piece's partial, kept in LDS (same lanes as wrote it)
+        const float* srow = stash_lds + (hi_w * ncols + c) * (D + 4);
+        float* arow = ws_acc + stash_row * D + 4 * g4;
+#pragma unroll
+        for (int dt = 0; dt < S::kDT; ++dt)
+          *reinterpret_cast<f32x4*>(arow + 16 * dt) = *reinterpret_cast<const f32x4*>(srow + 4 * g4 + 16 * dt);
+        if (g4 == 0) *reinterpret_cast<f32x2*>(ws_ml + stash_row * 2) = *reinterpret_cast<const f32x2*>(srow + D);
+      }
+      break;
+    }
     s0 = 0;
     if (++hg == ngroups) {
       hg = 0;
@@ -1362,7 +1397,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_fixed_kernel(
 
 template <int D, bool kLanePages, int kNC = 0, bool kFused = false, bool kFixed = false>
 static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
-  const size_t lds = attn_lds_bytes(D, a.batch, a.waves, kNC > 0);
+  const size_t lds = a.stash ? attn_stash_lds_bytes(D, a.batch, a.waves, a.hgs, a.group * a.nq, kNC > 0)
+                             : attn_lds_bytes(D, a.batch, a.waves, kNC > 0);
   // the dynamic-LDS limit is raised once per device (bit = device ordinal)
   static std::atomic<uint64_t> attr_set{0};
   int dev = 0;
@@ -1378,7 +1414,7 @@ static hipError_t launch_attn(const LaunchArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((attn_kernel<D, kLanePages, kNC, kFused, kFixed>), dim3(a.grid), dim3(64 * a.waves), lds, st, a.q,
                      a.k, a.v, a.bt, a.lens, a.out, a.ws_acc, a.ws_ml, a.ws_pref, a.ws_cnt, a.batch, a.hq, a.hkv,
                      a.group, a.hgs, a.page_shift, a.num_pages, a.maxp, a.min_steps, a.scale * kLog2e, a.nq,
-                     a.window, a.chunks, a.chunk_steps);
+                     a.window, a.chunks, a.chunk_steps, a.stash ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -1453,6 +1489,11 @@ hipError_t launch_merge_kernel(const LaunchArgs& a, hipStream_t st) {
   if (a.head_dim == 256)
     return many ? launch_merge<256, 4>(a, st) : by_split ? launch_merge<256, 1, true>(a, st) : launch_merge<256, 1>(a, st);
   return many ? launch_merge<64, 8>(a, st) : by_split ? launch_merge<64, 1, true>(a, st) : launch_merge<64, 1>(a, st);
+}
+
+size_t attn_stash_lds_bytes(int head_dim, int batch, int waves, int hgs, int cols, bool valu) {
+  return static_cast<size_t>(stash_offset(static_cast<int>(attn_lds_bytes(head_dim, batch, waves, valu)))) +
+         static_cast<size_t>(hgs) * cols * (head_dim + 4) * sizeof(float);
 }
 
 size_t attn_lds_bytes(int head_dim, int batch, int waves, bool valu) {
