@@ -230,9 +230,11 @@ Plan plan_for(int hgs, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t
 // number of chunks of whole 32-token steps, as many as the stream-K plan
 // would give it at the page table's largest context (but at least 2 and
 // within the device's workgroups), so each workgroup knows its piece from
-// its index.  Returns a plan with grid 0 where it does not apply: one
-// workgroup, or more sequences than half the device's workgroups (the
-// stream-K split balances those better).  One partial slot per workgroup.
+// its index.  Where the stream-K plan takes a single workgroup, every pair is
+// one chunk: whole sequences, one workgroup each, nothing to merge.  Returns
+// a plan with grid 0 where it does not apply: more pairs than half the
+// device's workgroups (the stream-K split balances those better).  One
+// partial slot per workgroup.
 Plan plan_fixed(const Plan& base, int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, int num_cus,
                 int cols) {
   Plan pl = base;
@@ -243,12 +245,15 @@ Plan plan_fixed(const Plan& base, int32_t batch, int32_t hkv, int32_t d, int32_t
   const int64_t max_ctx = static_cast<int64_t>(maxp) * p;
   const int64_t steps_seq = (max_ctx + pda::kStep - 1) / pda::kStep;
   const int64_t per_block = static_cast<int64_t>(pl.min_steps) * phases;
-  if (base.grid <= 1 || 2 * seqs > target) return pl;
-  int64_t chunks = std::min((steps_seq + per_block - 1) / per_block, target / seqs);
-  chunks = std::max<int64_t>(chunks, 1);
+  if (base.grid < 1 || 2 * seqs > target) return pl;
+  int64_t chunks = 1;
+  if (base.grid > 1) {
+    chunks = std::min((steps_seq + per_block - 1) / per_block, target / seqs);
+    chunks = std::max<int64_t>(chunks, 1);
+  }
   const int64_t chunk_steps = (steps_seq + chunks - 1) / chunks;
   chunks = (steps_seq + chunk_steps - 1) / chunk_steps;  // no chunk wholly past the largest context
-  if (chunks < 2) return pl;
+  if (base.grid > 1 && chunks < 2) return pl;
   pl.grid = static_cast<int>(seqs * chunks);
   pl.chunks = static_cast<int>(chunks);
   pl.chunk_steps = static_cast<int>(chunk_steps);
@@ -325,9 +330,9 @@ Plan make_plan(int32_t batch, int32_t hkv, int32_t d, int32_t p, int32_t maxp, i
   }
   // (the vector-ALU variant, a measurement aid, keeps the merge kernel)
   if (dflt.grid == 1 || !fused_merge() || compute_path() != 0) {
-    if (small && dflt.grid > 1 && fixed_split() && compute_path() == 0) {
+    if (small && fixed_split() && compute_path() == 0) {
       const Plan f = plan_fixed(dflt, batch, hkv, d, p, maxp, num_cus, cols);
-      if (f.grid > 1) return f;
+      if (f.grid > 0) return f;
     }
     return dflt;
   }
@@ -813,9 +818,10 @@ int attention_call(const void* q, const void* k_cache, const void* v_cache, cons
   if (prof && (e = hipEventRecord(rec.a, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
   if ((e = pda::launch_attn_kernel(a, st)) != hipSuccess) return hip_fail(e, "attention kernel launch");
   if (prof && (e = hipEventRecord(rec.b, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  // with one workgroup every piece is a whole sequence: nothing to merge;
-  // a fused plan merged in the attention kernel
-  if (pl.grid > 1 && !pl.fused && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
+  // with one workgroup, or one fixed-split chunk per sequence, every piece
+  // is a whole sequence: nothing to merge; a fused plan merged in the
+  // attention kernel
+  if (pl.grid > 1 && !pl.fused && pl.chunks != 1 && (e = pda::launch_merge_kernel(a, st)) != hipSuccess)
     return hip_fail(e, "merge kernel launch");
   if (prof) {
     if ((e = hipEventRecord(rec.c, st)) != hipSuccess) return hip_fail(e, "hipEventRecord");

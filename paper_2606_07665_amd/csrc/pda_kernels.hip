@@ -497,7 +497,19 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       first_pids(fx_s0 + ph + phases, fx_pa1, fx_pb1);
     }
     fx_nb = seq_steps(clamp_len(uniform(fx_L), max_ctx), nq, window);
-    if (fx_s0 >= fx_nb) return;  // a chunk past the sequence's end
+    if (fx_s0 >= fx_nb) {  // a chunk past the sequence's end
+      if (fx_nb == 0 && fx_s0 == 0) {
+        // an empty sequence: chunk 0's workgroup writes its zero rows (the
+        // heads of group fx_hg are contiguous for each query token)
+        const int row16 = hgs * group * D / 8;
+        for (int j = 0; j < nq; ++j) {
+          u32x4* orow = reinterpret_cast<u32x4*>(
+              out + ((static_cast<int64_t>(fx_b) * nq + j) * hq + fx_hg * hgs * group) * D);
+          for (int i = tid; i < row16; i += nthreads) orow[i] = u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+      return;
+    }
   }
 
   // ws_split[blk]: the (sequence, kv-head group) whose first split point
@@ -1288,8 +1300,8 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(
 // of chunk_steps-step chunks the sequence's steps fill.  n follows from the
 // length alone, so the partials of every chunk are requested together with
 // the length and those of chunks past n (stale data of other calls) are
-// selected away.  n = 1: the attention kernel wrote the sequence itself;
-// n = 0: the row is zero.  Same layout and slot order as merge_kernel.
+// selected away.  n = 1: the attention kernel wrote the sequence itself,
+// and n = 0 its zero row.  Same layout and slot order as merge_kernel.
 template <int D, int kPG>
 __global__ __launch_bounds__(kMergeThreads) void merge_fixed_kernel(
     uint16_t* __restrict__ out, const float* __restrict__ ws_acc, const float* __restrict__ ws_ml,
@@ -1361,7 +1373,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_fixed_kernel(
     const f32x2 mlv = *reinterpret_cast<const f32x2*>(ws_ml + row_of(w) * 2);
     take(mlv[0], mlv[1], *reinterpret_cast<const f32x4*>(ws_acc + row_of(w) * D + 4 * col));
   }
-  if (n == 1) return;  // whole: written by the attention kernel (uniform per workgroup)
+  if (n <= 1) return;  // whole or empty: written by the attention kernel (uniform per workgroup)
   if (kPG > 1) {
     s_num[hs][pg][col] = nn;
     if (col == 0) {

@@ -120,10 +120,14 @@ def test_fixed_split_option(lib):
     assert B.get_option(B.OPT_FIXED_SPLIT) == 1
     assert B.plan(2, 16, 4, 256, 32, 94, num_cus=256)[0] == 192
     assert B.plan(4, 64, 8, 128, 16, 8192, num_cus=256)[0] == 256  # long70b: stream-K
+    # a call the stream-K split gives one workgroup: one chunk per sequence,
+    # whole sequences on separate workgroups (2 x 128 tokens, 8:2 heads)
+    assert B.plan(2, 8, 2, 64, 16, 8, num_cus=256)[0] == 2
     try:
         B.set_option(B.OPT_FIXED_SPLIT, 0)
         assert B.get_option(B.OPT_FIXED_SPLIT) == 0
         assert B.plan(2, 16, 4, 256, 32, 94, num_cus=256)[0] == 188
+        assert B.plan(2, 8, 2, 64, 16, 8, num_cus=256)[0] == 1
         with pytest.raises(B.PdaError):
             B.set_option(B.OPT_FIXED_SPLIT, 2)
         with pytest.raises(B.PdaError):
