@@ -375,10 +375,13 @@ int32_t pda_version(void);
  *                          1: plans with little partial data per sequence
  *                          (small batches, single requests) merge inside
  *                          the attention kernel, by the last workgroup to
- *                          finish each sequence, with one kv head per
- *                          workgroup if that is what it takes (measured
- *                          slower than the merge kernel on MI355X: the
- *                          in-kernel hand-off costs more than a launch);
+ *                          finish each sequence: a call that takes the
+ *                          fixed split keeps it (the pieces of a sequence
+ *                          follow from its length), a stream-K plan takes
+ *                          one kv head per workgroup if that is what it
+ *                          takes (both measured slower than the merge
+ *                          kernel on MI355X: the in-kernel hand-off costs
+ *                          more than a launch);
  *                          2: every plan with several workgroups merges in
  *                          the attention kernel, with the default kv-head
  *                          grouping (for tests: slow for long contexts).

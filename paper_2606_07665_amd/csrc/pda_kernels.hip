@@ -230,8 +230,8 @@ __device__ __forceinline__ constexpr int valu_slot(int is) {
 }
 
 // The fused merge of one split sequence (kv-head group hg of sequence b,
-// pieces in workgroups w0 .. w1) by the workgroup that counted its last
-// piece: per (query row, float4 column) of the group,
+// pieces in workgroups w0 .. w1, in slots w + base) by the workgroup that
+// counted its last piece: per (query row, float4 column) of the group,
 //   out = sum_j 2^(m_j - M) acc_j / sum_j 2^(m_j - M) l_j,  M = max_j m_j,
 // in slot order.  When the rows x columns leave threads over, each item's
 // pieces are dealt to PG groups (piece w to group (w - w0) mod PG) whose
@@ -239,7 +239,7 @@ __device__ __forceinline__ constexpr int valu_slot(int is) {
 template <int D>
 __device__ void merge_in_workgroup(uint16_t* __restrict__ out, const float* __restrict__ ws_acc,
                                    const float* __restrict__ ws_ml, unsigned char* smem, int b, int hg, int w0,
-                                   int w1, int ngroups, int hgs, int ncols, int group, int nq, int hq) {
+                                   int w1, int64_t base, int hgs, int ncols, int group, int nq, int hq) {
   constexpr int kC4 = D / 4;
   const int nthreads = blockDim.x;
   const int tid = threadIdx.x;
@@ -247,7 +247,6 @@ __device__ void merge_in_workgroup(uint16_t* __restrict__ out, const float* __re
   int pgs = 1;
   while (pgs < 8 && items * pgs * 2 <= nthreads) pgs *= 2;
   const __amdgpu_buffer_rsrc_t ra = ws_rsrc(ws_acc), rm = ws_rsrc(ws_ml);
-  const int64_t base = static_cast<int64_t>(b) * ngroups + hg;
   f32x4* s_num = reinterpret_cast<f32x4*>(smem);        // [pg][item]
   f32x2* s_ml = reinterpret_cast<f32x2*>(s_num + items * pgs);
   for (int it0 = 0; it0 < items * pgs; it0 += nthreads) {
@@ -329,7 +328,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     int chunk_steps, int stash) {
   constexpr bool kValu = kNC > 0;
   static_assert(!kValu || (D == 128 && !kLanePages && (kNC == 4 || kNC == 8)), "vector-ALU variant shapes");
-  static_assert(!kFixed || (!kValu && !kFused), "the fixed split runs on the matrix cores with the merge kernel");
+  static_assert(!kFixed || !kValu, "the fixed split runs on the matrix cores");
   // Every argument in SGPRs before anything waits on one: the compiler
   // otherwise requests them in two groups with a wait between (the second
   // group only where the first pointer is used), and since scalar loads
@@ -461,7 +460,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
   // columns and the page ids of the wave's first two steps (without a
   // window they do not depend on the length) are requested before the
   // length is waited for
-  int fx_b = 0, fx_hg = 0, fx_s0 = 0, fx_L = 0, fx_nb = 0;
+  int fx_b = 0, fx_hg = 0, fx_s0 = 0, fx_L = 0, fx_nb = 0, fx_w0 = 0;
   u32x4 fx_q[S::kQK];
   int fx_pa0 = 0, fx_pb0 = 0, fx_pa1 = 0, fx_pb1 = 0;
   if constexpr (kFixed) {
@@ -469,6 +468,7 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
     fx_b = div_small_u(e, ngroups);
     fx_hg = e - fx_b * ngroups;
     fx_s0 = (blk - e * chunks) * chunk_steps;
+    fx_w0 = e * chunks;  // the pair's first workgroup (and slot)
     fx_L = lens[fx_b];
     // a padding column (c >= ncols) reads a row inside q (token nq - 1,
     // head qh < group) and is zeroed where the operand is formed
@@ -1146,14 +1146,21 @@ __global__ __launch_bounds__(64 * max_waves(D), 1) void attn_kernel(
       __builtin_amdgcn_s_waitcnt(0);
       __syncthreads();
       int32_t* flag = reinterpret_cast<int32_t*>(ml_x);
-      const int64_t x0 = static_cast<int64_t>(pref[b]) * ngroups + static_cast<int64_t>(hg) * nb;
-      const int w0 = static_cast<int>(owner_of(x0, total, beff));
-      const int w1 = static_cast<int>(owner_of(x0 + nb - 1, total, beff));
+      int w0, w1;
+      if constexpr (kFixed) {  // the pair's chunks that hold steps: workgroups w0 .. w0 + n - 1
+        w0 = fx_w0;
+        w1 = fx_w0 + div_small_u(nb + chunk_steps - 1, chunk_steps) - 1;
+      } else {
+        const int64_t x0 = static_cast<int64_t>(pref[b]) * ngroups + static_cast<int64_t>(hg) * nb;
+        w0 = static_cast<int>(owner_of(x0, total, beff));
+        w1 = static_cast<int>(owner_of(x0 + nb - 1, total, beff));
+      }
       if (tid == 0)
         *flag = __hip_atomic_fetch_add(ws_cnt + w0, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == w1 - w0;
       __syncthreads();
       if (uniform(*flag)) {
-        merge_in_workgroup<D>(out, ws_acc, ws_ml, smem, b, hg, w0, w1, ngroups, hgs, ncols, group, nq, hq);
+        merge_in_workgroup<D>(out, ws_acc, ws_ml, smem, b, hg, w0, w1,
+                              kFixed ? 0 : static_cast<int64_t>(b) * ngroups + hg, hgs, ncols, group, nq, hq);
         if (tid == 0) __hip_atomic_store(ws_cnt + w0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __syncthreads();  // the flag and the tiles are reused by the next piece
@@ -1439,8 +1446,14 @@ hipError_t launch_attn_kernel(const LaunchArgs& a, hipStream_t st) {
       return hipErrorInvalidValue;
     return a.valu_cols == 4 ? launch_attn<128, false, 4>(a, st) : launch_attn<128, false, 8>(a, st);
   }
+  if (a.chunks > 0 && a.fused) {
+    if (a.head_dim == 128)
+      return lane_pages ? launch_attn<128, true, 0, true, true>(a, st) : launch_attn<128, false, 0, true, true>(a, st);
+    if (a.head_dim == 256)
+      return lane_pages ? launch_attn<256, true, 0, true, true>(a, st) : launch_attn<256, false, 0, true, true>(a, st);
+    return lane_pages ? launch_attn<64, true, 0, true, true>(a, st) : launch_attn<64, false, 0, true, true>(a, st);
+  }
   if (a.chunks > 0) {
-    if (a.fused) return hipErrorInvalidValue;
     if (a.head_dim == 128)
       return lane_pages ? launch_attn<128, true, 0, false, true>(a, st) : launch_attn<128, false, 0, false, true>(a, st);
     if (a.head_dim == 256)
