@@ -9,6 +9,7 @@ call raises.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 import re
 from typing import Optional, Tuple
@@ -192,6 +193,20 @@ def _stream_ptr(stream, device=None):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+@functools.lru_cache(maxsize=None)
+def _parsed_dims(dims):
+    """dims string -> tuple of (kind, value): 0 any, 1 number, 2 symbol."""
+    out = []
+    for sym in dims.split():
+        if sym == "*":
+            out.append((0, None))
+        elif sym.isdigit():
+            out.append((1, int(sym)))
+        else:
+            out.append((2, sym))
+    return tuple(out)
+
+
 def _validate(specs, known=None):
     """Argument checks of a wrapper, before any launch.  ``specs``: (name,
     tensor or None, torch dtype, dims) with dims a space-separated list of
@@ -199,7 +214,42 @@ def _validate(specs, known=None):
     that has it (or by ``known``) and checked on every other.  All shapes are
     checked first, then dtypes, then that every tensor is on one GPU, then
     contiguity, so a bad argument raises whichever it is.  Returns the
-    bound sizes."""
+    bound sizes.  The usual case (every check passes) reads each property of
+    a tensor once; any failure reruns the checks in that order to raise."""
+    sizes = dict(known or {})
+    dev = None
+    ok = True
+    for _, t, dt, dims in specs:
+        if t is None:
+            continue
+        shape = t.shape
+        pd = _parsed_dims(dims)
+        if len(shape) != len(pd):
+            ok = False
+            break
+        for (kind, val), ext in zip(pd, shape):
+            if kind == 1:
+                if ext != val:
+                    ok = False
+            elif kind == 2:
+                want = sizes.get(val)
+                if want is None:
+                    sizes[val] = int(ext)
+                elif ext != want:
+                    ok = False
+        d = t.get_device()
+        if dev is None:
+            dev = d
+        if not ok or t.dtype != dt or d < 0 or d != dev or not t.is_contiguous():
+            ok = False
+            break
+    if ok:
+        return sizes
+    return _validate_raise(specs, known)
+
+
+def _validate_raise(specs, known=None):
+    """The checks of _validate one kind at a time, raising the first failure."""
     sizes = dict(known or {})
     present = [sp for sp in specs if sp[1] is not None]
     for name, t, _, dims in present:
