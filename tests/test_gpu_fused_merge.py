@@ -6,7 +6,10 @@ PDA_OPT_FUSED_MERGE: 0 (default) never fuses, 1 fuses plans with little
 partial data per sequence (single requests, small batches), 2 fuses every
 plan with several workgroups -- used here to run the fused merge over many
 pieces, several passes of a workgroup over the query rows, windows and
-several query tokens, head sizes 64/128/256 and both page-size paths."""
+several query tokens, head sizes 64/128/256 and both page-size paths.  A
+latency-bound call keeps its fixed split under either mode (the pieces of a
+sequence are the chunks its length fills); larger calls take the stream-K
+split."""
 import numpy as np
 import pytest
 
@@ -122,8 +125,9 @@ def test_fused_merge_through_noalloc_scratch(lib):
 
 
 def test_llama8b_single_request_fused_plan(lib):
-    # with the option on, the single-request workload merges in the
-    # attention kernel (one kv head per workgroup); within one bf16 spacing
+    # with the option on, the single-request workload keeps the fixed split
+    # and each (sequence, kv-head group) is merged by the last of its chunks
+    # to finish, in the attention kernel; within one bf16 spacing
     lib.set_option(lib.OPT_FUSED_MERGE, 1)
     w = W.make("llama8b")
     got = run(lib, w)
