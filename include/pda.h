@@ -398,18 +398,20 @@ int32_t pda_version(void);
  *                          largest group that cuts no (sequence, kv-head
  *                          group) into more than 32 pieces.
  *   PDA_OPT_FIXED_SPLIT    1 (default, env PDA_FIXED_SPLIT): a call whose
- *                          K and V fit in 128 MB, planned on several
- *                          workgroups for at most half the device's
- *                          workgroups' worth of (sequence, kv-head group)
- *                          pairs, cuts every pair into the same number of
- *                          chunks of whole 32-token steps sized by the page
- *                          table's largest context, so that a workgroup
- *                          knows its piece from its index (no steps prefix
- *                          on the way to the first loads; the merge finds
- *                          the pieces from the lengths).  0: every call is
- *                          split stream-K over the actual lengths.  Both
- *                          are deterministic for a fixed plan; they round
- *                          differently.
+ *                          K and V fit in 128 MB and that has at most half
+ *                          the device's workgroups' worth of (sequence,
+ *                          kv-head group) pairs cuts every pair into the
+ *                          same number of chunks of whole 32-token steps
+ *                          sized by the page table's largest context, so
+ *                          that a workgroup knows its piece from its index
+ *                          (no steps prefix on the way to the first loads;
+ *                          the merge finds the pieces from the lengths).
+ *                          Where the stream-K plan would take a single
+ *                          workgroup, every pair is one chunk: whole
+ *                          sequences on separate workgroups, no merge.
+ *                          0: every call is split stream-K over the actual
+ *                          lengths.  Both are deterministic for a fixed
+ *                          plan; they round differently.
  * Options are process-wide and apply to later calls.  pda_set_option
  * returns PDA_OK or PDA_ERR_SHAPE / PDA_ERR_UNSUPPORTED; pda_get_option
  * returns the current value or -1 for an unknown option.
