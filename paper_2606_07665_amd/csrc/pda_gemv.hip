@@ -355,9 +355,13 @@ __global__ __launch_bounds__(kW * 64, 1) void gemv_thin_kernel(const uint16_t* _
   constexpr int kDma = kFrags / kW;
   constexpr int kStages = kD + 1;
   constexpr int kLoads = kDma + kC * kR;  // vector memory instructions per wave and chunk
-  constexpr int kAhead = (kD - 1) * kLoads;
-  static_assert(kAhead < 64, "vmcnt holds at most 63");
-  constexpr int kWaitChunk = 0x0F70 | (kAhead & 15) | ((kAhead >> 4) << 14);
+  static_assert(kD >= 2, "the next chunk's loads are waited for while later ones stay in flight");
+  constexpr int kAheadFirst = (kD - 1) * kLoads;  // after chunk 0's loads
+  constexpr int kAheadNext = (kD - 2) * kLoads;   // after chunk c + 1's loads, at chunk c
+  static_assert(kAheadFirst < 64, "vmcnt holds at most 63");
+  // vmcnt(n) with expcnt and lgkmcnt not waited for / with lgkmcnt(0)
+  constexpr int kWaitFirst = 0x0F70 | (kAheadFirst & 15) | ((kAheadFirst >> 4) << 14);
+  constexpr int kWaitNext = 0x0070 | (kAheadNext & 15) | ((kAheadNext >> 4) << 14);
   constexpr uint32_t kOutside = 0x80000000u;  // past any descriptor of x: reads zero
   const int lane = threadIdx.x & 63;
   const int wv = uniform(threadIdx.x >> 6);
@@ -436,25 +440,33 @@ __global__ __launch_bounds__(kW * 64, 1) void gemv_thin_kernel(const uint16_t* _
   int mg = lg;
   int mkt = lkt;
   int64_t mu = u0;
-  // A unit's partial flush comes before its B fragments are read: every
-  // fragment is requested before the first MFMA, and each MFMA waits only
-  // for its own.
-  auto mma = [&](int stage) __attribute__((always_inline)) {
+  // B fragments of the chunk being multiplied; each register is refilled
+  // with the next chunk's fragment right after the kR MFMAs that read it,
+  // so the LDS reads of chunk c + 1 run under the MFMAs of chunk c and no
+  // MFMA waits for LDS.  A unit's partial flush comes before its MFMAs.
+  u32x4 b[kC][kNBT];
+  auto frag = [&](int stage, int j, int bt) __attribute__((always_inline)) {
+    return *reinterpret_cast<const u32x4*>(xs + ((stage * kC + j) * kNBT + bt) * 1024 + 16 * lane);
+  };
+  auto mma = [&](int stage, int next) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < kC; ++j) {
       if (mu < u1 && mkt == 0 && mu != u0) flush(mg - 1);
-      u32x4 b[kNBT];
+      // a chunk past the range holds zeros in LDS and in its weight
+      // registers (both read outside their descriptors), so its MFMAs add
+      // exact zeros: no branch around them
 #pragma unroll
-      for (int bt = 0; bt < kNBT; ++bt)
-        b[bt] = *reinterpret_cast<const u32x4*>(xs + ((stage * kC + j) * kNBT + bt) * 1024 + 16 * lane);
-      __builtin_amdgcn_sched_barrier(0);  // keeps the reads ahead of the MFMAs
-      if (mu < u1) {
+      for (int bt = 0; bt < kNBT; ++bt) {
 #pragma unroll
-        for (int bt = 0; bt < kNBT; ++bt)
+        for (int r = 0; r < kR; ++r)
+          acc[r][bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[stage][j][r]),
+                                                               __builtin_bit_cast(bf16x8, b[j][bt]), acc[r][bt], 0, 0, 0);
+        b[j][bt] = frag(next, j, bt);
+      }
 #pragma unroll
-          for (int r = 0; r < kR; ++r)
-            acc[r][bt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[stage][j][r]),
-                                                                 __builtin_bit_cast(bf16x8, b[bt]), acc[r][bt], 0, 0, 0);
+      for (int bt = 0; bt < kNBT; ++bt) {
+        __builtin_amdgcn_sched_group_barrier(0x008, kR, 0);  // the kR MFMAs of fragment bt
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // then its refill
       }
       ++mu;
       if (++mkt == kt_count) {
@@ -464,25 +476,44 @@ __global__ __launch_bounds__(kW * 64, 1) void gemv_thin_kernel(const uint16_t* _
     }
   };
 
-  // chunks past the range load nothing (zero-size reads), so every chunk
-  // issues the same loads and the wait for chunk c is one count
+  // Chunks past the range load nothing (zero-size reads) and add zeros,
+  // so every chunk issues the same loads, the waits are fixed counts, and
+  // the ring is walked in whole turns (a range is padded by at most
+  // kStages - 1 such chunks): with a branch around each stage the compiler
+  // must allow for skipped stages, and it then waited for every load but
+  // the newest chunk's before the MFMAs, one chunk of prefetch whatever the
+  // depth.  The prologue keeps each chunk's loads in the loop's order
+  // (copies, then weights), so the first turn counts like the others.
 #pragma unroll
-  for (int s = 0; s < kD; ++s) issue(s);
+  for (int s = 0; s < kD; ++s) {
+    issue(s);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // chunk 0 in LDS for every wave, then its fragments into registers
+  __builtin_amdgcn_s_waitcnt(kWaitFirst);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+#pragma unroll
+  for (int j = 0; j < kC; ++j)
+#pragma unroll
+    for (int bt = 0; bt < kNBT; ++bt) b[j][bt] = frag(0, j, bt);
   for (int c0 = 0; c0 < nch; c0 += kStages) {
 #pragma unroll
     for (int s = 0; s < kStages; ++s) {
-      if (c0 + s < nch) {
-        // this wave's copies and weights of chunk c0 + s; after the barrier,
-        // every wave's copies, and stage s - 1 has been read by all.  A bare
-        // s_barrier, fenced for the compiler only: a workgroup fence would
-        // also wait for the copies still in flight into the later stages.
-        __builtin_amdgcn_s_waitcnt(kWaitChunk);
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        issue((s + kD) % kStages);
-        mma(s);
-      }
+      // At chunk c = c0 + s: this wave's copies and weights of chunk c + 1
+      // have landed and its reads of chunk c's fragments are done; after the
+      // barrier every wave's copies of chunk c + 1 are in LDS and stage
+      // s - 1 (chunk c - 1, read during chunk c - 2) is free for chunk
+      // c + kD.  A bare s_barrier, fenced for the compiler only: a workgroup
+      // fence would also wait for the copies still in flight into the later
+      // stages.
+      __builtin_amdgcn_s_waitcnt(kWaitNext);
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      issue((s + kD) % kStages);
+      mma(s, (s + 1) % kStages);
     }
   }
   if (u1 > u0) {
@@ -1006,7 +1037,7 @@ hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
     if (nbt == 3) return launch_xlds<3>(a, st);
     if (nbt == 4) return launch_xlds<4>(a, st);
     if (nbt <= 8) return launch_xlds<8>(a, st);  // column tiles past the batch read zeros
-    return launch_thin<16, 4, 2, 1, 3>(a, st);
+    return launch_thin<16, 4, 2, 1, 4>(a, st);
   }
   if (nbt > 4) return hipErrorInvalidValue;  // above 64 sequences only the thin-GEMM form
   const bool grouped = a.plan.group > 1;
