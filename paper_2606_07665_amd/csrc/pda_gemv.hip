@@ -843,6 +843,71 @@ __global__ __launch_bounds__(kOProjOneThreads) void oproj_one_kernel(OProjArgs a
   }
 }
 
+
+// The same for tile-major partials (the 256-sequence GEMV form), two
+// sequences per workgroup: sequences 2i and 2i + 1 own the two 64-byte
+// halves of every 128-byte line of their partials, so this workgroup reads
+// whole lines that no other workgroup touches, where one workgroup per
+// sequence fetched each line twice, on two CUs (256 x 5120: 11.5 against
+// 17.1 us, event-timed).  In each group of eight threads, thread q takes
+// sequence 2i + q / 4 and features 4 (q % 4) .. +3 of a 16-feature piece.
+template <int kSlots>
+__global__ __launch_bounds__(kOProjOneThreads) void oproj_pair_kernel(OProjArgs a) {
+  constexpr int kGroups = 2 * kOProjOneFeatures / 4;  // groups of four features per thread, at most
+  constexpr int kPieces = kOProjOneThreads / 8;       // 16-feature pieces per round
+  __shared__ float wsum[2][kOProjOneThreads / 64];
+  const int tid = threadIdx.x;
+  const int q = tid & 7;
+  const int sq = q >> 2;
+  const int b = 2 * blockIdx.x + sq;
+  const bool live = b < a.batch;  // an odd batch: the last workgroup has one sequence
+  const int64_t base = static_cast<int64_t>(b) * a.hidden;
+  float4 z[kGroups];
+  uint2 w[kGroups];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kGroups; ++j) {
+    const int n = 16 * ((tid >> 3) + kPieces * j) + 4 * (q & 3);
+    z[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    w[j] = make_uint2(0u, 0u);
+    if (live && n < a.hidden) {
+      w[j] = *reinterpret_cast<const uint2*>(a.norm_w + n);
+      const uint2 r = *reinterpret_cast<const uint2*>(a.residual + base + n);
+      const float4 y = gemv_rows4<kSlots>(a.part, a.plan, a.batch, b, n);
+      z[j] = make_float4(y.x + bf16_to_f32(static_cast<uint16_t>(r.x)), y.y + bf16_to_f32(static_cast<uint16_t>(r.x >> 16)),
+                         y.z + bf16_to_f32(static_cast<uint16_t>(r.y)), y.w + bf16_to_f32(static_cast<uint16_t>(r.y >> 16)));
+      ss += z[j].x * z[j].x + z[j].y * z[j].y + z[j].z * z[j].z + z[j].w * z[j].w;
+      uint2 o;
+      o.x = f32_to_bf16(z[j].x) | (static_cast<uint32_t>(f32_to_bf16(z[j].y)) << 16);
+      o.y = f32_to_bf16(z[j].z) | (static_cast<uint32_t>(f32_to_bf16(z[j].w)) << 16);
+      *reinterpret_cast<uint2*>(a.residual_out + base + n) = o;
+    }
+  }
+  // per-sequence sums: the lanes of one sequence share bit 2 of the lane id
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1)
+    if (off != 4) ss += __shfl_xor(ss, off);
+  if ((tid & 63) == 0) wsum[0][tid >> 6] = ss;
+  if ((tid & 63) == 4) wsum[1][tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < kOProjOneThreads / 64; ++i) tot += wsum[sq][i];
+  const float inv = rsqrtf(tot / a.hidden + a.eps);
+#pragma unroll
+  for (int j = 0; j < kGroups; ++j) {
+    const int n = 16 * ((tid >> 3) + kPieces * j) + 4 * (q & 3);
+    if (live && n < a.hidden) {
+      uint2 o;
+      o.x = f32_to_bf16(z[j].x * inv * bf16_to_f32(static_cast<uint16_t>(w[j].x))) |
+            (static_cast<uint32_t>(f32_to_bf16(z[j].y * inv * bf16_to_f32(static_cast<uint16_t>(w[j].x >> 16)))) << 16);
+      o.y = f32_to_bf16(z[j].z * inv * bf16_to_f32(static_cast<uint16_t>(w[j].y))) |
+            (static_cast<uint32_t>(f32_to_bf16(z[j].w * inv * bf16_to_f32(static_cast<uint16_t>(w[j].y >> 16)))) << 16);
+      *reinterpret_cast<uint2*>(a.normed_out + base + n) = o;
+    }
+  }
+}
+
 }  // namespace
 
 // Instantiations of the epilogues by the plan's partial slots per group.
@@ -869,7 +934,10 @@ hipError_t launch_prelude(const PreludeArgs& a, hipStream_t st) {
 
 template <int kSlots>
 hipError_t launch_oproj_one(const OProjArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((oproj_one_kernel<kSlots>), dim3(a.batch), dim3(kOProjOneThreads), 0, st, a);
+  if (a.plan.seq_major)
+    hipLaunchKernelGGL((oproj_one_kernel<kSlots>), dim3(a.batch), dim3(kOProjOneThreads), 0, st, a);
+  else  // tile-major partials (the 256-sequence GEMV form): two sequences per workgroup
+    hipLaunchKernelGGL((oproj_pair_kernel<kSlots>), dim3((a.batch + 1) / 2), dim3(kOProjOneThreads), 0, st, a);
   return hipGetLastError();
 }
 
