@@ -55,8 +55,11 @@ SMALL = [(1, 32, 16), (3, 96, 48), (17, 4096, 2560), (64, 512, 1024), (5, 64, 32
          # by 8, otherwise the per-wave form with 2, 3 or 4 row tiles per unit
          # (1056 rows: 66 tiles; 1088: 68) or one (1040: 65)
          (32, 256, 1056), (48, 512, 1056), (64, 512, 1088), (40, 1024, 1040), (64, 4096, 4096),
-         # above 64 sequences: the thin-GEMM form with 8 or 16 column tiles
-         (65, 1024, 1024), (128, 512, 2048), (200, 256, 384), (256, 2048, 1280)]
+         # above 64 sequences: the thin-GEMM form with 8 or 16 column tiles;
+         # above 128 its tile-major partials go to the two-sequence epilogue,
+         # whose last workgroup has one sequence at an odd batch
+         (65, 1024, 1024), (128, 512, 2048), (200, 256, 384), (256, 2048, 1280),
+         (129, 512, 1024), (255, 1024, 640)]
 
 
 @pytest.mark.parametrize("b,k,h", SMALL, ids=[f"B{c[0]}-K{c[1]}-H{c[2]}" for c in SMALL])
