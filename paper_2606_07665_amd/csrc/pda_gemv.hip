@@ -884,9 +884,11 @@ __global__ __launch_bounds__(kOProjOneThreads) void oproj_pair_kernel(OProjArgs 
     }
   }
   // per-sequence sums: the lanes of one sequence share bit 2 of the lane id
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1)
-    if (off != 4) ss += __shfl_xor(ss, off);
+  ss += __shfl_xor(ss, 32);
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 8);
+  ss += __shfl_xor(ss, 2);
+  ss += __shfl_xor(ss, 1);
   if ((tid & 63) == 0) wsum[0][tid >> 6] = ss;
   if ((tid & 63) == 4) wsum[1][tid >> 6] = ss;
   __syncthreads();
