@@ -719,7 +719,11 @@ int run_prelude(const void* x, const void* w_packed, const void* bias, const voi
   ep.d = d.head_dim;
   ep.rotary_dim = d.rotary_dim;
   ep.interleaved = d.interleaved;
-  ep.log2_theta = std::log2(static_cast<double>(d.rope_theta));
+  {
+    const double log2_theta = std::log2(static_cast<double>(d.rope_theta));
+    for (int k = 0; k < 8; ++k)
+      ep.freq_pow2[k] = d.rotary_dim > 0 ? std::exp2(-(2.0 * (1 << k) / d.rotary_dim) * log2_theta) : 0.0;
+  }
   ep.eps = d.eps;
   if ((e = pda::launch_prelude_epilogue(ep, st)) != hipSuccess) return hip_fail(e, "prelude epilogue launch");
   if (prof) {

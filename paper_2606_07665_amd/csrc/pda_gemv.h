@@ -96,7 +96,10 @@ struct PreludeArgs {
   const int32_t* bt;         // [batch, maxp]
   int page_shift, num_pages, maxp;
   int batch, hq, hkv, d, rotary_dim, interleaved;
-  double log2_theta;  // log2 of the rotary base, computed in fp64 on the host
+  // theta^(-2 * 2^k / rotary_dim) for k = 0..7, in fp64 from the host: the
+  // frequency theta^(-2i/rotary_dim) of pair i (i < 128) is the product of
+  // those for the set bits of i
+  double freq_pow2[8];
   float eps;
 };
 
