@@ -709,8 +709,8 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
       // its fraction in [-1/2, 1/2] goes to the hardware sine and cosine,
       // which take turns.  The frequency is the product of the host's
       // theta^(-2 * 2^k / r) over the set bits k of i (at most seven fp64
-      // products, ~1e-15 relative): an fp64 exp2 and division per element
-      // took ~3.5 us of the 256-sequence epilogue.
+      // products, ~1e-15 relative) instead of an fp64 exp2 and division per
+      // element (0.6 us of the 256-sequence epilogue).
       double freq = 1.0;
 #pragma unroll
       for (int k = 0; k < 8; ++k) freq = (i >> k) & 1 ? freq * a.freq_pow2[k] : freq;
@@ -854,9 +854,10 @@ __global__ __launch_bounds__(kOProjOneThreads) void oproj_one_kernel(OProjArgs a
 // sequences per workgroup: sequences 2i and 2i + 1 own the two 64-byte
 // halves of every 128-byte line of their partials, so this workgroup reads
 // whole lines that no other workgroup touches, where one workgroup per
-// sequence fetched each line twice, on two CUs (256 x 5120: 11.5 against
-// 17.1 us, event-timed).  In each group of eight threads, thread q takes
-// sequence 2i + q / 4 and features 4 (q % 4) .. +3 of a 16-feature piece.
+// sequence fetched each line twice, on two CUs (256 x 5120: 10.6 against
+// 14.4 us in kernel traces).  In each group of eight threads, thread q
+// takes sequence 2i + q / 4 and features 4 (q % 4) .. +3 of a 16-feature
+// piece.
 template <int kSlots>
 __global__ __launch_bounds__(kOProjOneThreads) void oproj_pair_kernel(OProjArgs a) {
   constexpr int kGroups = 2 * kOProjOneFeatures / 4;  // groups of four features per thread, at most
