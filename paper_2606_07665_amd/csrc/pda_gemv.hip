@@ -684,42 +684,61 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
     for (int j = 0; j < E; ++j) v[j] = v[j] * inv * bf16_to_f32(wn_h[j]);
   }
   if ((is_q || is_k) && a.rotary_dim > 0) {
-#pragma unroll
-    for (int j = 0; j < E; ++j) s[lane + 64 * j] = v[j];
-    __syncthreads();
     const int r = a.rotary_dim;
     constexpr double kInvTwoPi = 0.15915494309189535;
-#pragma unroll
-    for (int j = 0; j < E; ++j) {
-      const int e = lane + 64 * j;
-      if (e >= r) continue;
-      int i, partner;
-      bool first;
-      if (a.interleaved) {
-        i = e >> 1;
-        partner = e ^ 1;
-        first = (e & 1) == 0;
-      } else {
-        first = e < r / 2;
-        i = first ? e : e - r / 2;
-        partner = first ? e + r / 2 : e - r / 2;
-      }
-      // the angle p * theta^(-2i/r), in turns, in fp64 (positions reach 10^5
-      // and more, where an fp32 angle would already be off by ~10^-2 rad);
-      // its fraction in [-1/2, 1/2] goes to the hardware sine and cosine,
-      // which take turns.  The frequency is the product of the host's
-      // theta^(-2 * 2^k / r) over the set bits k of i (at most seven fp64
-      // products, ~1e-15 relative) instead of an fp64 exp2 and division per
-      // element (0.6 us of the 256-sequence epilogue).
+    // the angle p * theta^(-2i/r), in turns, in fp64 (positions reach 10^5
+    // and more, where an fp32 angle would already be off by ~10^-2 rad);
+    // its fraction in [-1/2, 1/2] goes to the hardware sine and cosine,
+    // which take turns.  The frequency is the product of the host's
+    // theta^(-2 * 2^k / r) over the set bits k of i (at most seven fp64
+    // products, ~1e-15 relative) instead of an fp64 exp2 and division per
+    // element (0.6 us of the 256-sequence epilogue).
+    auto angle = [&](int i, float& sn, float& c) __attribute__((always_inline)) {
       double freq = 1.0;
 #pragma unroll
       for (int k = 0; k < 8; ++k) freq = (i >> k) & 1 ? freq * a.freq_pow2[k] : freq;
       const double turns = static_cast<double>(pos) * freq * kInvTwoPi;
       const float frac = static_cast<float>(turns - __builtin_rint(turns));
-      const float sn = __builtin_amdgcn_sinf(frac);
-      const float c = __builtin_amdgcn_cosf(frac);
-      const float other = s[partner];
-      v[j] = first ? v[j] * c - other * sn : v[j] * c + other * sn;
+      sn = __builtin_amdgcn_sinf(frac);
+      c = __builtin_amdgcn_cosf(frac);
+    };
+    if (E % 2 == 0 && !a.interleaved && r == D) {
+      // rotation of the whole head in halves: the partner of element
+      // lane + 64 j (j < E / 2) is lane + 64 (j + E / 2), in this lane, at
+      // the same angle, so the pair turns in registers with one angle
+      // (the same arithmetic as the exchange below)
+#pragma unroll
+      for (int j = 0; j < E / 2; ++j) {
+        float sn, c;
+        angle(lane + 64 * j, sn, c);
+        const float x0 = v[j], x1 = v[j + E / 2];
+        v[j] = x0 * c - x1 * sn;
+        v[j + E / 2] = x1 * c + x0 * sn;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < E; ++j) s[lane + 64 * j] = v[j];
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const int e = lane + 64 * j;
+        if (e >= r) continue;
+        int i, partner;
+        bool first;
+        if (a.interleaved) {
+          i = e >> 1;
+          partner = e ^ 1;
+          first = (e & 1) == 0;
+        } else {
+          first = e < r / 2;
+          i = first ? e : e - r / 2;
+          partner = first ? e + r / 2 : e - r / 2;
+        }
+        float sn, c;
+        angle(i, sn, c);
+        const float other = s[partner];
+        v[j] = first ? v[j] * c - other * sn : v[j] * c + other * sn;
+      }
     }
   }
 
