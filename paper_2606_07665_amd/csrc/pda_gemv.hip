@@ -715,6 +715,20 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
         v[j] = x0 * c - x1 * sn;
         v[j + E / 2] = x1 * c + x0 * sn;
       }
+    } else if (a.interleaved) {
+      // interleaved pairs (e, e ^ 1): the partner is the neighbouring lane,
+      // same register, fetched with a DPP swap of adjacent lanes (every
+      // lane takes part, before the range test)
+#pragma unroll
+      for (int j = 0; j < E; ++j) {
+        const float other = __builtin_bit_cast(
+            float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v[j]), 0xB1, 0xF, 0xF, false));
+        const int e = lane + 64 * j;
+        if (e >= r) continue;
+        float sn, c;
+        angle(e >> 1, sn, c);
+        v[j] = (e & 1) == 0 ? v[j] * c - other * sn : v[j] * c + other * sn;
+      }
     } else {
 #pragma unroll
       for (int j = 0; j < E; ++j) s[lane + 64 * j] = v[j];
@@ -723,17 +737,10 @@ __global__ __launch_bounds__(64) void prelude_epilogue(PreludeArgs a) {
       for (int j = 0; j < E; ++j) {
         const int e = lane + 64 * j;
         if (e >= r) continue;
-        int i, partner;
-        bool first;
-        if (a.interleaved) {
-          i = e >> 1;
-          partner = e ^ 1;
-          first = (e & 1) == 0;
-        } else {
-          first = e < r / 2;
-          i = first ? e : e - r / 2;
-          partner = first ? e + r / 2 : e - r / 2;
-        }
+        // a partial rotation in halves: pairs (e, e + r / 2), across lanes
+        const bool first = e < r / 2;
+        const int i = first ? e : e - r / 2;
+        const int partner = first ? e + r / 2 : e - r / 2;
         float sn, c;
         angle(i, sn, c);
         const float other = s[partner];
